@@ -1,0 +1,296 @@
+/*
+ * Plain CPU oracle for the MADDNESS-style encode + lookup-accumulate path
+ * studied in "Look-ups are not (yet) all you need for deep learning
+ * inference" (McCarter & Dronen).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the tests, the smoke check and the CPU-baseline leg
+ * of the benchmark do.  It shares no code, header, table or helper with the
+ * HIP path.
+ *
+ * Style: scalar loops in the order the method states them, double precision
+ * wherever the method leaves the precision open, no blocking, no fusion and
+ * no reordering.  OpenMP splits the independent rows across host threads and
+ * never changes the order of any sum.  Build with
+ *     gcc -O2 -std=c99 -fopenmp -ffp-contract=off -fno-fast-math -fPIC -shared
+ * so that no multiply-add is contracted.
+ *
+ * Readings of points the paper leaves open (numbered as in the design notes):
+ *   R1  a tree node sends x right iff x > threshold (strict; ties and NaN go
+ *       left).
+ *   R2  one split dimension per (codebook, level), a global column of A.
+ *   R3  node (t, i) of codebook c is thresholds[c*15 + 2^t - 1 + i]; the root
+ *       decision is the most significant bit of the 4-bit index.
+ *   R5  8-bit block floating point: table entry = scale_c * q + offset_c with
+ *       q an int8 and scale_c an exact power of two per codebook.
+ *   R6  quantizer: offset = midrange, exponent = the smallest that fits every
+ *       code in [-127, 127] (no clipping), raised to within `cap` of the
+ *       largest exponent so the int32 sum stays exact in fp32.
+ *   R9  y = fl32( float(acc) * 2^e_min + bias32 ), one rounding (fmaf), with
+ *       bias32 = fl32( sum_c offset_c accumulated in double, c ascending ).
+ *   R10 unquantized mode: y = (((0 + T_0) + T_1) + ...) in fp32, c ascending.
+ *
+ * Every entry point returns 0 on success and a negative code on a violated
+ * precondition (it never aborts): -1 bad size / pointer, -2 a scale that is
+ * not an exact normal power of two, -3 an accumulator that could overflow
+ * int32, -4 an out-of-range split dimension.
+ */
+#include <stdint.h>
+#include <stddef.h>
+#include <math.h>
+#include <stdlib.h>
+
+#define ORACLE_K 16      /* prototypes per codebook: 2^4 leaves         */
+#define ORACLE_LEVELS 4  /* "exactly 4 comparisons" per subvector, §2.1 */
+#define ORACLE_NODES 15  /* internal nodes of a balanced 4-level tree   */
+
+int oracle_version(void) { return 1; }
+
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/*
+ * Encoding function (§1: each subvector is mapped to the index of one of K
+ * prototypes, a log2(K)-bit integer; §1 and §2.1: MADDNESS does it with a
+ * balanced binary regression tree, exactly 4 comparisons for K = 16).
+ * Walk the tree of codebook c from the root: at level t the current node is
+ * i (0 <= i < 2^t), its threshold is thresholds[c][2^t - 1 + i], and the
+ * compared value is A[n][split[c][t]].  The next node is 2i + bit.
+ */
+int oracle_encode(const float* A, int64_t N, int32_t D, int64_t lda,
+                  const int32_t* split, const float* thr, int32_t C,
+                  uint8_t* idx)
+{
+    if (N < 0 || D <= 0 || C <= 0 || lda < D) return -1;
+    if (N > 0 && (!A || !split || !thr || !idx)) return -1;
+    for (int64_t j = 0; j < (int64_t)C * ORACLE_LEVELS; ++j)
+        if (split[j] < 0 || split[j] >= D) return -4;
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        const float* row = A + n * lda;
+        for (int32_t c = 0; c < C; ++c) {
+            int i = 0;                                   /* node within level */
+            for (int t = 0; t < ORACLE_LEVELS; ++t) {
+                float x = row[split[c * ORACLE_LEVELS + t]];
+                float v = thr[c * ORACLE_NODES + ((1 << t) - 1) + i];
+                int bit = (x > v) ? 1 : 0;               /* R1 */
+                i = 2 * i + bit;
+            }
+            idx[n * C + c] = (uint8_t)i;
+        }
+    }
+    return 0;
+}
+
+/* Block exponent of one scale: scale = 2^e exactly, with scale a normal
+ * fp32 number (R5).  Returns 0 and writes e, or -2. */
+int oracle_block_exponent(float scale, int32_t* e)
+{
+    if (!(scale > 0.0f) || isinf(scale)) return -2;
+    int x;
+    float m = frexpf(scale, &x);                         /* scale = m 2^x, m in [0.5,1) */
+    if (m != 0.5f) return -2;
+    if (x - 1 < -126) return -2;                         /* subnormal scales rejected */
+    *e = x - 1;
+    return 0;
+}
+
+/* Dequantization constants shared by every output (R5, R9): per-codebook
+ * shifts sh_c = e_c - e_min, e_min, and bias32.  Also checks that the int32
+ * accumulator cannot overflow: 127 * sum_c 2^sh_c < 2^31. */
+int oracle_dequant_params(const float* scale, const float* offset, int32_t C,
+                          int32_t* sh, int32_t* e_min, float* bias32)
+{
+    if (C <= 0 || !scale || !offset || !sh || !e_min || !bias32) return -1;
+    int32_t emin = 1000;
+    for (int32_t c = 0; c < C; ++c) {
+        int32_t e;
+        if (oracle_block_exponent(scale[c], &e) != 0) return -2;
+        sh[c] = e;
+        if (e < emin) emin = e;
+    }
+    double bound = 0.0;
+    for (int32_t c = 0; c < C; ++c) {
+        sh[c] -= emin;
+        if (sh[c] > 30) return -3;
+        bound += 127.0 * ldexp(1.0, sh[c]);
+    }
+    if (bound >= 2147483648.0) return -3;
+    double s = 0.0;
+    for (int32_t c = 0; c < C; ++c) s += (double)offset[c];
+    *e_min = emin;
+    *bias32 = (float)s;
+    return 0;
+}
+
+/*
+ * Lookup-accumulate (§1: the approximate inner product is the sum over
+ * codebooks of the table rows picked by the indices; 8-bit block floating
+ * point tables).  With table entry = 2^e_c q + o_c,
+ *     sum_c (2^e_c q_c + o_c) = 2^e_min * sum_c (q_c << sh_c) + sum_c o_c,
+ * so the codebook sum is an exact integer acc and the float work is one
+ * rounding at the end (R9).  lut is [C][16][M] int8, idx is [N][C].
+ * acc_out and y_out may each be NULL (not both).
+ */
+int oracle_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C,
+                          const int8_t* lut, const float* scale,
+                          const float* offset, int32_t M,
+                          int32_t* acc_out, float* y_out)
+{
+    if (N < 0 || C <= 0 || M <= 0) return -1;
+    if (!acc_out && !y_out) return -1;
+    if (N > 0 && (!idx || !lut || !scale || !offset)) return -1;
+    int32_t* sh = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
+    if (!sh) return -1;
+    int32_t emin;
+    float bias32;
+    int rc = oracle_dequant_params(scale, offset, C, sh, &emin, &bias32);
+    if (rc != 0) { free(sh); return rc; }
+    const float step = ldexpf(1.0f, emin);
+    for (int64_t n = 0; n < N; ++n)
+        for (int32_t c = 0; c < C; ++c)
+            if (idx[n * C + c] >= ORACLE_K) { free(sh); return -1; }
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        for (int32_t m = 0; m < M; ++m) {
+            int64_t acc = 0;
+            for (int32_t c = 0; c < C; ++c) {
+                int k = idx[n * C + c];
+                int64_t q = lut[((int64_t)c * ORACLE_K + k) * M + m];
+                acc += q * ((int64_t)1 << sh[c]);
+            }
+            if (acc_out) acc_out[n * M + m] = (int32_t)acc;
+            if (y_out) y_out[n * M + m] = fmaf((float)acc, step, bias32);
+        }
+    }
+    free(sh);
+    return 0;
+}
+
+/*
+ * Unquantized mode: the table holds fp32 entries T[c][k][m] and the sum over
+ * codebooks is taken in fp32, c ascending, starting from +0 (R10).
+ */
+int oracle_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C,
+                              const float* lut, int32_t M, float* y_out)
+{
+    if (N < 0 || C <= 0 || M <= 0) return -1;
+    if (N > 0 && (!idx || !lut || !y_out)) return -1;
+    for (int64_t n = 0; n < N; ++n)
+        for (int32_t c = 0; c < C; ++c)
+            if (idx[n * C + c] >= ORACLE_K) return -1;
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        for (int32_t m = 0; m < M; ++m) {
+            float s = 0.0f;
+            for (int32_t c = 0; c < C; ++c) {
+                int k = idx[n * C + c];
+                s = s + lut[((int64_t)c * ORACLE_K + k) * M + m];
+            }
+            y_out[n * M + m] = s;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Lookup table T = P B (§2.2): P is the prototype matrix, one block of 16
+ * rows per codebook ([C][16][D], zero outside the codebook's subspace), B is
+ * the weight matrix [D][M].  Each entry is a double sum over d ascending of
+ * exact products of fp32 values.
+ */
+int oracle_build_table(const float* P, const float* B, int32_t C, int32_t D,
+                       int32_t M, double* T)
+{
+    if (C <= 0 || D <= 0 || M <= 0 || !P || !B || !T) return -1;
+    int64_t r;
+#pragma omp parallel for schedule(static)
+    for (r = 0; r < (int64_t)C * ORACLE_K; ++r) {
+        for (int32_t m = 0; m < M; ++m) {
+            double s = 0.0;
+            for (int32_t d = 0; d < D; ++d)
+                s += (double)P[r * D + d] * (double)B[(int64_t)d * M + m];
+            T[r * M + m] = s;
+        }
+    }
+    return 0;
+}
+
+/* Largest cap with 127 * C * 2^cap < 2^24 (R6): keeps the int32 sum of any
+ * C codes, each shifted by at most cap, exactly representable in fp32. */
+int oracle_exponent_cap(int32_t C)
+{
+    if (C <= 0 || 127.0 * C >= 16777216.0) return -1;
+    int cap = 0;
+    while (127.0 * C * ldexp(1.0, cap + 1) < 16777216.0) ++cap;
+    return cap;
+}
+
+/*
+ * 8-bit block floating point quantization of T (§1; reading R6).
+ * Per codebook c over its 16 x M entries: offset o_c = fl32 of the midrange,
+ * r_c = max |T - o_c| (in double), e_c = the smallest e in [-126, 127] with
+ * r_c <= 127 * 2^e.  Then e_c is raised to at least max_c e_c - cap, and
+ * q = round-half-even((T - o_c) / 2^e_c), which always lies in [-127, 127].
+ */
+int oracle_quantize_table(const double* T, int32_t C, int32_t M,
+                          int8_t* lut, float* scale, float* offset)
+{
+    if (C <= 0 || M <= 0 || !T || !lut || !scale || !offset) return -1;
+    int cap = oracle_exponent_cap(C);
+    if (cap < 0) return -1;
+    const int64_t per = (int64_t)ORACLE_K * M;
+    int32_t emax = -126;
+    int32_t* ec = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
+    if (!ec) return -1;
+    for (int32_t c = 0; c < C; ++c) {
+        const double* t = T + c * per;
+        double lo = t[0], hi = t[0];
+        for (int64_t j = 1; j < per; ++j) {
+            if (t[j] < lo) lo = t[j];
+            if (t[j] > hi) hi = t[j];
+        }
+        float o = (float)((lo + hi) / 2.0);
+        double r = 0.0;
+        for (int64_t j = 0; j < per; ++j) {
+            double a = fabs(t[j] - (double)o);
+            if (a > r) r = a;
+        }
+        int32_t e = -126;
+        while (e < 127 && r > 127.0 * ldexp(1.0, e)) ++e;
+        offset[c] = o;
+        ec[c] = e;
+        if (e > emax) emax = e;
+    }
+    for (int32_t c = 0; c < C; ++c) {
+        int32_t e = ec[c];
+        if (e < emax - cap) e = emax - cap;
+        const double* t = T + c * per;
+        const double o = (double)offset[c];
+        for (int64_t j = 0; j < per; ++j) {
+            double q = nearbyint((t[j] - o) / ldexp(1.0, e));
+            if (q > 127.0 || q < -127.0) { free(ec); return -3; }  /* cannot happen; guard */
+            lut[c * per + j] = (int8_t)q;
+        }
+        scale[c] = ldexpf(1.0f, e);
+    }
+    free(ec);
+    return 0;
+}
+
+/* Unquantized table: each T entry rounded to fp32 (round to nearest even). */
+int oracle_round_table_f32(const double* T, int64_t n, float* out)
+{
+    if (n < 0 || (n > 0 && (!T || !out))) return -1;
+    for (int64_t j = 0; j < n; ++j) out[j] = (float)T[j];
+    return 0;
+}

@@ -1,0 +1,23 @@
+"""MI355X (gfx950) inference path of the MADDNESS-style approximate matrix
+product studied in McCarter & Dronen, "Look-ups are not (yet) all you need for
+deep learning inference": tree encoding plus lookup-accumulate over 8-bit
+block floating point (or fp32) tables, as hand-written HIP kernels behind the
+C ABI of include/maddness.h.
+
+The entry points load lazily, so ``paper_2207_05808_amd.workloads`` (the
+seeded input generator) imports without torch or the HIP library.
+"""
+_BINDING = ("encode", "lut_accumulate", "lut_accumulate_f32", "matmul", "matmul_f32",
+            "build_lut", "build_lut_f32", "version")
+
+__all__ = list(_BINDING) + ["MaddnessError"]
+
+
+def __getattr__(name):
+    if name in _BINDING:
+        from . import binding
+        return getattr(binding, name)
+    if name == "MaddnessError":
+        from ._lib import MaddnessError
+        return MaddnessError
+    raise AttributeError(name)

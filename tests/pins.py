@@ -1,0 +1,431 @@
+"""Checks that pin the CPU oracle to facts other than itself.
+
+Each check takes an oracle object (the default build, or a build with a
+planted mistake) and raises AssertionError when the oracle disagrees with
+what the paper or the mathematics fixes.  The expected values come from
+independent computations: brute-force enumeration, a textbook binary search,
+a one-hot dense integer product, exact rational arithmetic (fractions), a
+correctly rounded sum (math.fsum), or a hand-worked example in tests/golden.
+"""
+from __future__ import annotations
+
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+
+K, LEVELS, NODES = 16, 4, 15
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+U32 = 2.0 ** -24
+U64 = 2.0 ** -53
+
+
+def gamma(n, u):
+    return n * u / (1 - n * u)
+
+
+# ------------------------------------------------------------------ encode
+def brute_force_leaf(A, split, thr):
+    """For every (row, codebook) test all 16 leaves against the path
+    predicate: leaf k is reached iff, at every level t, the comparison of
+    A[n, split[c,t]] with the threshold of the node on k's path (node number
+    k >> (4 - t) within level t) gives bit 3 - t of k.  Returns the unique
+    leaf, asserting that exactly one leaf satisfies the predicate."""
+    N, C = A.shape[0], split.shape[0]
+    ok = np.ones((N, C, K), dtype=bool)
+    for k in range(K):
+        for t in range(LEVELS):
+            node = (1 << t) - 1 + (k >> (LEVELS - t))
+            bit = (k >> (LEVELS - 1 - t)) & 1
+            x = A[:, split[:, t]]                       # [N, C]
+            v = thr[np.arange(C), node][None, :]        # [1, C]
+            ok[:, :, k] &= ((x > v) == bool(bit))
+    count = ok.sum(axis=2)
+    assert np.all(count == 1), "leaf predicate not satisfied by exactly one leaf"
+    return ok.argmax(axis=2).astype(np.uint8)
+
+
+def bst_heap(sorted15):
+    """Breadth-first listing of the balanced binary search tree over 15 sorted
+    values (root = median, recursively): the heap layout of a search tree."""
+    out, queue = [], [(0, 15)]
+    while queue:
+        lo, hi = queue.pop(0)
+        mid = (lo + hi) // 2
+        out.append(sorted15[mid])
+        if hi - lo > 1:
+            queue.append((lo, mid))
+            queue.append((mid + 1, hi))
+    assert len(out) == 15
+    return np.array(out, dtype=np.float32)
+
+
+def check_encode_brute_force(orc, seed=0):
+    rng = np.random.default_rng(seed)
+    for (N, D, C) in [(300, 64, 4), (200, 576, 32), (150, 7, 9), (64, 1, 3)]:
+        A = rng.standard_normal((N, D), dtype=np.float32)
+        split = rng.integers(0, D, size=(C, LEVELS)).astype(np.int32)
+        thr = rng.standard_normal((C, NODES), dtype=np.float32)
+        # a share of exact ties with the compared thresholds
+        for n in range(0, N, 5):
+            c = n % C
+            A[n, split[c, 0]] = thr[c, 0]
+        idx = orc.encode(A, split, thr)
+        assert idx.shape == (N, C) and idx.dtype == np.uint8
+        assert int(idx.max()) < K, "index outside [0, 16)"
+        assert np.array_equal(idx, brute_force_leaf(A, split, thr)), "encode != brute force"
+        # the same rows inside a wider array (row stride > D)
+        wide = np.zeros((N, D + 3), dtype=np.float32)
+        wide[:, :D] = A
+        wide[:, D:] = np.nan
+        assert np.array_equal(orc.encode(wide[:, :D], split, thr), idx), "row stride ignored"
+
+
+def check_encode_search_tree(orc, seed=1):
+    """One column per codebook, all levels on it, thresholds of a binary search
+    tree: the leaf is the number of thresholds strictly below x, i.e.
+    numpy.searchsorted(s, x, side='left'), ties going left."""
+    rng = np.random.default_rng(seed)
+    C, N = 6, 4000
+    s = np.sort(rng.standard_normal((C, NODES), dtype=np.float32), axis=1)
+    s[0] = np.arange(-7, 8, dtype=np.float32)            # integer grid: exact ties
+    s[1, 7] = 0.0                                          # a zero threshold (against +-0 inputs)
+    s = np.sort(s, axis=1)
+    thr = np.stack([bst_heap(s[c]) for c in range(C)])
+    split = np.repeat(np.arange(C, dtype=np.int32)[:, None], LEVELS, axis=1)
+    A = rng.standard_normal((N, C), dtype=np.float32) * 2
+    A[::3, 0] = rng.integers(-8, 9, size=A[::3, 0].shape).astype(np.float32)
+    A[1::9, 1] = -0.0
+    A[2::9, 1] = 0.0
+    A[3::17, :] = np.inf
+    A[4::17, :] = -np.inf
+    idx = orc.encode(A, split, thr)
+    for c in range(C):
+        ref = np.searchsorted(s[c], A[:, c], side="left")
+        assert np.array_equal(idx[:, c], ref), f"codebook {c}: encode != searchsorted"
+
+
+def check_encode_nan(orc):
+    """Comparisons with NaN are false: a NaN input takes the 0 branch at every level."""
+    D, C = 8, 3
+    split = np.array([[0, 1, 2, 3], [4, 4, 4, 4], [7, 6, 5, 0]], dtype=np.int32)
+    thr = np.full((C, NODES), -1e30, dtype=np.float32)      # every finite value goes right
+    A = np.zeros((4, D), dtype=np.float32)
+    A[1, :] = np.nan
+    A[2, 4] = np.nan
+    idx = orc.encode(A, split, thr)
+    assert idx[0].tolist() == [15, 15, 15]
+    assert idx[1].tolist() == [0, 0, 0]
+    assert idx[2].tolist() == [15, 0, 15]
+
+
+def check_encode_permutation(orc, seed=2):
+    """Permuting the columns of A together with the split columns leaves the
+    indices unchanged (split columns are global indices)."""
+    rng = np.random.default_rng(seed)
+    N, D, C = 500, 40, 5
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, LEVELS)).astype(np.int32)
+    thr = rng.standard_normal((C, NODES), dtype=np.float32)
+    perm = rng.permutation(D)
+    inv = np.argsort(perm)
+    A2 = A[:, perm]                         # column j of A2 is column perm[j] of A
+    split2 = inv[split].astype(np.int32)    # so old column d is now at inv[d]
+    assert np.array_equal(orc.encode(A, split, thr), orc.encode(A2, split2, thr))
+
+
+def load_golden_tree_walk():
+    """tests/golden/tree_walk_tiny.txt: a hand-worked encoding example."""
+    path = os.path.join(GOLDEN, "tree_walk_tiny.txt")
+    sections, cur = {}, None
+    with open(path) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            if line.startswith("[") and line.endswith("]"):
+                cur = line[1:-1]
+                sections[cur] = []
+            else:
+                sections[cur].append([float(v) for v in line.split()])
+    split = np.array(sections["split"], dtype=np.int32)
+    thr = np.array(sections["thresholds"], dtype=np.float32)
+    A = np.array(sections["rows"], dtype=np.float32)
+    idx = np.array(sections["expected_idx"], dtype=np.uint8)
+    return A, split, thr, idx
+
+
+def check_encode_golden(orc):
+    A, split, thr, idx = load_golden_tree_walk()
+    assert np.array_equal(orc.encode(A, split, thr), idx), "hand-worked tree walks differ"
+
+
+# -------------------------------------------------------------- accumulate
+def one_hot(idx):
+    N, C = idx.shape
+    G = np.zeros((N, C * K), dtype=np.int64)
+    G[np.arange(N)[:, None], np.arange(C)[None, :] * K + idx.astype(np.int64)] = 1
+    return G
+
+
+def exponents(scale):
+    m, e = np.frexp(scale.astype(np.float64))
+    assert np.all(m == 0.5)
+    return (e - 1).astype(np.int64)
+
+
+def check_one_hot_identity(orc, seed=3):
+    """The lookup sum equals the dense product of the one-hot encoder output G
+    (N x 16C) with the stacked, shifted code table (16C x M), in int64."""
+    rng = np.random.default_rng(seed)
+    for (N, C, M, maxsh) in [(200, 4, 10, 3), (100, 32, 64, 5), (64, 7, 3, 10), (50, 1, 1, 0)]:
+        idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+        lut = rng.integers(-127, 128, size=(C, K, M)).astype(np.int8)
+        e = rng.integers(-3, -3 + maxsh + 1, size=C)
+        scale = np.ldexp(np.float32(1), e.astype(np.int32)).astype(np.float32)
+        offset = rng.standard_normal(C).astype(np.float32)
+        acc, _ = orc.lut_accumulate(idx, lut, scale, offset)
+        ex = exponents(scale)
+        Q = (lut.astype(np.int64) * (2 ** (ex - ex.min()))[:, None, None]).reshape(C * K, M)
+        assert np.array_equal(acc.astype(np.int64), one_hot(idx) @ Q), "acc != one-hot product"
+
+
+def check_decoder_table(orc, seed=4):
+    """With M = C and q[c][k][m] = k if m == c else 0 (equal scales), the sum
+    reads back the indices: acc[n][m] == idx[n][m]."""
+    rng = np.random.default_rng(seed)
+    N, C = 300, 9
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    lut = np.zeros((C, K, C), dtype=np.int8)
+    for c in range(C):
+        lut[c, :, c] = np.arange(K)
+    acc, _ = orc.lut_accumulate(idx, lut, np.ones(C, np.float32), np.zeros(C, np.float32))
+    assert np.array_equal(acc, idx.astype(np.int32)), "decoder table does not read back indices"
+
+
+def rne32(x: Fraction) -> float:
+    """Round an exact rational to the nearest fp32 (ties to even), finite range."""
+    if x == 0:
+        return 0.0
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = math.floor(math.log2(a.numerator) - math.log2(a.denominator))
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    e = max(e, -126)                        # subnormal spacing below 2^-126
+    ulp = Fraction(2) ** (e - 23)
+    q, r = divmod(a, ulp)
+    q = int(q)
+    if r * 2 > ulp or (r * 2 == ulp and q % 2 == 1):
+        q += 1
+    return sign * float(q * ulp)
+
+
+def check_output_rounding(orc, seed=5):
+    """y is the dequantized sum rounded once: with offsets whose double sum is
+    exact (integers), y == RNE32(acc 2^e_min + RNE32(sum o)) computed in exact
+    rationals, and |y - sum_c (2^e_c q_c + o_c)| obeys the closed-form bound."""
+    rng = np.random.default_rng(seed)
+    N, C, M = 60, 12, 9
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    lut = rng.integers(-127, 128, size=(C, K, M)).astype(np.int8)
+    e = rng.integers(-9, -5, size=C)
+    scale = np.ldexp(np.float32(1), e.astype(np.int32)).astype(np.float32)
+    offset = rng.integers(-2 ** 20, 2 ** 20, size=C).astype(np.float32)
+    acc, y = orc.lut_accumulate(idx, lut, scale, offset)
+    S = sum(Fraction(float(o)) for o in offset)
+    bias = rne32(S)
+    emin = int(e.min())
+    for n in range(N):
+        for m in range(M):
+            exact = sum(Fraction(float(scale[c])) * int(lut[c, idx[n, c], m]) for c in range(C))
+            assert Fraction(int(acc[n, m])) * Fraction(2) ** emin == exact, "acc scaling wrong"
+            want = rne32(exact + Fraction(bias))
+            assert float(y[n, m]) == want, f"y[{n},{m}] not the single rounding of its value"
+            deq = exact + S
+            bound = U32 * abs(float(y[n, m])) + abs(float(Fraction(bias) - S))
+            assert abs(float(Fraction(float(y[n, m])) - deq)) <= bound * (1 + 1e-12)
+    # offsets of mixed magnitude: bias32 within the rounding bound of the exact sum
+    offset2 = (rng.standard_normal(C) * 10.0 ** rng.integers(-6, 6, size=C)).astype(np.float32)
+    _, _, b2 = orc.dequant_params(scale, offset2)
+    S2 = sum(Fraction(float(o)) for o in offset2)
+    tol = U32 * abs(float(S2)) + gamma(C, U64) * float(np.abs(offset2.astype(np.float64)).sum())
+    assert abs(float(Fraction(float(b2)) - S2)) <= tol * (1 + 1e-12)
+
+
+def check_scale_linearity(orc, seed=6):
+    """Doubling every scale doubles acc * 2^e_min exactly (acc itself unchanged);
+    shifting one codebook's exponent by +1 doubles its share of acc."""
+    rng = np.random.default_rng(seed)
+    N, C, M = 100, 5, 8
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    lut = rng.integers(-127, 128, size=(C, K, M)).astype(np.int8)
+    scale = np.ldexp(np.float32(1), rng.integers(-4, 0, size=C).astype(np.int32)).astype(np.float32)
+    off = np.zeros(C, np.float32)
+    a1, y1 = orc.lut_accumulate(idx, lut, scale, off)
+    a2, y2 = orc.lut_accumulate(idx, lut, scale * 2, off)
+    assert np.array_equal(a1, a2) and np.array_equal(y2, y1 * 2)
+    one = np.zeros((C, K, M), np.int8)
+    one[2] = lut[2]
+    b1, _ = orc.lut_accumulate(idx, one, scale, off)
+    s3 = scale.copy()
+    s3[2] *= 2
+    b2, _ = orc.lut_accumulate(idx, one, s3, off)
+    ex = exponents(scale)
+    ex3 = exponents(s3)
+    # codebook 2's contribution in units of each call's own 2^e_min
+    assert np.array_equal(b2.astype(np.int64) * 2 ** int(ex3.min()),
+                          2 * b1.astype(np.int64) * 2 ** int(ex.min()))
+
+
+def check_f32_order(orc):
+    """fp32 tables are summed in codebook order from +0: ((0 + 1e8) + 1) - 1e8
+    is 0 in fp32, while other orders give 1."""
+    lut = np.zeros((3, K, 1), np.float32)
+    lut[0, :, 0] = 1e8
+    lut[1, :, 0] = 1.0
+    lut[2, :, 0] = -1e8
+    y = orc.lut_accumulate_f32(np.zeros((1, 3), np.uint8), lut)
+    assert y[0, 0] == 0.0
+    lut2 = lut[[0, 2, 1]]
+    assert orc.lut_accumulate_f32(np.zeros((1, 3), np.uint8), lut2)[0, 0] == 1.0
+
+
+def exact_table(P, B):
+    """T = P B entry by entry with math.fsum (correctly rounded double)."""
+    C, _, D = P.shape
+    M = B.shape[1]
+    T = np.zeros((C, K, M))
+    Pd, Bd = P.astype(np.float64), B.astype(np.float64)
+    for c in range(C):
+        for k in range(K):
+            for m in range(M):
+                T[c, k, m] = math.fsum(Pd[c, k] * Bd[:, m])
+    return T
+
+
+def check_table_build(orc, seed=7):
+    """T = P B: exact for integer data; within gamma_D sum |P B| otherwise."""
+    rng = np.random.default_rng(seed)
+    C, D, M = 3, 12, 5
+    Pi = rng.integers(-50, 50, size=(C, K, D)).astype(np.float32)
+    Bi = rng.integers(-50, 50, size=(D, M)).astype(np.float32)
+    T = orc.build_table(Pi, Bi)
+    assert np.array_equal(T, np.einsum("ckd,dm->ckm", Pi.astype(np.int64), Bi.astype(np.int64)))
+    P = rng.standard_normal((C, K, D), dtype=np.float32)
+    B = rng.standard_normal((D, M), dtype=np.float32)
+    T = orc.build_table(P, B)
+    ref = exact_table(P, B)
+    bnd = gamma(D, U64) * np.einsum("ckd,dm->ckm", np.abs(P.astype(np.float64)), np.abs(B.astype(np.float64)))
+    assert np.all(np.abs(T - ref) <= bnd + 1e-300)
+
+
+def check_quantizer(orc, seed=8):
+    """Block floating point codes: power-of-two scales, |q| <= 127, every
+    dequantized entry within half a step of T, the smallest exponent that fits
+    (unless raised to the common floor), and the int32 sum exact in fp32."""
+    rng = np.random.default_rng(seed)
+    C, M = 6, 11
+    T = rng.standard_normal((C, K, M)) * (10.0 ** np.arange(C))[:, None, None]
+    T[3] = 0.25                                   # a constant codebook
+    lut, scale, offset = orc.quantize_table(T)
+    ex = exponents(scale)
+    cap = orc.exponent_cap(C)
+    assert 127 * C * 2 ** cap < 2 ** 24 <= 127 * C * 2 ** (cap + 1)
+    assert int(ex.max() - ex.min()) <= cap
+    assert np.all(np.abs(lut.astype(np.int64)) <= 127)
+    deq = scale.astype(np.float64)[:, None, None] * lut + offset.astype(np.float64)[:, None, None]
+    assert np.all(np.abs(deq - T) <= scale.astype(np.float64)[:, None, None] / 2 * (1 + 1e-12))
+    assert np.all(lut[3] == 0) and offset[3] == np.float32(0.25)
+    floor_e = int(ex.max()) - cap
+    for c in range(C):
+        if ex[c] > floor_e and c != 3:
+            r = np.abs(T[c] - np.float64(offset[c])).max()
+            assert r > 127 * 2.0 ** (ex[c] - 1), f"codebook {c}: exponent not minimal"
+        lo, hi = T[c].min(), T[c].max()
+        assert offset[c] == np.float32((lo + hi) / 2)
+
+
+def check_f32_reconstruction(orc, seed=9):
+    """Unquantized mode against the fp64 reconstruction A_hat B, A_hat the
+    sum of the selected prototypes: |y - A_hat B| <= gamma_C^(32) sum|T32|
+    + sum_c |T32 - T| with T the exact table entries (rigorous bound)."""
+    rng = np.random.default_rng(seed)
+    N, C, L, M = 40, 6, 3, 7
+    D = C * L
+    P = np.zeros((C, K, D), np.float32)
+    for c in range(C):
+        P[c, :, c * L:(c + 1) * L] = rng.standard_normal((K, L), dtype=np.float32)
+    B = rng.standard_normal((D, M), dtype=np.float32)
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = (np.arange(C)[:, None] * L + rng.integers(0, L, size=(C, LEVELS))).astype(np.int32)
+    thr = rng.standard_normal((C, NODES), dtype=np.float32)
+    T32 = orc.build_lut_f32(P, B)
+    idx, y = orc.matmul_f32(A, split, thr, T32)
+    Tx = exact_table(P, B)
+    for n in range(N):
+        Ahat = sum(P[c, idx[n, c]].astype(np.float64) for c in range(C))
+        for m in range(M):
+            ref = math.fsum(Ahat * B[:, m].astype(np.float64))
+            t32 = np.array([T32[c, idx[n, c], m] for c in range(C)], np.float64)
+            tx = np.array([Tx[c, idx[n, c], m] for c in range(C)])
+            bound = gamma(C, U32) * np.abs(t32).sum() + np.abs(t32 - tx).sum() + 4 * U64 * abs(ref)
+            assert abs(float(y[n, m]) - ref) <= bound, f"({n},{m}) outside reconstruction bound"
+
+
+def check_quantized_reconstruction(orc, seed=10):
+    """Quantized end to end: |y - A_hat B| <= sum_c 2^e_c / 2 (code rounding)
+    + |bias32 - sum o| + 2^-24 |y| + table and reconstruction rounding."""
+    rng = np.random.default_rng(seed)
+    N, C, L, M = 50, 8, 4, 6
+    D = C * L
+    P = np.zeros((C, K, D), np.float32)
+    for c in range(C):
+        P[c, :, c * L:(c + 1) * L] = rng.standard_normal((K, L), dtype=np.float32)
+    B = rng.standard_normal((D, M), dtype=np.float32)
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = (np.arange(C)[:, None] * L + rng.integers(0, L, size=(C, LEVELS))).astype(np.int32)
+    thr = rng.standard_normal((C, NODES), dtype=np.float32)
+    lut, scale, offset = orc.build_quantized_lut(P, B)
+    idx, acc, y = orc.matmul(A, split, thr, lut, scale, offset)
+    _, _, bias = orc.dequant_params(scale, offset)
+    S = math.fsum(offset.astype(np.float64))
+    half = float(np.sum(scale.astype(np.float64))) / 2
+    for n in range(N):
+        Ahat = sum(P[c, idx[n, c]].astype(np.float64) for c in range(C))
+        for m in range(M):
+            ref = math.fsum(Ahat * B[:, m].astype(np.float64))
+            tab = sum(abs(float(x)) for x in (P[c, idx[n, c]].astype(np.float64) * B[:, m] for c in range(C)) for x in x)
+            bound = (half + abs(float(bias) - S) + U32 * abs(float(y[n, m])) + gamma(D, U64) * tab
+                     + 4 * U64 * abs(ref))
+            assert abs(float(y[n, m]) - ref) <= bound * (1 + 1e-9), f"({n},{m}) outside bound"
+
+
+def check_rejects_bad_inputs(orc):
+    from oracle import OracleError
+    idx = np.zeros((2, 2), np.uint8)
+    lut = np.zeros((2, K, 3), np.int8)
+    for bad in ([0.75, 1.0], [3.0, 1.0], [1.0, 2.0 ** 40], [2.0 ** -130, 1.0]):
+        try:
+            orc.lut_accumulate(idx, lut, np.array(bad, np.float32), np.zeros(2, np.float32))
+        except OracleError:
+            continue
+        raise AssertionError(f"scale {bad} accepted")
+    try:
+        orc.encode(np.zeros((1, 4), np.float32), np.array([[0, 1, 2, 4]], np.int32),
+                   np.zeros((1, NODES), np.float32))
+    except OracleError:
+        pass
+    else:
+        raise AssertionError("split column outside [0, D) accepted")
+
+
+ALL_CHECKS = [
+    check_encode_brute_force, check_encode_search_tree, check_encode_nan, check_encode_permutation,
+    check_encode_golden, check_one_hot_identity, check_decoder_table, check_output_rounding,
+    check_scale_linearity, check_f32_order, check_table_build, check_quantizer,
+    check_f32_reconstruction, check_quantized_reconstruction, check_rejects_bad_inputs,
+]

@@ -1,0 +1,56 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and require
+the pin suite to catch every one of them.  This checks that the pins are
+sharp enough: a dropped term, a wrong sign, index or operand fails a pin."""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "maddness_oracle.c")
+
+MUTANTS = [
+    ("ties go right", "int bit = (x > v) ? 1 : 0;", "int bit = (x >= v) ? 1 : 0;"),
+    ("root bit is the LSB", "i = 2 * i + bit;", "i = i + (bit << t);"),
+    ("wrong node numbering", "thr[c * ORACLE_NODES + ((1 << t) - 1) + i]", "thr[c * ORACLE_NODES + t + i]"),
+    ("split table transposed", "row[split[c * ORACLE_LEVELS + t]]", "row[split[t * C + c]]"),
+    ("row stride ignored", "const float* row = A + n * lda;", "const float* row = A + n * D;"),
+    ("shift dropped", "acc += q * ((int64_t)1 << sh[c]);", "acc += q;"),
+    ("table operand transposed", "int64_t q = lut[((int64_t)c * ORACLE_K + k) * M + m];",
+     "int64_t q = lut[((int64_t)k * C + c % ORACLE_K) * M + m];"),
+    ("index table transposed", "int k = idx[n * C + c];\n                int64_t q",
+     "int k = idx[(c * N + n) % (N * C)];\n                int64_t q"),
+    ("bias dropped", "for (int32_t c = 0; c < C; ++c) s += (double)offset[c];",
+     "for (int32_t c = 0; c < C; ++c) s += 0.0 * (double)offset[c];"),
+    ("step off by one", "const float step = ldexpf(1.0f, emin);", "const float step = ldexpf(1.0f, emin + 1);"),
+    ("fp32 sum reversed", "s = s + lut[((int64_t)c * ORACLE_K + k) * M + m];",
+     "s = s + lut[((int64_t)(C - 1 - c) * ORACLE_K + idx[n * C + (C - 1 - c)]) * M + m];"),
+    ("fp32 sum in double", "float s = 0.0f;\n            for (int32_t c = 0; c < C; ++c) {\n                int k",
+     "double s = 0.0;\n            for (int32_t c = 0; c < C; ++c) {\n                int k"),
+    ("weights transposed", "(double)B[(int64_t)d * M + m];", "(double)B[((int64_t)m * D + d) % ((int64_t)D * M)];"),
+    ("codes floored", "double q = nearbyint((t[j] - o) / ldexp(1.0, e));", "double q = floor((t[j] - o) / ldexp(1.0, e));"),
+    ("offset sign", "double q = nearbyint((t[j] - o) / ldexp(1.0, e));", "double q = nearbyint((t[j] + o) / ldexp(1.0, e));"),
+    ("exponent one too large", "        offset[c] = o;\n        ec[c] = e;", "        offset[c] = o;\n        ec[c] = e + 1;"),
+    ("exponent floor ignored", "if (e < emax - cap) e = emax - cap;", "(void)cap;"),
+    ("offset not the midrange", "float o = (float)((lo + hi) / 2.0);", "float o = (float)lo;"),
+]
+
+
+@pytest.mark.parametrize("what,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_planted_mistake_is_caught(tmp_path, what, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site not unique/found: {what}"
+    mut = tmp_path / "mutant.c"
+    mut.write_text(src.replace(old, new))
+    so = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", *oracle.CFLAGS, str(mut), "-o", str(so), "-lm"], check=True)
+    orc = oracle.Oracle(str(so))
+    caught = []
+    for check in pins.ALL_CHECKS:
+        try:
+            check(orc)
+        except (AssertionError, oracle.OracleError) as e:
+            caught.append(check.__name__)
+    assert caught, f"planted mistake '{what}' passed every pin"
