@@ -1,0 +1,172 @@
+/*
+ * maddness.h -- C ABI of the MI355X (gfx950) library for the inference path
+ * of the MADDNESS-style approximate matrix product studied in McCarter &
+ * Dronen, "Look-ups are not (yet) all you need for deep learning inference".
+ *
+ * The product A B (A: N x D activations, B: D x M weights known in advance,
+ * §1) is approximated by product quantization: each row of A is hashed, per
+ * codebook c, to one of K = 16 prototypes by a balanced 4-level binary tree
+ * (§1; §2.1: four comparisons per codebook), and the result is the sum over the C
+ * codebooks of the rows of precomputed tables T_c = P_c B (§1; §2.2) picked
+ * by those indices.  The tables are stored in 8-bit block floating point
+ * (§1): int8 codes with a power-of-two scale and an fp32 offset per codebook.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller.  The
+ *    library keeps no pointer after the call returns; the caller keeps the
+ *    buffers alive until the work on `stream` has completed.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  The
+ *    calls only enqueue work on it: no host synchronisation.  Only
+ *    maddness_matmul / maddness_matmul_f32 may allocate (stream-ordered) a
+ *    temporary index buffer, when idx_out is NULL and the table is too large
+ *    for one LDS tile; every other call allocates nothing.
+ *  - Row-major layouts.  A has row stride `lda` (elements, lda >= D); every
+ *    other array is dense.
+ *  - Return value: MADDNESS_OK or an error status (never aborts, never
+ *    throws).  Argument checks run before any HIP call, so they work on a
+ *    machine without a GPU.  N == 0 is valid and enqueues nothing.
+ *  - Device-array CONTENTS are preconditions that the hot path does not
+ *    check: split dims in [0, D) (kernels clamp them for memory safety only),
+ *    indices in [0, 16), scales exact normal fp32 powers of two with
+ *    127 * sum_c 2^(e_c - e_min) < 2^31.  Violations give unspecified values,
+ *    never out-of-bounds accesses.
+ *  - Thread safety: no mutable global state; concurrent calls on different
+ *    streams are independent.
+ */
+#ifndef MADDNESS_H
+#define MADDNESS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    MADDNESS_OK = 0,
+    MADDNESS_EINVAL = 1,       /* bad size, NULL or misaligned pointer      */
+    MADDNESS_EHIP = 2,         /* a HIP runtime call or a launch failed     */
+    MADDNESS_EUNSUPPORTED = 3, /* shape beyond what the kernels handle      */
+    MADDNESS_ENOMEM = 4        /* temporary index buffer could not be made  */
+};
+
+#define MADDNESS_K 16          /* prototypes per codebook (4-bit indices)   */
+#define MADDNESS_LEVELS 4      /* tree depth: comparisons per codebook      */
+#define MADDNESS_NODES 15      /* thresholds per codebook                   */
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int maddness_version(void);
+
+/* Static string naming a status code; never NULL. */
+const char* maddness_status_string(int status);
+
+/*
+ * Encoding function (§1: map each subvector to the index of one of K
+ * prototypes, a log2(K)-bit integer; §1 and §2.1: a balanced binary tree
+ * with four comparisons per codebook, K = 16).
+ *
+ *   A           [N][lda] fp32, row n at A + n * lda, D columns used.
+ *   split_dims  [C][4] int32: the column of A compared at tree level t.
+ *               A GLOBAL column index, so any permutation of the input
+ *               dimensions (the subspace partitioning of §2.1) is folded in.
+ *   thresholds  [C][15] fp32 in heap order: node i (0 <= i < 2^t) of level t
+ *               is thresholds[c][2^t - 1 + i].
+ *   idx_out     [N][C] uint8, written with values in [0, 16).
+ *
+ * idx[n][c] = i_4 where i_0 = 0 and
+ *   i_{t+1} = 2 i_t + (A[n][split[c][t]] > thresholds[c][2^t - 1 + i_t]);
+ * the comparison is strict (ties and NaN go to the 0 branch), so the root
+ * decision is the most significant bit.
+ *
+ * EINVAL: a NULL array (when N > 0), N < 0, D <= 0, C <= 0, lda < D,
+ * split_dims/thresholds/A not 4-byte aligned.  EUNSUPPORTED: C > 512.
+ */
+int maddness_encode(const float* A, int64_t N, int32_t D, int64_t lda,
+                    const int32_t* split_dims, const float* thresholds,
+                    int32_t C, uint8_t* idx_out, void* stream);
+
+/*
+ * Lookup-accumulate over 8-bit block floating point tables (§1: the result
+ * is the sum over codebooks of the table rows picked by the indices; tables
+ * quantized to 8-bit block floating point).
+ *
+ *   idx     [N][C] uint8 in [0, 16).
+ *   lut     [C][16][M] int8 codes q.
+ *   scale   [C] fp32, each an exact normal power of two 2^e_c.
+ *   offset  [C] fp32 o_c.  The table entry is 2^e_c * q + o_c.
+ *   acc_out [N][M] int32 or NULL:  acc = sum_c q[c][idx[n][c]][m] << (e_c - e_min),
+ *           exact (no overflow under the precondition above).
+ *   y_out   [N][M] fp32 or NULL (not both NULL):
+ *           y = fmaf((float)acc, 2^e_min, bias32), a single rounding, where
+ *           bias32 = (float)(sum_c offset[c] accumulated in double, c = 0..C-1).
+ *
+ * EINVAL: a NULL required array, both outputs NULL, N < 0, C <= 0, M <= 0,
+ * misaligned scale/offset/acc_out/y_out.  EUNSUPPORTED: C > 512.
+ */
+int maddness_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C,
+                            const int8_t* lut, const float* scale,
+                            const float* offset, int32_t M,
+                            int32_t* acc_out, float* y_out, void* stream);
+
+/*
+ * Lookup-accumulate over an unquantized fp32 table [C][16][M]:
+ *   y[n][m] = (((0 + T[0][idx0][m]) + T[1][idx1][m]) + ...) in fp32, codebooks
+ * in ascending order (a fixed order, so the result is deterministic).
+ * EINVAL / EUNSUPPORTED as above.
+ */
+int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C,
+                                const float* lut, int32_t M, float* y_out,
+                                void* stream);
+
+/*
+ * Fused encode + lookup-accumulate: the whole inference path for one layer
+ * (§1).  Same arguments and results as maddness_encode followed by
+ * maddness_lut_accumulate; y_out is required, acc_out and idx_out are
+ * optional extra outputs.  When the table [C][16][M] fits in LDS the indices
+ * never leave the chip; otherwise the rows are encoded into idx_out (or a
+ * stream-ordered temporary buffer, ENOMEM if it cannot be made) and
+ * accumulated in column tiles.
+ */
+int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda,
+                    const int32_t* split_dims, const float* thresholds,
+                    int32_t C, const int8_t* lut, const float* scale,
+                    const float* offset, int32_t M, float* y_out,
+                    int32_t* acc_out, uint8_t* idx_out, void* stream);
+
+/* Fused encode + fp32-table accumulate (unquantized mode); see above. */
+int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda,
+                        const int32_t* split_dims, const float* thresholds,
+                        int32_t C, const float* lut, int32_t M, float* y_out,
+                        uint8_t* idx_out, void* stream);
+
+/*
+ * Offline table construction (§2.2: T = P B) followed by 8-bit block
+ * floating point quantization (§1).
+ *
+ *   P      [C][16][D] fp32 prototypes (zero outside codebook c's subspace).
+ *   B      [D][M] fp32 weights.
+ *   T[c][k][m] = sum_d P[c][k][d] * B[d][m], a double sum over d ascending
+ *   (each product is exact in double).  Per codebook, over its 16 x M
+ *   entries: offset o_c = (float)((min + max) / 2); r_c = max |T - o_c|;
+ *   e_c = the smallest integer in [-126, 127] with r_c <= 127 * 2^e_c, then
+ *   raised to at least max_c e_c - cap, cap the largest integer with
+ *   127 * C * 2^cap < 2^24 (so acc stays exact in fp32); codes
+ *   q = round-half-even((T - o_c) / 2^e_c) in [-127, 127]; scale = 2^e_c.
+ *
+ *   lut_out [C][16][M] int8, scale_out [C] fp32, offset_out [C] fp32.
+ * EINVAL: NULL, non-positive sizes, 127 * C >= 2^24, misaligned P/B/scale/offset.
+ */
+int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D,
+                       int32_t M, int8_t* lut_out, float* scale_out,
+                       float* offset_out, void* stream);
+
+/* Same table T = P B, each entry rounded to fp32 (unquantized mode). */
+int maddness_build_lut_f32(const float* P, const float* B, int32_t C,
+                           int32_t D, int32_t M, float* lut_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MADDNESS_H */

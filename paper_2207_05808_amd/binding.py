@@ -1,0 +1,245 @@
+"""Torch-tensor front end of the C ABI (same names as include/maddness.h).
+
+Each function checks dtypes, devices and shapes, allocates outputs that were
+not supplied, and passes raw device pointers plus the current HIP stream to
+the library.  No arithmetic of the method happens here.
+
+With ``validate=True`` the device-array preconditions of the ABI (split
+columns in range, indices below 16, scales exact powers of two, no int32
+overflow) are checked on host copies first; this synchronises and is meant
+for tests and debugging.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib
+
+K, LEVELS, NODES = 16, 4, 15
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+
+
+def _dense(t: torch.Tensor, name: str):
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _rows(A: torch.Tensor) -> Tuple[int, int, int]:
+    _need(A, "A", torch.float32, 2)
+    if A.shape[0] > 1 and A.stride(1) != 1:
+        raise ValueError("A must have unit column stride")
+    N, D = A.shape
+    lda = A.stride(0) if N > 1 else D
+    return N, D, lda
+
+
+def _tree_args(split: torch.Tensor, thr: torch.Tensor) -> int:
+    _need(split, "split_dims", torch.int32, 2)
+    _need(thr, "thresholds", torch.float32, 2)
+    _dense(split, "split_dims")
+    _dense(thr, "thresholds")
+    C = split.shape[0]
+    if tuple(split.shape) != (C, LEVELS) or tuple(thr.shape) != (C, NODES):
+        raise ValueError(f"split_dims must be [C,4] and thresholds [C,15], got "
+                         f"{tuple(split.shape)} and {tuple(thr.shape)}")
+    return C
+
+
+def _validate_trees(split: torch.Tensor, D: int):
+    s = split.cpu()
+    if s.numel() and (int(s.min()) < 0 or int(s.max()) >= D):
+        raise ValueError("split_dims outside [0, D)")
+
+
+def _validate_scales(scale: torch.Tensor):
+    s = scale.cpu().numpy()
+    import numpy as np
+    m, e = np.frexp(s)
+    if not (np.all(m == 0.5) and np.all(e - 1 >= -126)):
+        raise ValueError("scales must be exact normal powers of two")
+    sh = (e - 1) - (e - 1).min()
+    if np.any(sh > 30) or float(np.sum(127.0 * np.ldexp(1.0, sh))) >= 2.0 ** 31:
+        raise ValueError("scale exponents too far apart: the int32 sum could overflow")
+
+
+def _validate_idx(idx: torch.Tensor):
+    if idx.numel() and int(idx.max()) >= K:
+        raise ValueError("indices must lie in [0, 16)")
+
+
+def encode(A, split_dims, thresholds, idx_out=None, stream=None, validate=False):
+    """Tree encoding: returns idx [N][C] uint8 (see maddness_encode)."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    if validate:
+        _validate_trees(split_dims, D)
+    if idx_out is None:
+        idx_out = torch.empty((N, C), dtype=torch.uint8, device=A.device)
+    _need(idx_out, "idx_out", torch.uint8, 2)
+    _dense(idx_out, "idx_out")
+    st = _lib.lib().maddness_encode(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
+                                    _ptr(idx_out), _stream(stream))
+    _lib.check("maddness_encode", st)
+    return idx_out
+
+
+def _lut_i8(lut, scale, offset):
+    _need(lut, "lut", torch.int8, 3)
+    _need(scale, "scale", torch.float32, 1)
+    _need(offset, "offset", torch.float32, 1)
+    for t, n in ((lut, "lut"), (scale, "scale"), (offset, "offset")):
+        _dense(t, n)
+    C, k, M = lut.shape
+    if k != K or scale.shape[0] != C or offset.shape[0] != C:
+        raise ValueError("lut must be [C,16,M], scale and offset [C]")
+    return C, M
+
+
+def lut_accumulate(idx, lut, scale, offset, acc_out=None, y_out=None, want_acc=False, want_y=True,
+                   stream=None, validate=False):
+    """Gather-accumulate over an int8 block-FP table; returns (acc or None, y or None)."""
+    _need(idx, "idx", torch.uint8, 2)
+    _dense(idx, "idx")
+    C, M = _lut_i8(lut, scale, offset)
+    N = idx.shape[0]
+    if idx.shape[1] != C:
+        raise ValueError("idx must be [N, C]")
+    if validate:
+        _validate_idx(idx)
+        _validate_scales(scale)
+    if acc_out is None and want_acc:
+        acc_out = torch.empty((N, M), dtype=torch.int32, device=idx.device)
+    if y_out is None and want_y:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=idx.device)
+    st = _lib.lib().maddness_lut_accumulate(_ptr(idx), N, C, _ptr(lut), _ptr(scale), _ptr(offset), M,
+                                            _ptr(acc_out), _ptr(y_out), _stream(stream))
+    _lib.check("maddness_lut_accumulate", st)
+    return acc_out, y_out
+
+
+def lut_accumulate_f32(idx, lut, y_out=None, stream=None, validate=False):
+    """Gather-accumulate over an fp32 table [C][16][M]; returns y [N][M]."""
+    _need(idx, "idx", torch.uint8, 2)
+    _need(lut, "lut", torch.float32, 3)
+    _dense(idx, "idx")
+    _dense(lut, "lut")
+    C, k, M = lut.shape
+    N = idx.shape[0]
+    if k != K or idx.shape[1] != C:
+        raise ValueError("lut must be [C,16,M] and idx [N,C]")
+    if validate:
+        _validate_idx(idx)
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=idx.device)
+    st = _lib.lib().maddness_lut_accumulate_f32(_ptr(idx), N, C, _ptr(lut), M, _ptr(y_out),
+                                                _stream(stream))
+    _lib.check("maddness_lut_accumulate_f32", st)
+    return y_out
+
+
+def matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, acc_out=None, idx_out=None,
+           want_acc=False, want_idx=False, stream=None, validate=False):
+    """Fused encode + int8 lookup-accumulate; returns (y, acc or None, idx or None)."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    C2, M = _lut_i8(lut, scale, offset)
+    if C2 != C:
+        raise ValueError("lut codebooks differ from the trees'")
+    if validate:
+        _validate_trees(split_dims, D)
+        _validate_scales(scale)
+    dev = A.device
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=dev)
+    if acc_out is None and want_acc:
+        acc_out = torch.empty((N, M), dtype=torch.int32, device=dev)
+    if idx_out is None and want_idx:
+        idx_out = torch.empty((N, C), dtype=torch.uint8, device=dev)
+    st = _lib.lib().maddness_matmul(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
+                                    _ptr(lut), _ptr(scale), _ptr(offset), M, _ptr(y_out),
+                                    _ptr(acc_out), _ptr(idx_out), _stream(stream))
+    _lib.check("maddness_matmul", st)
+    return y_out, acc_out, idx_out
+
+
+def matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None, want_idx=False, stream=None,
+               validate=False):
+    """Fused encode + fp32 lookup-accumulate; returns (y, idx or None)."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    _need(lut, "lut", torch.float32, 3)
+    _dense(lut, "lut")
+    if lut.shape[0] != C or lut.shape[1] != K:
+        raise ValueError("lut must be [C,16,M]")
+    M = lut.shape[2]
+    if validate:
+        _validate_trees(split_dims, D)
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
+    if idx_out is None and want_idx:
+        idx_out = torch.empty((N, C), dtype=torch.uint8, device=A.device)
+    st = _lib.lib().maddness_matmul_f32(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
+                                        _ptr(lut), M, _ptr(y_out), _ptr(idx_out), _stream(stream))
+    _lib.check("maddness_matmul_f32", st)
+    return y_out, idx_out
+
+
+def build_lut(P, B, stream=None):
+    """Table T = P B, 8-bit block-FP quantized; returns (lut int8 [C,16,M], scale [C], offset [C])."""
+    _need(P, "P", torch.float32, 3)
+    _need(B, "B", torch.float32, 2)
+    _dense(P, "P")
+    _dense(B, "B")
+    C, k, D = P.shape
+    if k != K or B.shape[0] != D:
+        raise ValueError("P must be [C,16,D] and B [D,M]")
+    M = B.shape[1]
+    lut = torch.empty((C, K, M), dtype=torch.int8, device=P.device)
+    scale = torch.empty((C,), dtype=torch.float32, device=P.device)
+    offset = torch.empty((C,), dtype=torch.float32, device=P.device)
+    st = _lib.lib().maddness_build_lut(_ptr(P), _ptr(B), C, D, M, _ptr(lut), _ptr(scale),
+                                       _ptr(offset), _stream(stream))
+    _lib.check("maddness_build_lut", st)
+    return lut, scale, offset
+
+
+def build_lut_f32(P, B, stream=None):
+    """Table T = P B rounded to fp32; returns lut [C,16,M]."""
+    _need(P, "P", torch.float32, 3)
+    _need(B, "B", torch.float32, 2)
+    _dense(P, "P")
+    _dense(B, "B")
+    C, k, D = P.shape
+    if k != K or B.shape[0] != D:
+        raise ValueError("P must be [C,16,D] and B [D,M]")
+    M = B.shape[1]
+    lut = torch.empty((C, K, M), dtype=torch.float32, device=P.device)
+    st = _lib.lib().maddness_build_lut_f32(_ptr(P), _ptr(B), C, D, M, _ptr(lut), _stream(stream))
+    _lib.check("maddness_build_lut_f32", st)
+    return lut
+
+
+def version() -> int:
+    return int(_lib.lib().maddness_version())

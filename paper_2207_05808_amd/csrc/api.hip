@@ -1,0 +1,358 @@
+// C ABI of libmaddness: argument validation, launch planning and dispatch.
+// Declarations and the meaning of every argument: include/maddness.h.
+#include "maddness.h"
+#include "internal.hpp"
+
+#include <stdint.h>
+
+namespace mdn {
+namespace {
+
+constexpr int kPFs[] = {1, 2, 4, 8, 9, 16};  // instantiated prefetch depths
+
+bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0; }
+int round_up(int v, int m) { return (v + m - 1) / m * m; }
+int ilog2(int v) { int r = 0; while ((1 << r) < v) ++r; return r; }
+
+int pick_pf(int units) {  // smallest instantiated depth holding `units` 16-byte units per wavefront
+  for (int pf : kPFs)
+    if (units <= 64 * pf) return pf;
+  return -1;
+}
+
+int status_from(hipError_t e) { return e == hipSuccess ? MADDNESS_OK : MADDNESS_EHIP; }
+
+struct Shape {
+  int mode, elem;
+  const float* A; int64_t N; int D; int64_t lda;
+  const int32_t* split; const float* thr; int C;
+  const void* lut; const float* scale; const float* offset; int M;
+  const uint8_t* idx_in;
+  float* y; int32_t* acc; uint8_t* idx_out;
+};
+
+// LDS layout for one workgroup of `nw` wavefronts.
+LdsLayout layout(const Shape& s, int nw, int rw, int Dp, int Cp, int lut_bytes) {
+  LdsLayout L{};
+  int off = 0;
+  auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
+  const bool enc = s.mode != kAccum;
+  L.lut = take(s.mode != kEncode ? lut_bytes : 0);
+  L.thr = take(enc ? s.C * 16 * 4 : 0);
+  L.split = take(enc ? s.C * kLevels * 4 : 0);
+  L.misc = take(16);
+  L.a = take(enc ? nw * rw * Dp * 4 : 0);
+  L.idx = take(nw * rw * Cp);
+  L.total = off;
+  return L;
+}
+
+struct Plan {
+  KArgs a;
+  int pf, uq, nw;
+  dim3 grid, block;
+};
+
+// LDS bytes of one (c, k) row of a LUT tile of `cols` columns.
+int lut_row_stride(int elem, int cols) {
+  if (elem == kI8) {
+    int b = round_up(cols, 4);
+    if (((b >> 2) & 1) == 0) b += 4;  // odd dword stride spreads the 16 rows of a codebook over banks
+    return b;
+  }
+  return round_up(cols, 4) * 4;
+}
+
+// Widest column tile (<= max_cols, multiple of 4 unless it is all of M) whose
+// C*16 rows fit in LDS next to `reserve` bytes, then narrowed to split M into
+// equal tiles.  Returns false when not even 4 columns fit.
+bool lut_tile(int elem, int C, int M, int reserve, int max_cols, int* Mt, int* rs) {
+  const int64_t rows = (int64_t)C * kK;
+  int cols = M < max_cols ? M : (max_cols & ~3);
+  while (cols > 0 && rows * lut_row_stride(elem, cols) + reserve > kLdsBytes)
+    cols = (cols > 4) ? ((cols - 1) & ~3) : 0;
+  if (cols <= 0) return false;
+  if (cols < M) {
+    const int ntiles = (M + cols - 1) / cols;
+    cols = round_up((M + ntiles - 1) / ntiles, 4);
+  }
+  *Mt = cols;
+  *rs = lut_row_stride(elem, cols);
+  return true;
+}
+
+// Builds the launch plan; returns a status (EUNSUPPORTED when the shape cannot run).
+// Chunk size RW (rows per wavefront iteration) is chosen by, in order:
+// fewest column tiles, fewest column quads per lane, largest RW.
+int plan(const Shape& s, Plan* out, bool single_tile_only) {
+  KArgs a{};
+  a.A = s.A; a.idx_in = s.idx_in; a.split = s.split; a.thr = s.thr;
+  a.lut = s.lut; a.scale = s.scale; a.offset = s.offset;
+  a.y = s.y; a.acc = s.acc; a.idx_out = s.idx_out;
+  a.N = s.N; a.lda = s.lda; a.D = s.D; a.C = s.C; a.M = s.M;
+  a.Cp = round_up(s.C, 4);
+  a.c_magic = s.C > 1 ? (uint32_t)((1ull << 32) / (uint64_t)s.C + 1) : 0u;
+
+  const bool enc = s.mode != kAccum;
+  const bool acc = s.mode != kEncode;
+  const int nw = 4;
+
+  bool vec_rows;
+  int upr;  // 16-byte units per staged source row
+  if (enc) {
+    vec_rows = (s.D % 4 == 0) && (s.lda % 4 == 0) && aligned(s.A, 16);
+    upr = s.D / 4;
+  } else {
+    vec_rows = (s.C % 16 == 0) && aligned(s.idx_in, 16);
+    upr = s.C / 16;
+  }
+  if (enc) {
+    a.Dp = round_up(s.D, 4);
+    if (a.Dp % 32 == 0) a.Dp += 4;  // rows of one chunk start on different banks
+  }
+  a.vec_out = acc && (s.M % 4 == 0) && aligned(s.lut, 4) && (s.y == nullptr || aligned(s.y, 16)) &&
+              (s.acc == nullptr || aligned(s.acc, 16));
+
+  // Accumulate cost model: lane-quad slots per row = tiles * LPR * UQ (idle
+  // lanes included); ties go to fewer quads per lane, then to larger chunks.
+  bool found = false;
+  int best_rw = 0, best_pf = 0, best_uq = 0, best_Mt = 1, best_rs = 0, best_tiles = 1;
+  int64_t best_cost = 0;
+  for (int rw_log2 = 6; rw_log2 >= 0; --rw_log2) {
+    const int rw = 1 << rw_log2;
+    const int lpr = 64 / rw;
+    int pf = 0;
+    if (vec_rows) {
+      pf = pick_pf(rw * upr);
+      if (pf < 0 || (pf > 9 && rw > 1)) continue;  // bound the prefetch registers
+      if (enc && (int64_t)rw * s.lda * 4 >= (1ll << 31)) continue;
+    } else if (rw > 8) {
+      continue;  // synchronous staging: small chunks
+    }
+    const int reserve = layout(s, nw, rw, a.Dp, a.Cp, 0).total;
+    if (reserve > kLdsBytes) continue;
+    for (int uq_cap = 1; uq_cap <= (acc ? 4 : 1); uq_cap *= 2) {
+      int uq = 1, Mt = 1, rs = 0, tiles = 1;
+      if (acc) {
+        if (!lut_tile(s.elem, s.C, s.M, reserve, 4 * lpr * uq_cap, &Mt, &rs)) continue;
+        tiles = (s.M + Mt - 1) / Mt;
+        if (single_tile_only && tiles > 1) continue;
+        if (tiles > 65535) continue;
+        uq = ((Mt + 3) / 4 + lpr - 1) / lpr;
+        if (uq == 3) uq = 4;
+        if (uq > 4) continue;
+      }
+      const int64_t cost = (int64_t)tiles * lpr * uq;
+      const bool better = !found || cost < best_cost || (cost == best_cost && uq < best_uq);
+      if (better) {
+        found = true;
+        best_cost = cost;
+        best_rw = rw; best_pf = pf; best_uq = uq; best_Mt = Mt; best_rs = rs; best_tiles = tiles;
+      }
+    }
+  }
+  if (!found) return MADDNESS_EUNSUPPORTED;
+
+  a.RW = best_rw;
+  a.rw_log2 = ilog2(best_rw);
+  a.Mt = best_Mt;
+  a.lut_rs = best_rs;
+  a.vec_rows = vec_rows;
+  a.nchunks = (s.N + best_rw - 1) / best_rw;
+  a.L = layout(s, nw, best_rw, a.Dp, a.Cp, acc ? s.C * kK * best_rs : 0);
+  if (a.L.total > kLdsBytes) return MADDNESS_EUNSUPPORTED;
+
+  int per_cu = kLdsBytes / (a.L.total > 0 ? a.L.total : 1);
+  const int by_threads = 2048 / (nw * 64);
+  if (per_cu > by_threads) per_cu = by_threads;
+  if (per_cu < 1) per_cu = 1;
+  int64_t gx = (int64_t)256 * per_cu / best_tiles;
+  if (gx < 8) gx = 8;
+  const int64_t need = (a.nchunks + nw - 1) / nw;
+  if (gx > need) gx = need;
+  if (gx < 1) gx = 1;
+
+  out->a = a;
+  out->pf = vec_rows ? best_pf : 0;
+  out->uq = best_uq;
+  out->nw = nw;
+  out->grid = dim3((unsigned)gx, (unsigned)best_tiles, 1);
+  out->block = dim3(nw * 64, 1, 1);
+  return MADDNESS_OK;
+}
+
+int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
+  Plan p;
+  const int rc = plan(s, &p, single_tile_only);
+  if (rc != MADDNESS_OK) return rc;
+  return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, stream));
+}
+
+// ----------------------------------------------------------------- checks
+int check_encode_args(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split,
+                      const float* thr, int32_t C) {
+  if (N < 0 || D <= 0 || C <= 0 || lda < D) return MADDNESS_EINVAL;
+  if (N == 0) return C > kMaxC ? MADDNESS_EUNSUPPORTED : MADDNESS_OK;
+  if (!A || !split || !thr) return MADDNESS_EINVAL;
+  if (!aligned(A, 4) || !aligned(split, 4) || !aligned(thr, 4)) return MADDNESS_EINVAL;
+  if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
+  return MADDNESS_OK;
+}
+
+int check_accum_args(int64_t N, int32_t C, const void* lut, int32_t M) {
+  if (N < 0 || C <= 0 || M <= 0) return MADDNESS_EINVAL;
+  if (N == 0) return C > kMaxC ? MADDNESS_EUNSUPPORTED : MADDNESS_OK;
+  if (!lut) return MADDNESS_EINVAL;
+  if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
+  return MADDNESS_OK;
+}
+
+Shape shape(int mode, int elem) {
+  Shape s{};
+  s.mode = mode;
+  s.elem = elem;
+  return s;
+}
+
+// Two-phase path for tables larger than one LDS tile: encode, then tiled accumulate.
+int two_phase(Shape s, uint8_t* idx_user, hipStream_t stream) {
+  uint8_t* idx = idx_user;
+  bool temp = false;
+  if (!idx) {
+    if (hipMallocAsync(reinterpret_cast<void**>(&idx), (size_t)s.N * (size_t)s.C, stream) != hipSuccess ||
+        !idx)
+      return MADDNESS_ENOMEM;
+    temp = true;
+  }
+  Shape e = s;
+  e.mode = kEncode;
+  e.idx_out = idx;
+  int rc = run(e, false, stream);
+  if (rc == MADDNESS_OK) {
+    Shape q = s;
+    q.mode = kAccum;
+    q.idx_in = idx;
+    q.idx_out = nullptr;
+    rc = run(q, false, stream);
+  }
+  if (temp && hipFreeAsync(idx, stream) != hipSuccess && rc == MADDNESS_OK) rc = MADDNESS_EHIP;
+  return rc;
+}
+
+}  // namespace
+}  // namespace mdn
+
+using namespace mdn;
+
+extern "C" {
+
+int maddness_version(void) { return 100; }
+
+const char* maddness_status_string(int status) {
+  switch (status) {
+    case MADDNESS_OK: return "ok";
+    case MADDNESS_EINVAL: return "invalid argument";
+    case MADDNESS_EHIP: return "HIP runtime error";
+    case MADDNESS_EUNSUPPORTED: return "unsupported shape";
+    case MADDNESS_ENOMEM: return "out of device memory";
+    default: return "unknown status";
+  }
+}
+
+int maddness_encode(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
+                    const float* thresholds, int32_t C, uint8_t* idx_out, void* stream) {
+  int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!idx_out) return MADDNESS_EINVAL;
+  Shape s = shape(kEncode, kI8);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
+  s.M = 1; s.idx_out = idx_out;
+  return run(s, false, static_cast<hipStream_t>(stream));
+}
+
+int maddness_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C, const int8_t* lut,
+                            const float* scale, const float* offset, int32_t M, int32_t* acc_out,
+                            float* y_out, void* stream) {
+  int rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!idx || !scale || !offset || (!acc_out && !y_out)) return MADDNESS_EINVAL;
+  if (!aligned(scale, 4) || !aligned(offset, 4) || (acc_out && !aligned(acc_out, 4)) ||
+      (y_out && !aligned(y_out, 4)))
+    return MADDNESS_EINVAL;
+  Shape s = shape(kAccum, kI8);
+  s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.scale = scale; s.offset = offset; s.M = M;
+  s.acc = acc_out; s.y = y_out;
+  return run(s, false, static_cast<hipStream_t>(stream));
+}
+
+int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C, const float* lut, int32_t M,
+                                float* y_out, void* stream) {
+  int rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!idx || !y_out || !aligned(lut, 4) || !aligned(y_out, 4)) return MADDNESS_EINVAL;
+  Shape s = shape(kAccum, kF32);
+  s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.M = M; s.y = y_out;
+  return run(s, false, static_cast<hipStream_t>(stream));
+}
+
+int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
+                    const float* thresholds, int32_t C, const int8_t* lut, const float* scale,
+                    const float* offset, int32_t M, float* y_out, int32_t* acc_out, uint8_t* idx_out,
+                    void* stream) {
+  int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
+  if (rc != MADDNESS_OK) return rc;
+  rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!scale || !offset || !y_out || !aligned(scale, 4) || !aligned(offset, 4) || !aligned(y_out, 4) ||
+      (acc_out && !aligned(acc_out, 4)))
+    return MADDNESS_EINVAL;
+  Shape s = shape(kFused, kI8);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
+  s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out; s.acc = acc_out;
+  s.idx_out = idx_out;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Plan p;
+  if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
+  return two_phase(s, idx_out, st);
+}
+
+int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
+                        const float* thresholds, int32_t C, const float* lut, int32_t M, float* y_out,
+                        uint8_t* idx_out, void* stream) {
+  int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
+  if (rc != MADDNESS_OK) return rc;
+  rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!y_out || !aligned(lut, 4) || !aligned(y_out, 4)) return MADDNESS_EINVAL;
+  Shape s = shape(kFused, kF32);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
+  s.lut = lut; s.M = M; s.y = y_out; s.idx_out = idx_out;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Plan p;
+  if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
+  return two_phase(s, idx_out, st);
+}
+
+int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D, int32_t M, int8_t* lut_out,
+                       float* scale_out, float* offset_out, void* stream) {
+  if (C <= 0 || D <= 0 || M <= 0 || !P || !B || !lut_out || !scale_out || !offset_out)
+    return MADDNESS_EINVAL;
+  if (!aligned(P, 4) || !aligned(B, 4) || !aligned(scale_out, 4) || !aligned(offset_out, 4))
+    return MADDNESS_EINVAL;
+  if (127.0 * C >= 16777216.0) return MADDNESS_EINVAL;
+  if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
+  int cap = 0;
+  while (127.0 * C * (double)(1ll << (cap + 1)) < 16777216.0) ++cap;
+  return status_from(launch_build_lut(P, B, C, D, M, lut_out, scale_out, offset_out, cap,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int maddness_build_lut_f32(const float* P, const float* B, int32_t C, int32_t D, int32_t M, float* lut_out,
+                           void* stream) {
+  if (C <= 0 || D <= 0 || M <= 0 || !P || !B || !lut_out) return MADDNESS_EINVAL;
+  if (!aligned(P, 4) || !aligned(B, 4) || !aligned(lut_out, 4)) return MADDNESS_EINVAL;
+  if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
+  return status_from(launch_build_lut_f32(P, B, C, D, M, lut_out, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,68 @@
+// Internal interface between the host dispatcher (api.hip) and the kernels.
+// Not installed; the public interface is include/maddness.h.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mdn {
+
+constexpr int kK = 16;       // prototypes per codebook
+constexpr int kLevels = 4;   // tree depth
+constexpr int kNodes = 15;   // thresholds per codebook (heap order)
+constexpr int kMaxC = 512;   // codebooks supported by one launch
+constexpr int kLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
+
+enum Mode : int { kEncode = 0, kAccum = 1, kFused = 2 };
+enum Elem : int { kI8 = 0, kF32 = 1 };
+
+// Byte offsets of the LDS regions of one workgroup (all 16-byte aligned).
+struct LdsLayout {
+  int lut;     // LUT tile: [C*16 rows][lut_rs bytes]
+  int thr;     // [C][16] fp32 thresholds (heap order, slot 15 unused)
+  int split;   // [C][4] int32 split columns (clamped to [0, D))
+  int misc;    // int32[4]: e_min, max shift, bias32 bits, step bits
+  int a;       // per wave: [RW][Dp] fp32 staged rows of A
+  int idx;     // per wave: [RW][Cp] uint8 indices
+  int total;
+};
+
+struct KArgs {
+  const float* A;         // [N][lda]
+  const uint8_t* idx_in;  // [N][C] (accumulate mode)
+  const int32_t* split;   // [C][4]
+  const float* thr;       // [C][15]
+  const void* lut;        // [C][16][M] int8 or fp32
+  const float* scale;     // [C]
+  const float* offset;    // [C]
+  float* y;               // [N][M]
+  int32_t* acc;           // [N][M] or null
+  uint8_t* idx_out;       // [N][C] or null
+  int64_t N;
+  int64_t lda;
+  int D, C, M;
+  int Mt;        // columns per LUT tile (blockIdx.y selects the tile)
+  int lut_rs;    // LDS bytes per (c,k) row of the LUT tile
+  int Dp;        // LDS row stride of staged A rows, floats
+  int Cp;        // LDS row stride of staged indices, bytes (multiple of 4)
+  int RW;        // rows per wave chunk (power of two, 1..64)
+  int rw_log2;
+  int64_t nchunks;       // ceil(N / RW)
+  uint32_t c_magic;      // p / C == umulhi(p, c_magic) >> c_shift for p < 2^16
+  int c_shift;
+  int vec_rows;          // 1: staged rows move in 16-byte units
+  int vec_out;           // 1: outputs / LUT rows allow 16-byte (4-column) stores
+  LdsLayout L;
+};
+
+// Launch one kernel of the family; returns hipSuccess or the launch error.
+hipError_t launch_path(int mode, int elem, int pf, int uq, const KArgs& a,
+                       dim3 grid, dim3 block, hipStream_t stream);
+
+// Offline table build (T = P B, quantization); see lut_build.hip.
+hipError_t launch_build_lut(const float* P, const float* B, int C, int D, int M,
+                            int8_t* lut, float* scale, float* offset, int cap,
+                            hipStream_t stream);
+hipError_t launch_build_lut_f32(const float* P, const float* B, int C, int D, int M,
+                                float* lut, hipStream_t stream);
+
+}  // namespace mdn

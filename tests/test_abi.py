@@ -1,0 +1,95 @@
+"""The C ABI on the host: the library loads, exports every symbol that
+include/maddness.h declares, and rejects bad arguments before any HIP call
+(so these checks need no GPU and launch nothing)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "maddness.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(maddness_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2207_05808_amd import _lib
+    return _lib.lib()
+
+
+def test_header_declares_the_path():
+    names = declared_functions()
+    for need in ("maddness_encode", "maddness_lut_accumulate", "maddness_matmul",
+                 "maddness_lut_accumulate_f32", "maddness_matmul_f32", "maddness_build_lut"):
+        assert need in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), f"{name} declared but not exported"
+
+
+def test_status_strings(L):
+    assert L.maddness_version() >= 100
+    for s in range(5):
+        assert L.maddness_status_string(s)
+    assert L.maddness_status_string(99) == b"unknown status"
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+NULL = None
+
+
+def test_encode_rejects(L):
+    E = L.maddness_encode
+    assert E(FAKE, -1, 64, 64, FAKE, FAKE, 4, FAKE, NULL) == 1      # N < 0
+    assert E(FAKE, 10, 0, 64, FAKE, FAKE, 4, FAKE, NULL) == 1       # D <= 0
+    assert E(FAKE, 10, 64, 63, FAKE, FAKE, 4, FAKE, NULL) == 1      # lda < D
+    assert E(FAKE, 10, 64, 64, FAKE, FAKE, 0, FAKE, NULL) == 1      # C <= 0
+    assert E(NULL, 10, 64, 64, FAKE, FAKE, 4, FAKE, NULL) == 1      # NULL A
+    assert E(FAKE, 10, 64, 64, NULL, FAKE, 4, FAKE, NULL) == 1      # NULL split
+    assert E(FAKE, 10, 64, 64, FAKE, FAKE, 4, NULL, NULL) == 1      # NULL out
+    assert E(ctypes.c_void_p(0x1002), 10, 64, 64, FAKE, FAKE, 4, FAKE, NULL) == 1  # misaligned A
+    assert E(FAKE, 10, 64, 64, FAKE, FAKE, 513, FAKE, NULL) == 3    # too many codebooks
+    assert E(NULL, 0, 64, 64, NULL, NULL, 4, NULL, NULL) == 0       # N == 0: nothing to do
+
+
+def test_accumulate_rejects(L):
+    A = L.maddness_lut_accumulate
+    assert A(FAKE, 10, 4, FAKE, FAKE, FAKE, 10, NULL, NULL, NULL) == 1   # both outputs NULL
+    assert A(FAKE, 10, 4, FAKE, FAKE, FAKE, 0, FAKE, FAKE, NULL) == 1    # M <= 0
+    assert A(FAKE, 10, 4, NULL, FAKE, FAKE, 10, FAKE, FAKE, NULL) == 1   # NULL lut
+    assert A(FAKE, 10, 4, FAKE, NULL, FAKE, 10, FAKE, FAKE, NULL) == 1   # NULL scale
+    assert A(FAKE, 10, 4, FAKE, FAKE, ctypes.c_void_p(0x1001), 10, FAKE, FAKE, NULL) == 1
+    assert A(FAKE, 10, 600, FAKE, FAKE, FAKE, 10, FAKE, FAKE, NULL) == 3
+    assert A(NULL, 0, 4, NULL, NULL, NULL, 10, NULL, NULL, NULL) == 0
+    F = L.maddness_lut_accumulate_f32
+    assert F(FAKE, 10, 4, FAKE, 10, NULL, NULL) == 1
+    assert F(FAKE, -5, 4, FAKE, 10, FAKE, NULL) == 1
+
+
+def test_matmul_rejects(L):
+    Mm = L.maddness_matmul
+    args = [FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, FAKE, NULL, NULL, NULL]
+    bad = list(args); bad[11] = NULL          # y_out required
+    assert Mm(*bad) == 1
+    bad = list(args); bad[3] = 10             # lda < D
+    assert Mm(*bad) == 1
+    bad = list(args); bad[10] = -1            # M
+    assert Mm(*bad) == 1
+    F = L.maddness_matmul_f32
+    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, NULL, NULL) == 1
+
+
+def test_build_lut_rejects(L):
+    B = L.maddness_build_lut
+    assert B(FAKE, FAKE, 0, 64, 10, FAKE, FAKE, FAKE, NULL) == 1
+    assert B(FAKE, FAKE, 4, 64, 10, NULL, FAKE, FAKE, NULL) == 1
+    assert B(FAKE, FAKE, 140000, 64, 10, FAKE, FAKE, FAKE, NULL) == 1  # 127 C >= 2^24
+    assert L.maddness_build_lut_f32(FAKE, FAKE, 4, 0, 10, FAKE, NULL) == 1
