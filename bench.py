@@ -1,0 +1,218 @@
+"""Throughput of the fused encode + lookup-accumulate path on one MI355X.
+
+A step is one call of the fused path (maddness_matmul: tree encoding of
+every row plus int8 lookup-accumulate and dequantization) over the whole
+batch of the conv3x3_im2col workload (N = 131072 rows, D = 576, C = 32
+codebooks, M = 64 outputs), inputs already resident in HBM.  Prints one JSON
+line with rows/s, the HBM roofline of the fused kernel, the CPU oracle timed
+on a bounded sample of the same workload, and a dense fp32 GEMM of the same
+shape as context.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, published
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "api.hip", "internal.hpp"):
+        with open(os.path.join(ROOT, "paper_2207_05808_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(spec, N) -> int:
+    """Bytes the fused path must move per launch, each counted once: every row
+    of A (4 D bytes; the split columns touch every 64-byte segment of a row),
+    every output (4 M bytes), the int8 table (16 C M bytes), and the trees
+    (4 split ints + 15 thresholds per codebook), scales and offsets."""
+    per_row = 4 * spec.D + 4 * spec.M
+    fixed = 16 * spec.C * spec.M + spec.C * (4 * 4 + 15 * 4) + 2 * 4 * spec.C
+    return N * per_row + fixed
+
+
+def stored_traffic(workload: str, kh: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when it is missing or was taken on a different kernel source."""
+    path = os.path.join(PROFILE_DIR, f"traffic_fused_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_hash") != kh:
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(p, lut, scale, offset, budget_s: float):
+    """The oracle as it stands, on a bounded prefix of the workload's rows."""
+    import oracle
+    o = oracle.get()
+    probe = min(p.N, 2048)
+    t = time.perf_counter()
+    o.matmul(p.A[:probe], p.split, p.thr, lut, scale, offset)
+    per_row = max((time.perf_counter() - t) / probe, 1e-9)
+    rows = int(min(p.N, max(probe, budget_s / per_row)))
+    t = time.perf_counter()
+    o.matmul(p.A[:rows], p.split, p.thr, lut, scale, offset)
+    dt = time.perf_counter() - t
+    return {"value": rows / dt, "unit": "rows/s", "cores": o.max_threads(), "kind": "oracle",
+            "sample": f"first {rows} of {p.N} rows, full encode + int8 lookup-accumulate, "
+                      f"{dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-context", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="also run a plain device copy of this size (for counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "the path shards by rows with no exchange, so a multi-GPU run is not part of this "
+              "build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2207_05808_amd as mdn
+    from paper_2207_05808_amd import workloads as W
+
+    name = args.workload or W.HEADLINE
+    spec = W.SPECS[name]
+    if not spec.quantized:
+        raise SystemExit("bench.py times the int8 fused path; pick a quantized workload")
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    log(f"[bench] drawing workload {name}: N={spec.N} D={spec.D} C={spec.C} M={spec.M}")
+    p = W.make(name)
+    N = p.N
+
+    # two copies of A so that consecutive steps never find their input in the
+    # 256 MB last-level cache (the headline A is 302 MB)
+    A_bufs = [torch.from_numpy(p.A).to(dev) for _ in range(2)]
+    split = torch.from_numpy(p.split).to(dev)
+    thr = torch.from_numpy(p.thr).to(dev)
+    lut, scale, offset = mdn.build_lut(torch.from_numpy(p.P).to(dev), torch.from_numpy(p.B).to(dev))
+    y = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    def step(i):
+        mdn.matmul(A_bufs[i % 2], split, thr, lut, scale, offset, y_out=y)
+
+    log(f"[bench] warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    log(f"[bench] timing {K} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        ev[i][0].record()
+        step(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = wall / K * 1e3
+    avg_kern_s = float(np.mean(kern_ms)) / 1e3
+    value = N / (wall / K)
+    log(f"[bench] wall {ms_per_step * 1e3:.1f} us/step, kernel avg {avg_kern_s * 1e6:.1f} us "
+        f"(min {min(kern_ms) * 1e3:.1f}, max {max(kern_ms) * 1e3:.1f})")
+
+    abytes = algorithmic_bytes(spec, N)
+    achieved = abytes / avg_kern_s / 1e9
+    kh = kernel_source_hash()
+    traffic = stored_traffic(name, kh)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes": abytes, "kernel_us": round(avg_kern_s * 1e6, 2),
+                "kernel": "path_kernel<kFused,int8> (maddness_matmul)", "kernel_source_hash": kh}
+
+    result = {
+        "metric": "rows/sec + achieved HBM GB/s (fraction of peak) for fused encode+LUT matmul",
+        "value": round(value, 1), "unit": "rows/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp32 in / int8 table / int32 accumulate", "data": "synthetic",
+        "config": {"workload": name, "N": N, "D": spec.D, "C": spec.C, "K": 16, "M": spec.M,
+                   "table": "int8 block floating point", "parallelism": "single GPU"},
+        "roofline": roofline,
+    }
+
+    if not args.no_context:
+        # dense fp32 GEMM of the same shape (torch -> hipBLASLt / rocBLAS), TF32 off
+        torch.backends.cuda.matmul.allow_tf32 = False
+        Bd = torch.from_numpy(p.B).to(dev)
+        out = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
+        for _ in range(3):
+            torch.mm(A_bufs[0], Bd, out=out)
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 10
+        g0.record()
+        for i in range(reps):
+            torch.mm(A_bufs[i % 2], Bd, out=out)
+        g1.record()
+        torch.cuda.synchronize()
+        gms = g0.elapsed_time(g1) / reps
+        result["context"] = {"dense_fp32_gemm_us": round(gms * 1e3, 2),
+                             "dense_fp32_gemm_tflops": round(2.0 * N * spec.D * spec.M / (gms / 1e3) / 1e12, 2),
+                             "fused_speedup_vs_gemm": round(gms / 1e3 / avg_kern_s, 3)}
+        del out, Bd
+
+    if args.copy_calibration_mb > 0:
+        nb = args.copy_calibration_mb << 20
+        src = torch.ones(nb // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: {nb} bytes read + {nb} bytes written")
+
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s)")
+        import oracle
+        rl, rs, ro = oracle.get().build_quantized_lut(p.P, p.B)
+        result["cpu_baseline"] = cpu_baseline(p, rl, rs, ro, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -41,8 +41,13 @@ LdsLayout layout(const Shape& s, int nw, int rw, int Dp, int Cp, int lut_bytes) 
   L.thr = take(enc ? s.C * 16 * 4 : 0);
   L.split = take(enc ? s.C * kLevels * 4 : 0);
   L.misc = take(16);
-  L.a = take(enc ? nw * rw * Dp * 4 : 0);
-  L.idx = take(nw * rw * Cp);
+  const bool q8 = s.mode != kEncode && s.elem == kI8;
+  L.sh = take(q8 ? s.C * 4 : 0);
+  L.shp = take(q8 ? (s.C + 7) / 8 * 4 : 0);
+  L.a_wave = enc ? round_up(rw * Dp * 4 + 16, 16) : 0;
+  L.a = take(nw * L.a_wave);
+  L.idx_wave = round_up(rw * Cp + 16, 16);
+  L.idx = take(nw * L.idx_wave);
   L.total = off;
   return L;
 }

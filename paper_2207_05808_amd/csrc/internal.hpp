@@ -21,8 +21,12 @@ struct LdsLayout {
   int thr;     // [C][16] fp32 thresholds (heap order, slot 15 unused)
   int split;   // [C][4] int32 split columns (clamped to [0, D))
   int misc;    // int32[4]: e_min, max shift, bias32 bits, step bits
-  int a;       // per wave: [RW][Dp] fp32 staged rows of A
-  int idx;     // per wave: [RW][Cp] uint8 indices
+  int sh;      // [C] int32 per-codebook shift e_c - e_min
+  int shp;     // [ceil(C/8)] uint32: the shifts as nibbles, 8 codebooks per word
+  int a;       // per wave: [RW][Dp] fp32 staged rows of A, then a 16-byte dummy slot
+  int a_wave;  //   bytes per wave of the region above
+  int idx;     // per wave: [RW][Cp] uint8 indices, then a 16-byte dummy slot
+  int idx_wave;
   int total;
 };
 

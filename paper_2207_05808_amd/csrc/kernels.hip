@@ -30,6 +30,8 @@ namespace mdn {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 #define MDN_CONST __attribute__((address_space(4)))
+typedef __attribute__((address_space(3))) char lds_t;           // 32-bit LDS addresses
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -48,67 +50,173 @@ __device__ __forceinline__ uint32_t bfe(uint32_t v, int off, int width) {
 
 // Rows of a strided 2-D byte array, RW rows per chunk, prefetched in 16-byte
 // units through VGPRs.  Unit j of lane l is u = l + 64 j; it belongs to row
-// u / upr and column unit u % upr.
+// u / upr and column unit u % upr.  Loads and LDS stores carry no per-lane
+// predicate (a predicate would make the compiler wait for every load in
+// turn): idle units re-read unit 0 and land in a per-wavefront dummy slot,
+// and in the last, partial chunk the rows past N re-read the last valid row.
 template <int PF, bool NT>
 struct Prefetch {
   u32x4 buf[PF > 0 ? PF : 1];
   int goff[PF > 0 ? PF : 1];   // byte offset from the chunk's first row in global memory
-  int loff[PF > 0 ? PF : 1];   // byte offset in the LDS buffer, -1 when idle
-  int rrow[PF > 0 ? PF : 1];   // row within the chunk (1 << 30 when idle)
+  int loff[PF > 0 ? PF : 1];   // byte offset in the LDS buffer (dummy slot when idle)
+  int rrow[PF > 0 ? PF : 1];   // row within the chunk (0 when idle)
 
-  __device__ __forceinline__ void init(int lane, int rw, int upr, int64_t src_rs, int lds_rs) {
+  __device__ __forceinline__ void init(int lane, int rw, int upr, int64_t src_rs, int lds_rs, int dummy) {
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
       const int u = lane + 64 * j;
-      if (u < rw * upr) {
-        const int r = u / upr;
-        const int col = u - r * upr;
-        goff[j] = (int)(r * src_rs) + col * 16;
-        loff[j] = r * lds_rs + col * 16;
-        rrow[j] = r;
-      } else {
-        goff[j] = 0;
-        loff[j] = -1;
-        rrow[j] = 1 << 30;
+      const bool live = u < rw * upr;
+      const int r = live ? u / upr : 0;
+      const int col = live ? u - r * upr : 0;
+      goff[j] = (int)(r * src_rs) + col * 16;
+      loff[j] = live ? r * lds_rs + col * 16 : dummy;
+      rrow[j] = r;
+    }
+  }
+  __device__ __forceinline__ u32x4 ld(const char* p) const {
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    return NT ? __builtin_nontemporal_load(q) : *q;
+  }
+  // rows_valid is wavefront-uniform, so the tail test is a scalar branch
+  __device__ __forceinline__ void load(const char* base, int rows_valid, int rw, int src_rs) {
+    if (rows_valid == rw) {
+#pragma unroll
+      for (int j = 0; j < PF; ++j) buf[j] = ld(base + goff[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < PF; ++j) {
+        const int over = max(rrow[j] - (rows_valid - 1), 0);
+        buf[j] = ld(base + goff[j] - over * src_rs);
       }
     }
   }
-  __device__ __forceinline__ void load(const char* base, int rows_valid) {
+  __device__ __forceinline__ void store(lds_t* lds) const {
 #pragma unroll
-    for (int j = 0; j < PF; ++j) {
-      if (rrow[j] < rows_valid) {
-        const u32x4* p = reinterpret_cast<const u32x4*>(base + goff[j]);
-        buf[j] = NT ? __builtin_nontemporal_load(p) : *p;
-      }
-    }
-  }
-  __device__ __forceinline__ void store(char* lds) const {
-#pragma unroll
-    for (int j = 0; j < PF; ++j)
-      if (loff[j] >= 0) *reinterpret_cast<u32x4*>(lds + loff[j]) = buf[j];
+    for (int j = 0; j < PF; ++j) *reinterpret_cast<lds_u32x4*>(lds + loff[j]) = buf[j];
   }
 };
+
+typedef __attribute__((address_space(3))) float lds_f32;
+typedef __attribute__((address_space(3))) int lds_i32;
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
+
+// Accumulate one chunk of rows over the LUT tile.  Lane (ar, cg) owns column
+// quads q = cg + u * LPR of row ar (u < UQ); quads past the tile are clamped
+// to the last one (read, never stored), so no load carries a predicate.
+// Codebooks go in groups of 8: two idx dwords and one packed-shift dword
+// per group, then 8 independent LDS reads, then the 32 (or 8 x 4) updates.
+template <int ELEM, int UQ, bool DOT>
+__device__ __forceinline__ void accumulate(const lds_t* ir, const lds_t* const* lq, int C, int rs,
+                                           const lds_t* s_shp, const lds_i32* s_sh,
+                                           int (&iacc)[UQ][4], float (&facc)[UQ][4]) {
+  constexpr int kQB = ELEM == kI8 ? 4 : 16;
+  (void)kQB;
+  const int C8 = C & ~7;
+  int c0 = 0;
+  for (; c0 < C8; c0 += 8) {
+    const uint32_t k0 = *reinterpret_cast<const lds_u32*>(ir + c0);
+    const uint32_t k1 = *reinterpret_cast<const lds_u32*>(ir + c0 + 4);
+    if (ELEM == kI8) {
+      int v[8][UQ];
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const int k = (int)bfe(b < 4 ? k0 : k1, 8 * (b & 3), 4);
+        const int off = (int)__umul24((uint32_t)((c0 + b) * kK + k), (uint32_t)rs);
+#pragma unroll
+        for (int u = 0; u < UQ; ++u) v[b][u] = *reinterpret_cast<const lds_i32*>(lq[u] + off);
+      }
+      if (DOT) {
+        const uint32_t shw = (uint32_t)uniform((int)*reinterpret_cast<const lds_u32*>(s_shp + (c0 >> 1)));
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const int w = 1 << bfe(shw, 4 * b, 4);
+#pragma unroll
+          for (int u = 0; u < UQ; ++u) {
+            iacc[u][0] = __builtin_amdgcn_sdot4(v[b][u], w, iacc[u][0], false);
+            iacc[u][1] = __builtin_amdgcn_sdot4(v[b][u], w << 8, iacc[u][1], false);
+            iacc[u][2] = __builtin_amdgcn_sdot4(v[b][u], w << 16, iacc[u][2], false);
+            iacc[u][3] = __builtin_amdgcn_sdot4(v[b][u], w << 24, iacc[u][3], false);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const int sh = uniform(s_sh[c0 + b]);
+#pragma unroll
+          for (int u = 0; u < UQ; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) iacc[u][e] += __builtin_amdgcn_sbfe(v[b][u], 8 * e, 8) << sh;
+        }
+      }
+    } else {
+      f32x4 v[8][UQ];
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const int k = (int)bfe(b < 4 ? k0 : k1, 8 * (b & 3), 4);
+        const int off = (int)__umul24((uint32_t)((c0 + b) * kK + k), (uint32_t)rs);
+#pragma unroll
+        for (int u = 0; u < UQ; ++u) v[b][u] = *reinterpret_cast<const lds_f32x4*>(lq[u] + off);
+      }
+#pragma unroll
+      for (int b = 0; b < 8; ++b)   // codebooks strictly in ascending order
+#pragma unroll
+        for (int u = 0; u < UQ; ++u) {
+          facc[u][0] = facc[u][0] + v[b][u].x;
+          facc[u][1] = facc[u][1] + v[b][u].y;
+          facc[u][2] = facc[u][2] + v[b][u].z;
+          facc[u][3] = facc[u][3] + v[b][u].w;
+        }
+    }
+  }
+  for (; c0 < C; ++c0) {
+    const int k = (int)(*reinterpret_cast<const lds_u8*>(ir + c0) & 15u);
+    const int off = (int)__umul24((uint32_t)(c0 * kK + k), (uint32_t)rs);
+    if (ELEM == kI8) {
+      const int sh = uniform(s_sh[c0]);
+#pragma unroll
+      for (int u = 0; u < UQ; ++u) {
+        const int v = *reinterpret_cast<const lds_i32*>(lq[u] + off);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) iacc[u][e] += __builtin_amdgcn_sbfe(v, 8 * e, 8) << sh;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < UQ; ++u) {
+        const f32x4 v = *reinterpret_cast<const lds_f32x4*>(lq[u] + off);
+        facc[u][0] = facc[u][0] + v.x;
+        facc[u][1] = facc[u][1] + v.y;
+        facc[u][2] = facc[u][2] + v.z;
+        facc[u][3] = facc[u][3] + v.w;
+      }
+    }
+  }
+}
 
 template <int MODE, int ELEM, int PF, int UQ>
 __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   constexpr bool kEnc = MODE != kAccum;
   constexpr bool kAcc = MODE != kEncode;
   constexpr int kQB = ELEM == kI8 ? 4 : 16;  // bytes of one 4-column quad of a LUT row
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  lds_t* smem = (lds_t*)smem_raw;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = uniform(tid >> 6);   // wavefront-uniform: loop control stays scalar
   const int nw = blockDim.x >> 6;
   const int C = a.C;
   const int m0 = blockIdx.y * a.Mt;
   const int mt = min(a.Mt, a.M - m0);   // columns of this tile
   const int nq = (mt + 3) >> 2;         // column quads of this tile
 
-  char* s_lut = smem + a.L.lut;
-  float* s_thr = reinterpret_cast<float*>(smem + a.L.thr);
-  int* s_split = reinterpret_cast<int*>(smem + a.L.split);
-  int* s_misc = reinterpret_cast<int*>(smem + a.L.misc);
+  lds_t* s_lut = smem + a.L.lut;
+  lds_f32* s_thr = reinterpret_cast<lds_f32*>(smem + a.L.thr);
+  lds_i32* s_split = reinterpret_cast<lds_i32*>(smem + a.L.split);
+  lds_i32* s_misc = reinterpret_cast<lds_i32*>(smem + a.L.misc);
+  lds_i32* s_sh = reinterpret_cast<lds_i32*>(smem + a.L.sh);
+  lds_t* s_shp = smem + a.L.shp;
 
   // ---------------- workgroup prologue ----------------
   if (kAcc) {
@@ -124,8 +232,7 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
         for (int u = tid; u < total; u += blockDim.x) {
           const int row = u >> qlog, q = u & ((1 << qlog) - 1);
           if (q < nq)
-            *reinterpret_cast<uint32_t*>(s_lut + row * a.lut_rs + 4 * q) =
-                src[(int64_t)row * m4 + (m0 >> 2) + q];
+            *reinterpret_cast<lds_u32*>(s_lut + row * a.lut_rs + 4 * q) = src[(int64_t)row * m4 + (m0 >> 2) + q];
         }
       } else {
         const int8_t* src = reinterpret_cast<const int8_t*>(a.lut);
@@ -140,7 +247,7 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
       for (int u = tid; u < (rows << (qlog + 2)); u += blockDim.x) {
         const int row = u >> (qlog + 2), j = u & ((4 << qlog) - 1);
         if (j < 4 * nq)
-          *reinterpret_cast<float*>(s_lut + row * a.lut_rs + 4 * j) =
+          *reinterpret_cast<lds_f32*>(s_lut + row * a.lut_rs + 4 * j) =
               (j < mt) ? src[(int64_t)row * a.M + m0 + j] : 0.0f;
       }
     }
@@ -151,31 +258,42 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
       s_thr[u] = (j < kNodes) ? a.thr[c * kNodes + j] : 0.0f;
     }
     for (int u = tid; u < C * kLevels; u += blockDim.x) {
-      const unsigned s = (unsigned)a.split[u];
-      s_split[u] = (int)min(s, (unsigned)(a.D - 1));  // memory safety only
+      const unsigned sp = (unsigned)a.split[u];
+      s_split[u] = (int)min(sp, (unsigned)(a.D - 1));  // memory safety only
     }
   }
   if (kAcc && ELEM == kI8) {
     if (tid == 0) { s_misc[0] = 1 << 30; s_misc[1] = 0; }
     __syncthreads();
     const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
-    for (int c = tid; c < C; c += blockDim.x) atomicMin(&s_misc[0], exp_of_bits(sb[c]));
+    for (int c = tid; c < C; c += blockDim.x) atomicMin((int*)&s_misc[0], exp_of_bits(sb[c]));
     __syncthreads();
     const int emin = s_misc[0];
-    for (int c = tid; c < C; c += blockDim.x) atomicMax(&s_misc[1], exp_of_bits(sb[c]) - emin);
+    for (int c = tid; c < C; c += blockDim.x) {
+      const int sh = exp_of_bits(sb[c]) - emin;
+      s_sh[c] = sh;
+      atomicMax((int*)&s_misc[1], sh);
+    }
     if (tid == 0) {
-      double s = 0.0;  // bias32: double sum over codebooks in ascending order
-      for (int c = 0; c < C; ++c) s += (double)a.offset[c];
-      s_misc[2] = __float_as_int((float)s);
+      double sum = 0.0;  // bias32: double sum over codebooks in ascending order
+      for (int c = 0; c < C; ++c) sum += (double)a.offset[c];
+      s_misc[2] = __float_as_int((float)sum);
       s_misc[3] = __float_as_int(__builtin_ldexpf(1.0f, emin));
+    }
+    __syncthreads();
+    // shifts packed as nibbles, 8 codebooks per dword (used while every shift <= 6)
+    for (int g = tid; g < (C + 7) / 8; g += blockDim.x) {
+      uint32_t w = 0;
+      for (int b = 0; b < 8 && 8 * g + b < C; ++b) w |= (uint32_t)(min(s_sh[8 * g + b], 15)) << (4 * b);
+      *reinterpret_cast<lds_u32*>(s_shp + 4 * g) = w;
     }
   }
   __syncthreads();
 
   // ---------------- per-wavefront chunk loop ----------------
   const int RW = a.RW;
-  float* sA = reinterpret_cast<float*>(smem + a.L.a) + (size_t)wave * RW * a.Dp;
-  uint8_t* sI = reinterpret_cast<uint8_t*>(smem + a.L.idx) + (size_t)wave * RW * a.Cp;
+  lds_t* sA = smem + a.L.a + wave * a.L.a_wave;
+  lds_t* sI = smem + a.L.idx + wave * a.L.idx_wave;
   const int64_t tw = (int64_t)gridDim.x * nw;
   int64_t ch = (int64_t)blockIdx.x * nw + wave;
 
@@ -184,11 +302,11 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   const int64_t src_rs = kEnc ? a.lda * 4 : (int64_t)C;  // bytes between rows
   Prefetch<PF, kEnc> pf;
   if (PF > 0) {
-    if (kEnc) pf.init(lane, RW, a.D >> 2, src_rs, a.Dp * 4);
-    else      pf.init(lane, RW, C >> 4, src_rs, a.Cp);
+    if (kEnc) pf.init(lane, RW, a.D >> 2, src_rs, a.Dp * 4, RW * a.Dp * 4);
+    else      pf.init(lane, RW, C >> 4, src_rs, a.Cp, RW * a.Cp);
     if (ch < a.nchunks) {
       const int64_t row0 = ch << a.rw_log2;
-      pf.load(src0 + row0 * src_rs, (int)min<int64_t>(RW, a.N - row0));
+      pf.load(src0 + row0 * src_rs, (int)min<int64_t>(RW, a.N - row0), RW, (int)src_rs);
     }
   }
 
@@ -197,32 +315,34 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   const int ar = lane >> lpr_log2;                  // row of the chunk
   const int cg = lane & ((1 << lpr_log2) - 1);      // first column quad
   const int LPR = 1 << lpr_log2;
-  int emin = 0, maxsh = 0;
+  const lds_t* lq[UQ];
+#pragma unroll
+  for (int u = 0; u < UQ; ++u) lq[u] = s_lut + min(cg + u * LPR, nq - 1) * kQB;
+  int maxsh = 0;
   float step = 1.0f, bias = 0.0f;
   if (kAcc && ELEM == kI8) {
-    emin = uniform(s_misc[0]);
     maxsh = uniform(s_misc[1]);
     bias = __int_as_float(uniform(s_misc[2]));
     step = __int_as_float(uniform(s_misc[3]));
   }
-  const MDN_CONST uint32_t* cscale = (const MDN_CONST uint32_t*)(uintptr_t)a.scale;
 
   for (; ch < a.nchunks; ch += tw) {
     const int64_t row0 = ch << a.rw_log2;
     const int rows_valid = (int)min<int64_t>(RW, a.N - row0);
 
-    // 1. stage this chunk's rows in LDS
+    // 1. stage this chunk's rows in LDS, start loading the next chunk
     if (PF > 0) {
-      pf.store(kEnc ? reinterpret_cast<char*>(sA) : reinterpret_cast<char*>(sI));
+      pf.store(kEnc ? sA : sI);
       const int64_t nx = ch + tw;
       if (nx < a.nchunks) {
         const int64_t nrow0 = nx << a.rw_log2;
-        pf.load(src0 + nrow0 * src_rs, (int)min<int64_t>(RW, a.N - nrow0));
+        pf.load(src0 + nrow0 * src_rs, (int)min<int64_t>(RW, a.N - nrow0), RW, (int)src_rs);
       }
     } else if (kEnc) {
       for (int r = 0; r < rows_valid; ++r) {
         const float* src = a.A + (row0 + r) * a.lda;
-        for (int col = lane; col < a.D; col += 64) sA[r * a.Dp + col] = src[col];
+        for (int col = lane; col < a.D; col += 64)
+          reinterpret_cast<lds_f32*>(sA)[r * a.Dp + col] = src[col];
       }
     } else {
       for (int r = 0; r < rows_valid; ++r) {
@@ -234,12 +354,13 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
 
     // 2. encode: 4 comparisons per (row, codebook)
     if (kEnc) {
+      const lds_f32* xa = reinterpret_cast<const lds_f32*>(sA);
       for (int p = lane; p < RW * C; p += 64) {
         const int r = (C == 1) ? p : (int)__umulhi((uint32_t)p, a.c_magic);
         const int c = p - r * C;
-        const float* xr = sA + r * a.Dp;
-        const int* sp = s_split + c * kLevels;
-        const float* th = s_thr + c * 16;
+        const lds_f32* xr = xa + r * a.Dp;
+        const lds_i32* sp = s_split + c * kLevels;
+        const lds_f32* th = s_thr + c * 16;
         int i = (xr[sp[0]] > th[0]) ? 1 : 0;
         i = 2 * i + ((xr[sp[1]] > th[1 + i]) ? 1 : 0);
         i = 2 * i + ((xr[sp[2]] > th[3 + i]) ? 1 : 0);
@@ -250,7 +371,7 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
       if (a.idx_out != nullptr) {
         if (a.Cp == C && ((reinterpret_cast<uintptr_t>(a.idx_out) & 3) == 0)) {
           uint32_t* dst = reinterpret_cast<uint32_t*>(a.idx_out + row0 * C);
-          const uint32_t* s32 = reinterpret_cast<const uint32_t*>(sI);
+          const lds_u32* s32 = reinterpret_cast<const lds_u32*>(sI);
           const int n32 = (rows_valid * C) >> 2;
           for (int u = lane; u < n32; u += 64) dst[u] = s32[u];
         } else {
@@ -262,130 +383,46 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
 
     // 3. accumulate + 4. epilogue
     if (kAcc) {
-      const uint8_t* ir = sI + ar * a.Cp;
-      const char* lut_lane = s_lut + cg * kQB;
+      const lds_t* ir = sI + ar * a.Cp;
       const int64_t row = row0 + ar;
+      int iacc[UQ][4];
+      float facc[UQ][4];
+#pragma unroll
+      for (int u = 0; u < UQ; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { iacc[u][e] = 0; facc[u][e] = 0.0f; }
       if (ELEM == kI8) {
-        int acc[UQ][4];
-#pragma unroll
-        for (int u = 0; u < UQ; ++u)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[u][b] = 0;
-        if (maxsh <= 6) {
-          for (int c0 = 0; c0 < C; c0 += 4) {
-            const uint32_t kw = *reinterpret_cast<const uint32_t*>(ir + c0);
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-              const int c = c0 + b;
-              if (c < C) {
-                const int w = 1 << (exp_of_bits(cscale[c]) - emin);
-                const int k = (int)bfe(kw, 8 * b, 4);
-                const char* rowp = lut_lane + (c * kK + k) * a.lut_rs;
-#pragma unroll
-                for (int u = 0; u < UQ; ++u) {
-                  if (UQ == 1 || cg + u * LPR < nq) {
-                    const int v = *reinterpret_cast<const int*>(rowp + u * LPR * kQB);
-                    acc[u][0] = __builtin_amdgcn_sdot4(v, w, acc[u][0], false);
-                    acc[u][1] = __builtin_amdgcn_sdot4(v, w << 8, acc[u][1], false);
-                    acc[u][2] = __builtin_amdgcn_sdot4(v, w << 16, acc[u][2], false);
-                    acc[u][3] = __builtin_amdgcn_sdot4(v, w << 24, acc[u][3], false);
-                  }
-                }
-              }
-            }
-          }
-        } else {
-          for (int c0 = 0; c0 < C; c0 += 4) {
-            const uint32_t kw = *reinterpret_cast<const uint32_t*>(ir + c0);
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-              const int c = c0 + b;
-              if (c < C) {
-                const int sh = exp_of_bits(cscale[c]) - emin;
-                const int k = (int)bfe(kw, 8 * b, 4);
-                const char* rowp = lut_lane + (c * kK + k) * a.lut_rs;
-#pragma unroll
-                for (int u = 0; u < UQ; ++u) {
-                  if (UQ == 1 || cg + u * LPR < nq) {
-                    const int v = *reinterpret_cast<const int*>(rowp + u * LPR * kQB);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                      acc[u][e] += __builtin_amdgcn_sbfe(v, 8 * e, 8) << sh;
-                  }
-                }
-              }
-            }
-          }
-        }
-        if (ar < rows_valid) {
-#pragma unroll
-          for (int u = 0; u < UQ; ++u) {
-            const int q = cg + u * LPR;
-            if (q < nq) {
-              const int mloc = 4 * q;
-              float o[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) o[e] = __builtin_fmaf((float)acc[u][e], step, bias);
-              float* yp = a.y ? a.y + row * a.M + m0 + mloc : nullptr;
-              int32_t* ap = a.acc ? a.acc + row * a.M + m0 + mloc : nullptr;
-              if (a.vec_out && mloc + 4 <= mt) {
-                if (yp) __builtin_nontemporal_store((f32x4){o[0], o[1], o[2], o[3]}, reinterpret_cast<f32x4*>(yp));
-                if (ap) __builtin_nontemporal_store((u32x4){(uint32_t)acc[u][0], (uint32_t)acc[u][1],
-                                                            (uint32_t)acc[u][2], (uint32_t)acc[u][3]},
-                                                    reinterpret_cast<u32x4*>(ap));
-              } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  if (mloc + e < mt) {
-                    if (yp) yp[e] = o[e];
-                    if (ap) ap[e] = acc[u][e];
-                  }
-                }
-              }
-            }
-          }
-        }
+        if (maxsh <= 6)
+          accumulate<ELEM, UQ, true>(ir, lq, C, a.lut_rs, s_shp, s_sh, iacc, facc);
+        else
+          accumulate<ELEM, UQ, false>(ir, lq, C, a.lut_rs, s_shp, s_sh, iacc, facc);
       } else {
-        float acc[UQ][4];
+        accumulate<ELEM, UQ, false>(ir, lq, C, a.lut_rs, s_shp, s_sh, iacc, facc);
+      }
+      if (ar < rows_valid) {
 #pragma unroll
-        for (int u = 0; u < UQ; ++u)
+        for (int u = 0; u < UQ; ++u) {
+          const int q = cg + u * LPR;
+          if (q < nq) {
+            const int mloc = 4 * q;
+            float o[4];
 #pragma unroll
-          for (int b = 0; b < 4; ++b) acc[u][b] = 0.0f;
-        for (int c0 = 0; c0 < C; c0 += 4) {
-          const uint32_t kw = *reinterpret_cast<const uint32_t*>(ir + c0);
+            for (int e = 0; e < 4; ++e)
+              o[e] = (ELEM == kI8) ? __builtin_fmaf((float)iacc[u][e], step, bias) : facc[u][e];
+            float* yp = a.y ? a.y + row * a.M + m0 + mloc : nullptr;
+            int32_t* ap = (ELEM == kI8 && a.acc) ? a.acc + row * a.M + m0 + mloc : nullptr;
+            if (a.vec_out && mloc + 4 <= mt) {
+              if (yp) __builtin_nontemporal_store((f32x4){o[0], o[1], o[2], o[3]}, reinterpret_cast<f32x4*>(yp));
+              if (ap) __builtin_nontemporal_store((u32x4){(uint32_t)iacc[u][0], (uint32_t)iacc[u][1],
+                                                          (uint32_t)iacc[u][2], (uint32_t)iacc[u][3]},
+                                                  reinterpret_cast<u32x4*>(ap));
+            } else {
 #pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int c = c0 + b;
-            if (c < C) {
-              const int k = (int)bfe(kw, 8 * b, 4);
-              const char* rowp = lut_lane + (c * kK + k) * a.lut_rs;
-#pragma unroll
-              for (int u = 0; u < UQ; ++u) {
-                if (UQ == 1 || cg + u * LPR < nq) {
-                  const f32x4 v = *reinterpret_cast<const f32x4*>(rowp + u * LPR * kQB);
-                  acc[u][0] = acc[u][0] + v.x;
-                  acc[u][1] = acc[u][1] + v.y;
-                  acc[u][2] = acc[u][2] + v.z;
-                  acc[u][3] = acc[u][3] + v.w;
+              for (int e = 0; e < 4; ++e) {
+                if (mloc + e < mt) {
+                  if (yp) yp[e] = o[e];
+                  if (ap) ap[e] = iacc[u][e];
                 }
-              }
-            }
-          }
-        }
-        if (ar < rows_valid) {
-#pragma unroll
-          for (int u = 0; u < UQ; ++u) {
-            const int q = cg + u * LPR;
-            if (q < nq) {
-              const int mloc = 4 * q;
-              float* yp = a.y + row * a.M + m0 + mloc;
-              if (a.vec_out && mloc + 4 <= mt) {
-                __builtin_nontemporal_store((f32x4){acc[u][0], acc[u][1], acc[u][2], acc[u][3]},
-                                            reinterpret_cast<f32x4*>(yp));
-              } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  if (mloc + e < mt) yp[e] = acc[u][e];
               }
             }
           }
