@@ -25,6 +25,9 @@
 //      with 16-byte non-temporal stores.
 #include "internal.hpp"
 
+#include <atomic>
+#include <mutex>
+
 namespace mdn {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -102,73 +105,85 @@ typedef __attribute__((address_space(3))) uint32_t lds_u32;
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
 
+// One group of G codebooks (G = 8 or 16) of the accumulate: all idx words and
+// all G x UQ LUT quads are read first (independent LDS reads), then the
+// updates run.  int8 with DOT: v_dot4c_i32_i8 against weight 2^sh << 8e picks
+// byte e of the quad, sign-extends it and shifts it; fp32: ordered adds.
+template <int ELEM, int UQ, bool DOT, int G>
+__device__ __forceinline__ void acc_group(int c0, const lds_t* ir, const lds_t* const* lq, int rs,
+                                          const lds_t* s_shp, const lds_i32* s_sh,
+                                          int (&iacc)[UQ][4], float (&facc)[UQ][4]) {
+  uint32_t kw[G / 4];
+#pragma unroll
+  for (int q = 0; q < G / 4; ++q) kw[q] = *reinterpret_cast<const lds_u32*>(ir + c0 + 4 * q);
+  if (ELEM == kI8) {
+    int v[G][UQ];
+#pragma unroll
+    for (int b = 0; b < G; ++b) {
+      const int k = (int)bfe(kw[b >> 2], 8 * (b & 3), 4);
+      const int off = (int)__umul24((uint32_t)((c0 + b) * kK + k), (uint32_t)rs);
+#pragma unroll
+      for (int u = 0; u < UQ; ++u) v[b][u] = *reinterpret_cast<const lds_i32*>(lq[u] + off);
+    }
+    if (DOT) {
+      uint32_t shw[G / 8];
+#pragma unroll
+      for (int q = 0; q < G / 8; ++q)
+        shw[q] = (uint32_t)uniform((int)*reinterpret_cast<const lds_u32*>(s_shp + (c0 >> 1) + 4 * q));
+#pragma unroll
+      for (int b = 0; b < G; ++b) {
+        const int w = 1 << bfe(shw[b >> 3], 4 * (b & 7), 4);
+#pragma unroll
+        for (int u = 0; u < UQ; ++u) {
+          iacc[u][0] = __builtin_amdgcn_sdot4(v[b][u], w, iacc[u][0], false);
+          iacc[u][1] = __builtin_amdgcn_sdot4(v[b][u], w << 8, iacc[u][1], false);
+          iacc[u][2] = __builtin_amdgcn_sdot4(v[b][u], w << 16, iacc[u][2], false);
+          iacc[u][3] = __builtin_amdgcn_sdot4(v[b][u], w << 24, iacc[u][3], false);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int b = 0; b < G; ++b) {
+        const int sh = uniform(s_sh[c0 + b]);
+#pragma unroll
+        for (int u = 0; u < UQ; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) iacc[u][e] += __builtin_amdgcn_sbfe(v[b][u], 8 * e, 8) << sh;
+      }
+    }
+  } else {
+    f32x4 v[G][UQ];
+#pragma unroll
+    for (int b = 0; b < G; ++b) {
+      const int k = (int)bfe(kw[b >> 2], 8 * (b & 3), 4);
+      const int off = (int)__umul24((uint32_t)((c0 + b) * kK + k), (uint32_t)rs);
+#pragma unroll
+      for (int u = 0; u < UQ; ++u) v[b][u] = *reinterpret_cast<const lds_f32x4*>(lq[u] + off);
+    }
+#pragma unroll
+    for (int b = 0; b < G; ++b)   // codebooks strictly in ascending order
+#pragma unroll
+      for (int u = 0; u < UQ; ++u) {
+        facc[u][0] = facc[u][0] + v[b][u].x;
+        facc[u][1] = facc[u][1] + v[b][u].y;
+        facc[u][2] = facc[u][2] + v[b][u].z;
+        facc[u][3] = facc[u][3] + v[b][u].w;
+      }
+  }
+}
+
 // Accumulate one chunk of rows over the LUT tile.  Lane (ar, cg) owns column
 // quads q = cg + u * LPR of row ar (u < UQ); quads past the tile are clamped
 // to the last one (read, never stored), so no load carries a predicate.
-// Codebooks go in groups of 8: two idx dwords and one packed-shift dword
-// per group, then 8 independent LDS reads, then the 32 (or 8 x 4) updates.
 template <int ELEM, int UQ, bool DOT>
 __device__ __forceinline__ void accumulate(const lds_t* ir, const lds_t* const* lq, int C, int rs,
                                            const lds_t* s_shp, const lds_i32* s_sh,
                                            int (&iacc)[UQ][4], float (&facc)[UQ][4]) {
-  constexpr int kQB = ELEM == kI8 ? 4 : 16;
-  (void)kQB;
-  const int C8 = C & ~7;
   int c0 = 0;
-  for (; c0 < C8; c0 += 8) {
-    const uint32_t k0 = *reinterpret_cast<const lds_u32*>(ir + c0);
-    const uint32_t k1 = *reinterpret_cast<const lds_u32*>(ir + c0 + 4);
-    if (ELEM == kI8) {
-      int v[8][UQ];
-#pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const int k = (int)bfe(b < 4 ? k0 : k1, 8 * (b & 3), 4);
-        const int off = (int)__umul24((uint32_t)((c0 + b) * kK + k), (uint32_t)rs);
-#pragma unroll
-        for (int u = 0; u < UQ; ++u) v[b][u] = *reinterpret_cast<const lds_i32*>(lq[u] + off);
-      }
-      if (DOT) {
-        const uint32_t shw = (uint32_t)uniform((int)*reinterpret_cast<const lds_u32*>(s_shp + (c0 >> 1)));
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-          const int w = 1 << bfe(shw, 4 * b, 4);
-#pragma unroll
-          for (int u = 0; u < UQ; ++u) {
-            iacc[u][0] = __builtin_amdgcn_sdot4(v[b][u], w, iacc[u][0], false);
-            iacc[u][1] = __builtin_amdgcn_sdot4(v[b][u], w << 8, iacc[u][1], false);
-            iacc[u][2] = __builtin_amdgcn_sdot4(v[b][u], w << 16, iacc[u][2], false);
-            iacc[u][3] = __builtin_amdgcn_sdot4(v[b][u], w << 24, iacc[u][3], false);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-          const int sh = uniform(s_sh[c0 + b]);
-#pragma unroll
-          for (int u = 0; u < UQ; ++u)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) iacc[u][e] += __builtin_amdgcn_sbfe(v[b][u], 8 * e, 8) << sh;
-        }
-      }
-    } else {
-      f32x4 v[8][UQ];
-#pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const int k = (int)bfe(b < 4 ? k0 : k1, 8 * (b & 3), 4);
-        const int off = (int)__umul24((uint32_t)((c0 + b) * kK + k), (uint32_t)rs);
-#pragma unroll
-        for (int u = 0; u < UQ; ++u) v[b][u] = *reinterpret_cast<const lds_f32x4*>(lq[u] + off);
-      }
-#pragma unroll
-      for (int b = 0; b < 8; ++b)   // codebooks strictly in ascending order
-#pragma unroll
-        for (int u = 0; u < UQ; ++u) {
-          facc[u][0] = facc[u][0] + v[b][u].x;
-          facc[u][1] = facc[u][1] + v[b][u].y;
-          facc[u][2] = facc[u][2] + v[b][u].z;
-          facc[u][3] = facc[u][3] + v[b][u].w;
-        }
-    }
+  for (; c0 + 16 <= C; c0 += 16) acc_group<ELEM, UQ, DOT, 16>(c0, ir, lq, rs, s_shp, s_sh, iacc, facc);
+  if (c0 + 8 <= C) {
+    acc_group<ELEM, UQ, DOT, 8>(c0, ir, lq, rs, s_shp, s_sh, iacc, facc);
+    c0 += 8;
   }
   for (; c0 < C; ++c0) {
     const int k = (int)(*reinterpret_cast<const lds_u8*>(ir + c0) & 15u);
@@ -192,6 +207,25 @@ __device__ __forceinline__ void accumulate(const lds_t* ir, const lds_t* const* 
       }
     }
   }
+}
+
+// One tree walk with the codebook's 15 thresholds in registers, passed as 15
+// scalars (an array or struct would let the compiler turn a select between
+// two elements into one dynamically indexed load and push it to scratch).
+// The four compared values are independent loads; each level's threshold is
+// selected by the decisions above it, with no memory access.
+#define MDN_TREE_PARAMS float t0, float t1, float t2, float t3, float t4, float t5, float t6, \
+  float t7, float t8, float t9, float t10, float t11, float t12, float t13, float t14
+#define MDN_TREE_ARGS t0, t1, t2, t3, t4, t5, t6, t7, t8, t9, t10, t11, t12, t13, t14
+__device__ __forceinline__ int tree_walk(float x0, float x1, float x2, float x3, MDN_TREE_PARAMS) {
+  const bool b0 = x0 > t0;
+  const bool b1 = x1 > (b0 ? t2 : t1);
+  const float v2 = b0 ? (b1 ? t6 : t5) : (b1 ? t4 : t3);
+  const bool b2 = x2 > v2;
+  const float lo = b1 ? (b2 ? t10 : t9) : (b2 ? t8 : t7);
+  const float hi = b1 ? (b2 ? t14 : t13) : (b2 ? t12 : t11);
+  const bool b3 = x3 > (b0 ? hi : lo);
+  return ((int)b0 << 3) | ((int)b1 << 2) | ((int)b2 << 1) | (int)b3;
 }
 
 template <int MODE, int ELEM, int PF, int UQ>
@@ -318,6 +352,26 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   const lds_t* lq[UQ];
 #pragma unroll
   for (int u = 0; u < UQ; ++u) lq[u] = s_lut + min(cg + u * LPR, nq - 1) * kQB;
+  // register-resident tree: when C divides 64, lane l always handles
+  // codebook l % C of rows l / C + j * (64 / C), j < RW * C / 64
+  float t0 = 0, t1 = 0, t2 = 0, t3 = 0, t4 = 0, t5 = 0, t6 = 0, t7 = 0, t8 = 0, t9 = 0, t10 = 0,
+        t11 = 0, t12 = 0, t13 = 0, t14 = 0;
+  int sc0 = 0, sc1 = 0, sc2 = 0, sc3 = 0;
+  int cl = 0, er0 = 0, erstep = 1, enr = 0;
+  if (kEnc && a.enc_reg) {
+    cl = lane & (C - 1);
+    er0 = lane >> a.c_log2;
+    erstep = 64 >> a.c_log2;
+    enr = (RW * C) >> 6;
+    const lds_f32* th = s_thr + cl * 16;
+    t0 = th[0]; t1 = th[1]; t2 = th[2]; t3 = th[3]; t4 = th[4]; t5 = th[5]; t6 = th[6];
+    t7 = th[7]; t8 = th[8]; t9 = th[9]; t10 = th[10]; t11 = th[11]; t12 = th[12]; t13 = th[13];
+    t14 = th[14];
+    sc0 = s_split[cl * kLevels + 0];
+    sc1 = s_split[cl * kLevels + 1];
+    sc2 = s_split[cl * kLevels + 2];
+    sc3 = s_split[cl * kLevels + 3];
+  }
   int maxsh = 0;
   float step = 1.0f, bias = 0.0f;
   if (kAcc && ELEM == kI8) {
@@ -353,7 +407,20 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     wave_sync();
 
     // 2. encode: 4 comparisons per (row, codebook)
-    if (kEnc) {
+    if (kEnc && a.enc_reg) {
+      const lds_f32* xa = reinterpret_cast<const lds_f32*>(sA);
+      for (int j = 0; j < enr; j += 2) {  // two rows per step: 8 independent loads
+        const int ra = er0 + j * erstep;
+        const int rb = er0 + min(j + 1, enr - 1) * erstep;
+        const lds_f32* pa = xa + ra * a.Dp;
+        const lds_f32* pb = xa + rb * a.Dp;
+        const float a0 = pa[sc0], a1 = pa[sc1], a2 = pa[sc2], a3 = pa[sc3];
+        const float b0 = pb[sc0], b1 = pb[sc1], b2 = pb[sc2], b3 = pb[sc3];
+        sI[ra * a.Cp + cl] = (uint8_t)tree_walk(a0, a1, a2, a3, MDN_TREE_ARGS);
+        const int ib = tree_walk(b0, b1, b2, b3, MDN_TREE_ARGS);
+        if (j + 1 < enr) sI[rb * a.Cp + cl] = (uint8_t)ib;
+      }
+    } else if (kEnc) {
       const lds_f32* xa = reinterpret_cast<const lds_f32*>(sA);
       for (int p = lane; p < RW * C; p += 64) {
         const int r = (C == 1) ? p : (int)__umulhi((uint32_t)p, a.c_magic);
@@ -367,6 +434,8 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
         i = 2 * i + ((xr[sp[3]] > th[7 + i]) ? 1 : 0);
         sI[r * a.Cp + c] = (uint8_t)i;
       }
+    }
+    if (kEnc) {
       wave_sync();
       if (a.idx_out != nullptr) {
         if (a.Cp == C && ((reinterpret_cast<uintptr_t>(a.idx_out) & 3) == 0)) {
@@ -440,14 +509,58 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   X(MODE, ELEM, 0, UQ) X(MODE, ELEM, 1, UQ) X(MODE, ELEM, 2, UQ) X(MODE, ELEM, 4, UQ) \
   X(MODE, ELEM, 8, UQ) X(MODE, ELEM, 9, UQ) X(MODE, ELEM, 16, UQ)
 
-#define MDN_CASE(MODE, ELEM, PF, UQ)                                                  \
-  if (mode == MODE && elem == ELEM && pf == PF && uq == UQ) {                         \
-    hipLaunchKernelGGL((path_kernel<MODE, ELEM, PF, UQ>), grid, block, a.L.total,     \
-                       stream, a);                                                    \
-    return hipGetLastError();                                                         \
-  }
+// Resident workgroups per CU for one kernel / block / LDS size, cached.
+static int resident_per_cu(const void* fn, int block, int lds) {
+  struct Entry { const void* fn; int block, lds, n; };
+  static Entry cache[64];
+  static int used = 0;
+  static std::mutex mu;
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < used; ++i)
+    if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
+  if (used < 64) cache[used++] = Entry{fn, block, lds, n};
+  return n;
+}
 
-static hipError_t set_lds_limit(int mode, int elem, int pf, int uq, int bytes);
+static int device_cus() {
+  static std::atomic<int> cus{0};
+  int v = cus.load();
+  if (v == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      v = n;
+    else
+      v = 256;
+    cus.store(v);
+  }
+  return v;
+}
+
+// The persistent grid never exceeds what is resident at once, so no wave of
+// workgroups runs after the first has drained.
+template <int MODE, int ELEM, int PF, int UQ>
+static hipError_t launch_one(const KArgs& a, dim3 grid, dim3 block, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&path_kernel<MODE, ELEM, PF, UQ>);
+  if (a.L.total > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t resident = (int64_t)resident_per_cu(fn, (int)block.x, a.L.total) * device_cus();
+  int64_t gx = (int64_t)grid.x;
+  const int64_t cap = resident / (int64_t)grid.y;
+  if (gx > cap) gx = cap > 0 ? cap : 1;
+  grid.x = (unsigned)gx;
+  hipLaunchKernelGGL((path_kernel<MODE, ELEM, PF, UQ>), grid, block, a.L.total, stream, a);
+  return hipGetLastError();
+}
+
+#define MDN_CASE(MODE, ELEM, PF, UQ)                                         \
+  if (mode == MODE && elem == ELEM && pf == PF && uq == UQ) {                \
+    return launch_one<MODE, ELEM, PF, UQ>(a, grid, block, stream);           \
+  }
 
 hipError_t launch_path(int mode, int elem, int pf, int uq, const KArgs& a, dim3 grid, dim3 block,
                        hipStream_t stream) {
@@ -466,10 +579,7 @@ hipError_t launch_path(int mode, int elem, int pf, int uq, const KArgs& a, dim3 
   MDN_PF_LIST(MDN_CASE, kAccum, kF32, 1)
   MDN_PF_LIST(MDN_CASE, kAccum, kF32, 2)
   MDN_PF_LIST(MDN_CASE, kAccum, kF32, 4)
-  (void)set_lds_limit;
   return hipErrorInvalidValue;
 }
-
-static hipError_t set_lds_limit(int, int, int, int, int) { return hipSuccess; }
 
 }  // namespace mdn
