@@ -243,3 +243,47 @@ def build_lut_f32(P, B, stream=None):
 
 def version() -> int:
     return int(_lib.lib().maddness_version())
+
+
+class PreparedCall:
+    """One C-ABI call with its arguments validated and marshalled once.
+
+    Calling the object issues the same launch again on the stream captured
+    when it was prepared (no checks, no allocation, no Python-side work
+    beyond the ctypes call), for serving loops and benchmarks.  The tensors
+    it was prepared with must stay alive and keep their storage.
+    """
+
+    def __init__(self, name, args, keep, outputs):
+        self._fn = getattr(_lib.lib(), name)
+        self._name = name
+        self._args = args
+        self._keep = keep          # tensors whose storage the pointers refer to
+        self.outputs = outputs
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st:
+            _lib.check(self._name, st)
+        return self.outputs
+
+
+def prepare_matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, acc_out=None,
+                   idx_out=None, stream=None, validate=False):
+    """Prepared maddness_matmul; ``call()`` returns (y, acc or None, idx or None)."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    C2, M = _lut_i8(lut, scale, offset)
+    if C2 != C:
+        raise ValueError("lut codebooks differ from the trees'")
+    if validate:
+        _validate_trees(split_dims, D)
+        _validate_scales(scale)
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
+    _need(y_out, "y_out", torch.float32, 2)
+    _dense(y_out, "y_out")
+    args = (_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut), _ptr(scale),
+            _ptr(offset), M, _ptr(y_out), _ptr(acc_out), _ptr(idx_out), _stream(stream))
+    keep = (A, split_dims, thresholds, lut, scale, offset, y_out, acc_out, idx_out)
+    return PreparedCall("maddness_matmul", args, keep, (y_out, acc_out, idx_out))

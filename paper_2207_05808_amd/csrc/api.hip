@@ -188,6 +188,68 @@ int plan(const Shape& s, Plan* out, bool single_tile_only) {
   return MADDNESS_OK;
 }
 
+// Gather-fused plan: C divides 64 and the whole table (plus one zero row,
+// staged as int16 for int8 tables) fits in LDS.  Returns false when the
+// shape does not qualify.
+bool plan_gfused(const Shape& s, GArgs* g, int* ng_out, int* uq_out, int* nw_out) {
+  if (s.C > 64 || (64 % s.C) != 0) return false;
+  int nw = 16;   // one 1024-thread workgroup per CU stages the table once
+  const int G = 64 / s.C;
+  const int no = (s.M + 7) / 8;   // column octets
+  int best_ng = 0, best_uq = 0, best_lpr = 0;
+  int64_t best_cost = 0;
+  for (int ng = 1; ng <= 4; ng *= 2) {
+    const int R = ng * G;
+    if (R > 64) break;
+    for (int uq = 1; uq <= 4; uq *= 2) {
+      int lpr = 1;
+      while (lpr < 64 && lpr * uq < no) lpr *= 2;
+      if (lpr < 64 / R) lpr = 64 / R;   // one accumulate pass covers at most R rows
+      int uq_eff = (no + lpr - 1) / lpr;
+      if (uq_eff == 3) uq_eff = 4;
+      if (uq_eff > uq) continue;
+      const int64_t cost = (int64_t)lpr * uq_eff;   // lane-slots per row
+      if (best_ng == 0 || cost < best_cost) {
+        best_ng = ng; best_uq = uq_eff; best_lpr = lpr; best_cost = cost;
+      }
+    }
+  }
+  if (best_ng == 0) return false;
+  GArgs a{};
+  a.A = s.A; a.split = s.split; a.thr = s.thr; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset;
+  a.y = s.y; a.acc = s.acc; a.idx_out = s.idx_out;
+  a.N = s.N; a.lda = s.lda; a.D = s.D; a.C = s.C; a.M = s.M;
+  a.c_log2 = ilog2(s.C);
+  a.rs8 = round_up(s.M, 8);
+  a.rs16 = 2 * round_up(s.M, 8);
+  a.rs32 = 4 * round_up(s.M, 8);
+  a.R = best_ng * G;
+  a.NSP = round_up(s.C, 4);
+  a.lpr_log2 = ilog2(best_lpr);
+  a.vec_out = (s.M % 4 == 0) && aligned(s.y, 16) && (s.acc == nullptr || aligned(s.acc, 16));
+  a.vec16 = aligned(s.lut, 16) && (s.elem == kF32 ? (s.M % 4 == 0) : (s.M % 16 == 0));
+  if ((int64_t)a.R * s.lda * 4 >= (1ll << 31)) return false;   // 32-bit per-lane gather offsets
+  const int64_t tab = (int64_t)(s.C * kK + 1) * (s.elem == kF32 ? a.rs32 : a.rs16);
+  if (tab > kLdsBytes) return false;
+  int off = 0;
+  for (;; nw /= 2) {   // widest workgroup whose offsets fit next to the table
+    off = 0;
+    auto take = [&](int64_t bytes) { const int o = off; off += round_up((int)bytes, 16); return o; };
+    take(tab);
+    a.off_shc = take(s.C * 4);
+    a.off_misc = take(32);
+    a.off_wave = take((int64_t)nw * a.R * a.NSP * 4);
+    if (off <= kLdsBytes || nw == 1) break;
+  }
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  *g = a;
+  *ng_out = best_ng;
+  *uq_out = best_uq;
+  *nw_out = nw;
+  return true;
+}
+
 int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   Plan p;
   const int rc = plan(s, &p, single_tile_only);
@@ -318,6 +380,10 @@ int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda, const int
   s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out; s.acc = acc_out;
   s.idx_out = idx_out;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  GArgs g;
+  int ng, uq, nw;
+  if (plan_gfused(s, &g, &ng, &uq, &nw))
+    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
   Plan p;
   if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
   return two_phase(s, idx_out, st);
@@ -335,6 +401,10 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda, const
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.M = M; s.y = y_out; s.idx_out = idx_out;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  GArgs g;
+  int ng, uq, nw;
+  if (plan_gfused(s, &g, &ng, &uq, &nw))
+    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
   Plan p;
   if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
   return two_phase(s, idx_out, st);

@@ -1,0 +1,465 @@
+// Fused encode + lookup-accumulate for tables that fit in LDS and codebook
+// counts that divide 64 (§1, §2.1 of McCarter & Dronen: the encoding function
+// is 4 comparisons per codebook; the product is the sum over codebooks of the
+// selected table rows).
+//
+// Rows of A never go through LDS.  Lane l owns codebook c = l % C and row
+// l / C of every group of G = 64 / C rows; it keeps c's 15 thresholds and 4
+// split columns in registers and loads exactly the 4 values its walk compares
+// (plain cached loads: a codebook's 4 columns share cache lines, and every
+// line of a row is fetched from HBM once).  A wavefront handles R = NG * G
+// rows per step, with one uniform row base and per-lane 32-bit offsets, and
+// prefetches the next step's values while it computes.
+//
+// The walk writes, per (row, codebook), the LDS byte offset of the selected
+// table row.  The accumulate gives each lane 8 consecutive columns of one row
+// and, 4 codebooks at a time, adds the selected rows:
+//  * int8 tables whose shifted codes cannot overflow 16 bits in total
+//    (127 * sum_c 2^(e_c - e_min) <= 32767) are staged in LDS as int16
+//    values q << (e_c - e_min) and summed with packed 16-bit adds: the
+//    arithmetic is modular and the exact total fits, so the sum is exact;
+//  * other int8 tables are staged as int8 and summed with v_dot4c_i32_i8
+//    against per-codebook weights 2^sh << 8b (exact int32);
+//  * fp32 tables are summed with ordered fp32 adds, codebooks ascending.
+// Codebooks are padded to a multiple of 4 with offsets of an all-zero row.
+#include "internal.hpp"
+
+#include <mutex>
+
+namespace mdn {
+
+namespace {
+
+typedef uint32_t u32x4g __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2g __attribute__((ext_vector_type(2)));
+typedef float f32x4g __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char glds_t;
+typedef __attribute__((address_space(3))) int32_t glds_i32;
+typedef __attribute__((address_space(3))) uint32_t glds_u32;
+typedef __attribute__((address_space(3))) u32x4g glds_u32x4;
+typedef __attribute__((address_space(3))) u32x2g glds_u32x2;
+typedef __attribute__((address_space(3))) f32x4g glds_f32x4;
+
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ void wsync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int walk(float x0, float x1, float x2, float x3, float t0, float t1, float t2,
+                                    float t3, float t4, float t5, float t6, float t7, float t8, float t9,
+                                    float t10, float t11, float t12, float t13, float t14) {
+  const bool b0 = x0 > t0;
+  const bool b1 = x1 > (b0 ? t2 : t1);
+  const float v2 = b0 ? (b1 ? t6 : t5) : (b1 ? t4 : t3);
+  const bool b2 = x2 > v2;
+  const float lo = b1 ? (b2 ? t10 : t9) : (b2 ? t8 : t7);
+  const float hi = b1 ? (b2 ? t14 : t13) : (b2 ? t12 : t11);
+  const bool b3 = x3 > (b0 ? hi : lo);
+  return ((int)b0 << 3) | ((int)b1 << 2) | ((int)b2 << 1) | (int)b3;
+}
+
+// packed 16-bit add, lanes independent (wrap-around)
+__device__ __forceinline__ uint32_t pk_add16(uint32_t a, uint32_t b) {
+  typedef short s2 __attribute__((ext_vector_type(2)));
+  const s2 x = __builtin_bit_cast(s2, a), y = __builtin_bit_cast(s2, b);
+  return __builtin_bit_cast(uint32_t, (s2)(x + y));
+}
+
+}  // namespace
+
+// LDS layout (bytes): [table: C*16 rows + 1 zero row, rs bytes each (sized for
+// the widest staging)][shift per codebook][misc]
+// [per wavefront: R rows x NSP int32 table offsets]
+template <int ELEM, int NG, int UQ>
+__global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  glds_t* smem = (glds_t*)smem_raw;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = uni(tid >> 6);
+  const int nw = blockDim.x >> 6;
+  const int C = g.C, M = g.M;
+  const int no = (M + 7) >> 3;   // column octets
+  const int NSP = g.NSP;
+
+  glds_t* s_tab = smem;
+  glds_i32* s_shc = reinterpret_cast<glds_i32*>(smem + g.off_shc);    // [C] shifts
+  glds_i32* s_misc = reinterpret_cast<glds_i32*>(smem + g.off_misc);  // -, -, bias, step, emin, sum 2^sh
+  glds_i32* s_off = reinterpret_cast<glds_i32*>(smem + g.off_wave) + (size_t)wave * g.R * NSP;
+
+  // ---------------- per-lane tree registers
+  const int c = lane & (C - 1);
+  const int gsub = lane >> g.c_log2;   // row within a group of G rows
+  const int G = 64 >> g.c_log2;
+  const int R = g.R;
+  const float* th = g.thr + c * kNodes;
+  const float t0 = th[0], t1 = th[1], t2 = th[2], t3 = th[3], t4 = th[4], t5 = th[5], t6 = th[6],
+              t7 = th[7], t8 = th[8], t9 = th[9], t10 = th[10], t11 = th[11], t12 = th[12], t13 = th[13],
+              t14 = th[14];
+  const unsigned dmax = (unsigned)(g.D - 1);
+  uint32_t goff[NG][4];  // byte offsets from the step's first row (split columns clamped: memory safety)
+#pragma unroll
+  for (int q = 0; q < NG; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      goff[q][t] = (uint32_t)(((int64_t)(q * G + gsub) * g.lda + min((unsigned)g.split[c * 4 + t], dmax)) * 4);
+
+  const int64_t N = g.N;
+  const int64_t tw = (int64_t)gridDim.x * nw;
+  int64_t st = (int64_t)blockIdx.x * nw + wave;   // step index: rows [st * R, st * R + R)
+  const char* A8 = reinterpret_cast<const char*>(g.A);
+  const int64_t step_bytes = (int64_t)R * g.lda * 4;
+
+  float x[NG][4];
+  auto gather = [&](int64_t s, float (&v)[NG][4]) {
+    const int64_t row0 = s * R;
+    const char* base = A8 + s * step_bytes;   // wavefront-uniform
+    if (row0 + R <= N) {
+#pragma unroll
+      for (int q = 0; q < NG; ++q)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[q][t] = *reinterpret_cast<const float*>(base + goff[q][t]);
+    } else {   // last, partial step: rows past N re-read row N - 1
+#pragma unroll
+      for (int q = 0; q < NG; ++q) {
+        const int64_t over = max((int64_t)(q * G + gsub) - (N - 1 - row0), (int64_t)0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          v[q][t] = *reinterpret_cast<const float*>(base + goff[q][t] - over * g.lda * 4);
+      }
+    }
+  };
+  if (st * R < N) gather(st, x);
+
+  // ---------------- prologue (the first step's gathers are already in flight)
+  if (tid == 0) { s_misc[4] = 1 << 30; s_misc[5] = 0; }
+  __syncthreads();
+  const uint32_t* sb = reinterpret_cast<const uint32_t*>(g.scale);
+  if (ELEM == kI8 && tid < C) atomicMin((int*)&s_misc[4], (int)((sb[tid] >> 23) & 0xffu) - 127);
+  __syncthreads();
+  if (tid < C) {
+    const int sh = (ELEM == kI8) ? min((int)((sb[tid] >> 23) & 0xffu) - 127 - s_misc[4], 30) : 0;
+    s_shc[tid] = sh;
+    if (ELEM == kI8) atomicAdd((int*)&s_misc[5], sh <= 14 ? (1 << sh) : (1 << 15));
+  }
+  __syncthreads();
+  const bool narrow = (ELEM == kI8) && (127 * s_misc[5] <= 32767);
+  const int rs = (ELEM == kF32) ? g.rs32 : (narrow ? g.rs16 : g.rs8);
+  if (ELEM == kI8 && wave == 0) {
+    // bias32: double sum over codebooks in ascending order (one coalesced load,
+    // then the ordered sum through readlane; every lane computes the same value)
+    const float ov = g.offset[min(lane, C - 1)];
+    double sum = 0.0;
+    for (int cc = 0; cc < C; ++cc) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), cc));
+    if (lane == 0) {
+      s_misc[2] = __float_as_int((float)sum);
+      s_misc[3] = __float_as_int(__builtin_ldexpf(1.0f, s_misc[4]));
+    }
+  }
+  {
+    // table rows (c, k) plus the zero row C*16; columns padded to octets with zeros
+    const int rows = C * 16;
+    const int wpr = (ELEM == kF32) ? 8 * no : (narrow ? 4 * no : 2 * no);  // dwords per LDS row
+    int wlog = 0;
+    while ((1 << wlog) < wpr) ++wlog;
+    // 8 LDS dwords per thread per round, all global loads issued first (clamped
+    // addresses, masked afterwards) so the round costs one memory latency
+    const int total = (rows + 1) << wlog;
+    const int8_t* q8 = reinterpret_cast<const int8_t*>(g.lut);
+    const float* qf = reinterpret_cast<const float*>(g.lut);
+    const int64_t last = (int64_t)rows * M - 1;
+    for (int base = tid; base < total; base += 8 * blockDim.x) {
+      uint32_t v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int u = base + j * blockDim.x;
+        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
+        const int64_t e0 = (int64_t)row * M;
+        if (ELEM == kF32) {
+          v[j] = __float_as_uint(qf[min(e0 + w, last)]);
+        } else if (narrow) {
+          const uint32_t lo = (uint8_t)q8[min(e0 + 2 * w, last)], hi = (uint8_t)q8[min(e0 + 2 * w + 1, last)];
+          v[j] = lo | (hi << 8);
+        } else {
+          uint32_t x = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x |= (uint32_t)(uint8_t)q8[min(e0 + 4 * w + e, last)] << (8 * e);
+          v[j] = x;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int u = base + j * blockDim.x;
+        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
+        if (u >= total || w >= wpr) continue;
+        uint32_t x = 0;
+        if (row < rows) {
+          if (ELEM == kF32) {
+            x = w < M ? v[j] : 0u;
+          } else if (narrow) {
+            const int sh = s_shc[row >> 4];
+            const int m = 2 * w;
+            const int lo = m < M ? ((int)(int8_t)(v[j] & 0xffu) << sh) : 0;
+            const int hi = m + 1 < M ? ((int)(int8_t)(v[j] >> 8) << sh) : 0;
+            x = ((uint32_t)lo & 0xffffu) | ((uint32_t)hi << 16);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (4 * w + e < M) x |= v[j] & (0xffu << (8 * e));
+          }
+        }
+        *reinterpret_cast<glds_u32*>(s_tab + row * rs + 4 * w) = x;
+      }
+    }
+    // padding codebook slots of every row point at the zero row
+    glds_i32* all_off = reinterpret_cast<glds_i32*>(smem + g.off_wave);
+    for (int u = tid; u < nw * g.R * NSP; u += blockDim.x) all_off[u] = rows * rs;
+  }
+  __syncthreads();
+
+  const float bias = __int_as_float(uni(s_misc[2]));
+  const float step = __int_as_float(uni(s_misc[3]));
+  const int cbase = c * 16 * rs;
+
+  // ---------------- accumulate lane mapping: LPR lanes per row, 8 columns per lane-slot
+  const int lpr_log2 = g.lpr_log2;
+  const int LPR = 1 << lpr_log2;
+  const int ar = lane >> lpr_log2;
+  const int cg = lane & (LPR - 1);
+  const int RA = 64 >> lpr_log2;
+  // lane-slot u covers column quads qa = cg + 2 LPR u and qb = qa + LPR, so each
+  // output store instruction writes LPR consecutive 16-byte chunks of a row
+  const int nq4 = (M + 3) >> 2;
+  const int qbytes = (ELEM == kF32) ? 16 : (narrow ? 8 : 4);  // LDS bytes of 4 columns
+  int lqa[UQ], lqb[UQ];
+#pragma unroll
+  for (int u = 0; u < UQ; ++u) {
+    lqa[u] = min(cg + 2 * LPR * u, nq4 - 1) * qbytes;
+    lqb[u] = min(cg + 2 * LPR * u + LPR, nq4 - 1) * qbytes;
+  }
+  const int nslot = (C + 3) & ~3;
+
+  for (; st * R < N; st += tw) {
+    const int64_t row0 = st * R;
+    float xn[NG][4];
+    if ((st + tw) * R < N) gather(st + tw, xn);
+
+    // encode: one walk per (row, codebook) of this lane
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      const int k = walk(x[q][0], x[q][1], x[q][2], x[q][3], t0, t1, t2, t3, t4, t5, t6, t7, t8, t9, t10,
+                         t11, t12, t13, t14);
+      const int r = q * G + gsub;
+      s_off[r * NSP + c] = cbase + k * rs;
+      if (g.idx_out) {
+        const int64_t row = row0 + r;
+        if (row < N) g.idx_out[row * C + c] = (uint8_t)k;
+      }
+    }
+    wsync();
+
+    for (int rb = 0; rb < R; rb += RA) {
+      const int rr = rb + ar;
+      const glds_i32* orow = s_off + rr * NSP;
+      int iacc[UQ][8];
+      float facc[UQ][8];
+#pragma unroll
+      for (int u = 0; u < UQ; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { iacc[u][e] = 0; facc[u][e] = 0.0f; }
+      u32x4g o = *reinterpret_cast<const glds_u32x4*>(orow);
+      if (ELEM == kI8 && narrow) {
+        uint32_t hacc[UQ][4];     // 8 int16 sums in 4 dwords
+#pragma unroll
+        for (int u = 0; u < UQ; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) hacc[u][e] = 0u;
+        for (int j = 0; j < nslot; j += 4) {
+          const u32x4g on = *reinterpret_cast<const glds_u32x4*>(orow + min(j + 4, nslot - 4));
+          u32x2g va[4][UQ], vb[4][UQ];
+#pragma unroll
+          for (int u = 0; u < UQ; ++u) {
+            va[0][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.x + lqa[u]);
+            vb[0][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.x + lqb[u]);
+            va[1][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.y + lqa[u]);
+            vb[1][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.y + lqb[u]);
+            va[2][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.z + lqa[u]);
+            vb[2][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.z + lqb[u]);
+            va[3][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.w + lqa[u]);
+            vb[3][u] = *reinterpret_cast<const glds_u32x2*>(s_tab + o.w + lqb[u]);
+          }
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int u = 0; u < UQ; ++u) {
+              hacc[u][0] = pk_add16(hacc[u][0], va[b][u].x);
+              hacc[u][1] = pk_add16(hacc[u][1], va[b][u].y);
+              hacc[u][2] = pk_add16(hacc[u][2], vb[b][u].x);
+              hacc[u][3] = pk_add16(hacc[u][3], vb[b][u].y);
+            }
+          o = on;
+        }
+#pragma unroll
+        for (int u = 0; u < UQ; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            iacc[u][2 * e] = __builtin_amdgcn_sbfe((int)hacc[u][e], 0, 16);
+            iacc[u][2 * e + 1] = (int)hacc[u][e] >> 16;
+          }
+      } else if (ELEM == kI8) {
+        for (int j = 0; j < nslot; j += 4) {
+          const u32x4g on = *reinterpret_cast<const glds_u32x4*>(orow + min(j + 4, nslot - 4));
+          u32x2g v[4][UQ];
+#pragma unroll
+          for (int u = 0; u < UQ; ++u) {
+            v[0][u].x = *reinterpret_cast<const glds_u32*>(s_tab + o.x + lqa[u]);
+            v[0][u].y = *reinterpret_cast<const glds_u32*>(s_tab + o.x + lqb[u]);
+            v[1][u].x = *reinterpret_cast<const glds_u32*>(s_tab + o.y + lqa[u]);
+            v[1][u].y = *reinterpret_cast<const glds_u32*>(s_tab + o.y + lqb[u]);
+            v[2][u].x = *reinterpret_cast<const glds_u32*>(s_tab + o.z + lqa[u]);
+            v[2][u].y = *reinterpret_cast<const glds_u32*>(s_tab + o.z + lqb[u]);
+            v[3][u].x = *reinterpret_cast<const glds_u32*>(s_tab + o.w + lqa[u]);
+            v[3][u].y = *reinterpret_cast<const glds_u32*>(s_tab + o.w + lqb[u]);
+          }
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int cc = min(j + b, C - 1);   // padding slots read the zero row: any weight
+            const int sh = uni(s_shc[cc]);
+#pragma unroll
+            for (int u = 0; u < UQ; ++u)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                iacc[u][e] += __builtin_amdgcn_sbfe((int)v[b][u].x, 8 * e, 8) << sh;
+                iacc[u][4 + e] += __builtin_amdgcn_sbfe((int)v[b][u].y, 8 * e, 8) << sh;
+              }
+          }
+          o = on;
+        }
+      } else {
+        for (int j = 0; j < nslot; j += 4) {
+          const u32x4g on = *reinterpret_cast<const glds_u32x4*>(orow + min(j + 4, nslot - 4));
+          f32x4g v[4][UQ][2];
+#pragma unroll
+          for (int u = 0; u < UQ; ++u) {
+            v[0][u][0] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.x + lqa[u]);
+            v[0][u][1] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.x + lqb[u]);
+            v[1][u][0] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.y + lqa[u]);
+            v[1][u][1] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.y + lqb[u]);
+            v[2][u][0] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.z + lqa[u]);
+            v[2][u][1] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.z + lqb[u]);
+            v[3][u][0] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.w + lqa[u]);
+            v[3][u][1] = *reinterpret_cast<const glds_f32x4*>(s_tab + o.w + lqb[u]);
+          }
+#pragma unroll
+          for (int b = 0; b < 4; ++b)   // codebooks strictly in ascending order
+#pragma unroll
+            for (int u = 0; u < UQ; ++u) {
+              facc[u][0] = facc[u][0] + v[b][u][0].x;
+              facc[u][1] = facc[u][1] + v[b][u][0].y;
+              facc[u][2] = facc[u][2] + v[b][u][0].z;
+              facc[u][3] = facc[u][3] + v[b][u][0].w;
+              facc[u][4] = facc[u][4] + v[b][u][1].x;
+              facc[u][5] = facc[u][5] + v[b][u][1].y;
+              facc[u][6] = facc[u][6] + v[b][u][1].z;
+              facc[u][7] = facc[u][7] + v[b][u][1].w;
+            }
+          o = on;
+        }
+      }
+
+      // epilogue: 8 columns per lane-slot
+      const int64_t row = row0 + rr;
+      if (rr < R && row < N) {
+        float* yrow = g.y + row * M;
+        int32_t* arow = (ELEM == kI8 && g.acc) ? g.acc + row * M : nullptr;
+#pragma unroll
+        for (int u = 0; u < UQ; ++u) {
+          float out[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            out[e] = (ELEM == kI8) ? __builtin_fmaf((float)iacc[u][e], step, bias) : facc[u][e];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int qd = cg + 2 * LPR * u + h * LPR;
+            if (qd >= nq4) continue;
+            const int mh = 4 * qd;
+            if (g.vec_out && mh + 4 <= M) {
+              __builtin_nontemporal_store((f32x4g){out[4 * h], out[4 * h + 1], out[4 * h + 2], out[4 * h + 3]},
+                                          reinterpret_cast<f32x4g*>(yrow + mh));
+              if (arow)
+                __builtin_nontemporal_store((u32x4g){(uint32_t)iacc[u][4 * h], (uint32_t)iacc[u][4 * h + 1],
+                                                     (uint32_t)iacc[u][4 * h + 2], (uint32_t)iacc[u][4 * h + 3]},
+                                            reinterpret_cast<u32x4g*>(arow + mh));
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (mh + e < M) {
+                  yrow[mh + e] = out[4 * h + e];
+                  if (arow) arow[mh + e] = iacc[u][4 * h + e];
+                }
+            }
+          }
+        }
+      }
+    }
+    wsync();  // the next step overwrites this wavefront's offsets
+#pragma unroll
+    for (int q = 0; q < NG; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[q][e] = xn[q][e];
+  }
+}
+
+// Per (kernel, block, LDS size): the LDS attribute is raised once and the
+// number of resident workgroups per CU is queried once.
+static int g_prepare(const void* fn, int block, int lds, hipError_t* err) {
+  struct Entry { const void* fn; int block, lds, n; };
+  static Entry cache[64];
+  static int used = 0;
+  static std::mutex mu;
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < used; ++i)
+    if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
+  if (lds > 64 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) { *err = e; return 0; }
+  }
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
+  if (used < 64) cache[used++] = Entry{fn, block, lds, n};
+  return n;
+}
+
+template <int ELEM, int NG, int UQ>
+static hipError_t glaunch(const GArgs& g, int nw, int cus, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&gfused_kernel<ELEM, NG, UQ>);
+  hipError_t err = hipSuccess;
+  const int per_cu = g_prepare(fn, nw * 64, g.lds_total, &err);
+  if (err != hipSuccess) return err;
+  const int64_t steps = (g.N + g.R - 1) / g.R;
+  int64_t blocks = (steps + nw - 1) / nw;
+  const int64_t resident = (int64_t)per_cu * cus;
+  if (blocks > resident) blocks = resident;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL((gfused_kernel<ELEM, NG, UQ>), dim3((unsigned)blocks), dim3(nw * 64), g.lds_total, stream, g);
+  return hipGetLastError();
+}
+
+#define MDN_G_CASE(E, NG, UQ) \
+  if (elem == E && ng == NG && uq == UQ) return glaunch<E, NG, UQ>(g, nw, cus, stream);
+
+hipError_t launch_gfused(int elem, int ng, int uq, const GArgs& g, int nw, int cus, hipStream_t stream) {
+  MDN_G_CASE(kI8, 1, 1) MDN_G_CASE(kI8, 2, 1) MDN_G_CASE(kI8, 4, 1)
+  MDN_G_CASE(kI8, 1, 2) MDN_G_CASE(kI8, 2, 2) MDN_G_CASE(kI8, 4, 2)
+  MDN_G_CASE(kI8, 1, 4) MDN_G_CASE(kI8, 2, 4) MDN_G_CASE(kI8, 4, 4)
+  MDN_G_CASE(kF32, 1, 1) MDN_G_CASE(kF32, 2, 1) MDN_G_CASE(kF32, 4, 1)
+  MDN_G_CASE(kF32, 1, 2) MDN_G_CASE(kF32, 2, 2) MDN_G_CASE(kF32, 4, 2)
+  MDN_G_CASE(kF32, 1, 4) MDN_G_CASE(kF32, 2, 4) MDN_G_CASE(kF32, 4, 4)
+  return hipErrorInvalidValue;
+}
+
+}  // namespace mdn

@@ -60,6 +60,36 @@ struct KArgs {
   LdsLayout L;
 };
 
+// Arguments of the gather-fused kernel (fused_gather.hip): C divides 64 and the
+// whole table fits in LDS.
+struct GArgs {
+  const float* A;         // [N][lda]
+  const int32_t* split;   // [C][4]
+  const float* thr;       // [C][15]
+  const void* lut;        // [C][16][M] int8 or fp32
+  const float* scale;     // [C]
+  const float* offset;    // [C]
+  float* y;               // [N][M]
+  int32_t* acc;           // [N][M] or null
+  uint8_t* idx_out;       // [N][C] or null
+  int64_t N;
+  int64_t lda;
+  int D, C, M;
+  int c_log2;
+  int rs8, rs16, rs32;    // LDS bytes per (c,k) row: int8, int16 and fp32 staging
+  int R;                  // rows per wavefront step (NG * 64 / C)
+  int NSP;                // offset slots per row (C rounded up to 4)
+  int lpr_log2;           // accumulate: 2^lpr_log2 lanes per row, 8 columns each
+  int vec_out;            // outputs allow 16-byte stores
+  int vec16;              // table rows are whole 16-byte units (int8: M % 16 == 0; fp32: M % 4 == 0)
+  int off_shc, off_misc, off_wave, lds_total;  // LDS byte offsets
+};
+
+hipError_t launch_gfused(int elem, int ng, int uq, const GArgs& g, int nw, int cus, hipStream_t stream);
+
+// Compute units of the current device (queried once per process).
+int device_cus();
+
 // Launch one kernel of the family; returns hipSuccess or the launch error.
 hipError_t launch_path(int mode, int elem, int pf, int uq, const KArgs& a,
                        dim3 grid, dim3 block, hipStream_t stream);

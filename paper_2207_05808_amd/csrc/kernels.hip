@@ -253,36 +253,51 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   lds_t* s_shp = smem + a.L.shp;
 
   // ---------------- workgroup prologue ----------------
+  // Table staging: 8 LDS dwords per thread per round with every global load
+  // issued first (clamped addresses, masked afterwards), so a round costs one
+  // memory latency instead of eight.
   if (kAcc) {
     const int rows = C * kK;
-    // quads per LDS row, padded to a power of two so the index split is a shift
-    int qlog = 0;
-    while ((1 << qlog) < nq) ++qlog;
-    const int total = rows << qlog;
-    if (ELEM == kI8) {
-      if (a.vec_out) {  // M % 4 == 0 and 4-byte aligned table: dword copies
-        const uint32_t* src = reinterpret_cast<const uint32_t*>(a.lut);
-        const int m4 = a.M >> 2;
-        for (int u = tid; u < total; u += blockDim.x) {
-          const int row = u >> qlog, q = u & ((1 << qlog) - 1);
-          if (q < nq)
-            *reinterpret_cast<lds_u32*>(s_lut + row * a.lut_rs + 4 * q) = src[(int64_t)row * m4 + (m0 >> 2) + q];
-        }
-      } else {
-        const int8_t* src = reinterpret_cast<const int8_t*>(a.lut);
-        for (int u = tid; u < (rows << (qlog + 2)); u += blockDim.x) {
-          const int row = u >> (qlog + 2), j = u & ((4 << qlog) - 1);
-          if (j < 4 * nq)
-            s_lut[row * a.lut_rs + j] = (j < mt) ? src[(int64_t)row * a.M + m0 + j] : (int8_t)0;
+    const int wpr = (ELEM == kI8) ? nq : 4 * nq;   // LDS dwords per table row
+    int wlog = 0;
+    while ((1 << wlog) < wpr) ++wlog;
+    const int total = rows << wlog;
+    const int8_t* q8 = reinterpret_cast<const int8_t*>(a.lut);
+    const float* qf = reinterpret_cast<const float*>(a.lut);
+    const int64_t last = (int64_t)rows * a.M - 1;
+    for (int base = tid; base < total; base += 8 * blockDim.x) {
+      uint32_t v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int u = base + j * blockDim.x;
+        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
+        const int64_t e0 = (int64_t)row * a.M + m0;
+        if (ELEM == kF32) {
+          v[j] = __float_as_uint(qf[min(e0 + w, last)]);
+        } else if (a.vec_out) {   // M % 4 == 0, aligned: whole dwords
+          v[j] = *reinterpret_cast<const uint32_t*>(q8 + min(e0 + 4 * w, last - 3));
+        } else {
+          uint32_t x = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x |= (uint32_t)(uint8_t)q8[min(e0 + 4 * w + e, last)] << (8 * e);
+          v[j] = x;
         }
       }
-    } else {
-      const float* src = reinterpret_cast<const float*>(a.lut);
-      for (int u = tid; u < (rows << (qlog + 2)); u += blockDim.x) {
-        const int row = u >> (qlog + 2), j = u & ((4 << qlog) - 1);
-        if (j < 4 * nq)
-          *reinterpret_cast<lds_f32*>(s_lut + row * a.lut_rs + 4 * j) =
-              (j < mt) ? src[(int64_t)row * a.M + m0 + j] : 0.0f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int u = base + j * blockDim.x;
+        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
+        if (u >= total || w >= wpr) continue;
+        uint32_t x;
+        if (ELEM == kF32) {
+          x = w < mt ? v[j] : 0u;
+        } else {
+          x = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * w + e < mt) x |= v[j] & (0xffu << (8 * e));
+        }
+        *reinterpret_cast<lds_u32*>(s_lut + row * a.lut_rs + 4 * w) = x;
       }
     }
   }
@@ -308,11 +323,19 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
       s_sh[c] = sh;
       atomicMax((int*)&s_misc[1], sh);
     }
-    if (tid == 0) {
-      double sum = 0.0;  // bias32: double sum over codebooks in ascending order
-      for (int c = 0; c < C; ++c) sum += (double)a.offset[c];
-      s_misc[2] = __float_as_int((float)sum);
-      s_misc[3] = __float_as_int(__builtin_ldexpf(1.0f, emin));
+    if (wave == 0) {
+      // bias32: double sum over codebooks in ascending order, 64 offsets per
+      // coalesced load, summed in order through readlane (all lanes alike)
+      double sum = 0.0;
+      for (int j0 = 0; j0 < C; j0 += 64) {
+        const float ov = a.offset[min(j0 + lane, C - 1)];
+        const int n = min(64, C - j0);
+        for (int l = 0; l < n; ++l) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), l));
+      }
+      if (lane == 0) {
+        s_misc[2] = __float_as_int((float)sum);
+        s_misc[3] = __float_as_int(__builtin_ldexpf(1.0f, emin));
+      }
     }
     __syncthreads();
     // shifts packed as nibbles, 8 codebooks per dword (used while every shift <= 6)
@@ -509,22 +532,27 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   X(MODE, ELEM, 0, UQ) X(MODE, ELEM, 1, UQ) X(MODE, ELEM, 2, UQ) X(MODE, ELEM, 4, UQ) \
   X(MODE, ELEM, 8, UQ) X(MODE, ELEM, 9, UQ) X(MODE, ELEM, 16, UQ)
 
-// Resident workgroups per CU for one kernel / block / LDS size, cached.
-static int resident_per_cu(const void* fn, int block, int lds) {
+// Per (kernel, block, LDS size): the LDS attribute is raised once and the
+// number of resident workgroups per CU is queried once.
+static int prepare_kernel(const void* fn, int block, int lds, hipError_t* err) {
   struct Entry { const void* fn; int block, lds, n; };
-  static Entry cache[64];
+  static Entry cache[128];
   static int used = 0;
   static std::mutex mu;
   std::lock_guard<std::mutex> lock(mu);
   for (int i = 0; i < used; ++i)
     if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
+  if (lds > 64 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) { *err = e; return 0; }
+  }
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
-  if (used < 64) cache[used++] = Entry{fn, block, lds, n};
+  if (used < 128) cache[used++] = Entry{fn, block, lds, n};
   return n;
 }
 
-static int device_cus() {
+int device_cus() {
   static std::atomic<int> cus{0};
   int v = cus.load();
   if (v == 0) {
@@ -544,11 +572,10 @@ static int device_cus() {
 template <int MODE, int ELEM, int PF, int UQ>
 static hipError_t launch_one(const KArgs& a, dim3 grid, dim3 block, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&path_kernel<MODE, ELEM, PF, UQ>);
-  if (a.L.total > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total);
-    if (e != hipSuccess) return e;
-  }
-  const int64_t resident = (int64_t)resident_per_cu(fn, (int)block.x, a.L.total) * device_cus();
+  hipError_t err = hipSuccess;
+  const int per_cu = prepare_kernel(fn, (int)block.x, a.L.total, &err);
+  if (err != hipSuccess) return err;
+  const int64_t resident = (int64_t)per_cu * device_cus();
   int64_t gx = (int64_t)grid.x;
   const int64_t cap = resident / (int64_t)grid.y;
   if (gx > cap) gx = cap > 0 ? cap : 1;

@@ -286,3 +286,16 @@ def test_matmul_full_size_sampled(orc, name):
     assert int(idx.max()) < 16
     del y, idx, A
     torch.cuda.empty_cache()
+
+
+def test_prepared_call_matches(orc):
+    p = W.make("conv3x3_im2col", N=2222)
+    lut, scale, offset = W.random_codes(p.C, p.M, seed=11, max_shift=3)
+    args = (dev(p.A), dev(p.split), dev(p.thr), dev(lut), dev(scale), dev(offset))
+    call = mdn.prepare_matmul(*args)
+    y, _, _ = call()
+    first = host(y).copy()
+    call()
+    _, _, ry = orc.matmul(p.A, p.split, p.thr, lut, scale, offset)
+    assert_y(first, ry)
+    assert np.array_equal(host(y), first)
