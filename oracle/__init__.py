@@ -9,7 +9,7 @@ Functions and the passages they follow (the paper: McCarter & Dronen,
 "Look-ups are not (yet) all you need for deep learning inference"):
 
 * :func:`encode` -- §1 (encoding function, log2(K)-bit indices) and §2.1
-  (exactly 4 comparisons, K = 16 leaves).
+  (one comparison per tree level, four levels, K = 16 leaves).
 * :func:`lut_accumulate` -- §1 (sum of the table rows picked per codebook;
   8-bit block floating point tables).
 * :func:`lut_accumulate_f32` -- same sum over an unquantized fp32 table.

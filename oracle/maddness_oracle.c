@@ -15,7 +15,8 @@
  *     gcc -O2 -std=c99 -fopenmp -ffp-contract=off -fno-fast-math -fPIC -shared
  * so that no multiply-add is contracted.
  *
- * Readings of points the paper leaves open (numbered as in the design notes):
+ * Readings of points the paper leaves open (the same numbers label them in
+ * the tests and in the HIP sources):
  *   R1  a tree node sends x right iff x > threshold (strict; ties and NaN go
  *       left).
  *   R2  one split dimension per (codebook, level), a global column of A.
