@@ -8,8 +8,12 @@
 // split columns in registers and loads exactly the 4 values its walk compares
 // (plain cached loads: a codebook's 4 columns share cache lines, and every
 // line of a row is fetched from HBM once).  A wavefront handles R = NG * G
-// rows per step, with one uniform row base and per-lane 32-bit offsets, and
-// prefetches the next step's values while it computes.
+// rows per step through a buffer descriptor per step (uniform base, per-lane
+// 32-bit offsets, range = the rows that exist) and keeps two steps of gathers
+// in flight: the gathers of step s + 2 reuse step s's registers right after
+// its walk.  The prologue issues the table's 16-byte units and the first two
+// steps' gathers before it waits for anything, reduces the block exponents
+// inside each wavefront, and has a single workgroup barrier.
 //
 // The walk writes, per (row, codebook), the LDS byte offset of the selected
 // table row.  The accumulate gives each lane 8 consecutive columns of one row
@@ -39,6 +43,9 @@ typedef __attribute__((address_space(3))) uint32_t glds_u32;
 typedef __attribute__((address_space(3))) u32x4g glds_u32x4;
 typedef __attribute__((address_space(3))) u32x2g glds_u32x2;
 typedef __attribute__((address_space(3))) f32x4g glds_f32x4;
+
+// third descriptor dword for a raw (untyped, unswizzled) buffer on gfx9-family chips
+constexpr int kBufferDword3 = 0x00020000;
 
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -88,86 +95,140 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
 
   glds_t* s_tab = smem;
   glds_i32* s_shc = reinterpret_cast<glds_i32*>(smem + g.off_shc);    // [C] shifts
-  glds_i32* s_misc = reinterpret_cast<glds_i32*>(smem + g.off_misc);  // -, -, bias, step, emin, sum 2^sh
+  glds_i32* s_misc = reinterpret_cast<glds_i32*>(smem + g.off_misc);  // bias32
   glds_i32* s_off = reinterpret_cast<glds_i32*>(smem + g.off_wave) + (size_t)wave * g.R * NSP;
 
-  // ---------------- per-lane tree registers
   const int c = lane & (C - 1);
   const int gsub = lane >> g.c_log2;   // row within a group of G rows
   const int G = 64 >> g.c_log2;
   const int R = g.R;
-  const float* th = g.thr + c * kNodes;
-  const float t0 = th[0], t1 = th[1], t2 = th[2], t3 = th[3], t4 = th[4], t5 = th[5], t6 = th[6],
-              t7 = th[7], t8 = th[8], t9 = th[9], t10 = th[10], t11 = th[11], t12 = th[12], t13 = th[13],
-              t14 = th[14];
-  const unsigned dmax = (unsigned)(g.D - 1);
-  uint32_t goff[NG][4];  // byte offsets from the step's first row (split columns clamped: memory safety)
-#pragma unroll
-  for (int q = 0; q < NG; ++q)
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-      goff[q][t] = (uint32_t)(((int64_t)(q * G + gsub) * g.lda + min((unsigned)g.split[c * 4 + t], dmax)) * 4);
-
   const int64_t N = g.N;
+
+  // ---------------- loads issued before any waiting, oldest first: the split
+  // columns (the gather offsets need them), the dequantization constants, the
+  // table as 16-byte units, then the gathers of this wavefront's first two
+  // steps.  The prologue below waits only for what it uses, so HBM streams A
+  // while the table is staged.
+  int sp[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) sp[t] = g.split[c * 4 + t];
+  const uint32_t sbits = (ELEM == kI8) ? __float_as_uint(g.scale[c]) : 0u;
+  const float ofs = (ELEM == kI8) ? g.offset[c] : 0.0f;
+
+  constexpr int kTabUnits = 4;   // 16-byte table units per thread loaded up front
+  const int upr = g.vec16 ? (ELEM == kF32 ? M >> 2 : M >> 4) : 0;   // units per table row
+  const int units = C * 16 * upr;
+  const __amdgpu_buffer_rsrc_t trs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(g.lut), 0, units * 16, kBufferDword3);
+  u32x4g tv[kTabUnits];   // units past the table read as zeros and are not used
+#pragma unroll
+  for (int j = 0; j < kTabUnits; ++j)
+    tv[j] = __builtin_amdgcn_raw_buffer_load_b128(trs, (tid + j * (int)blockDim.x) * 16, 0, 0);
+
+  const unsigned dmax = (unsigned)(g.D - 1);
+  // byte offsets from the step's first row (split columns clamped: memory
+  // safety); group q of G rows adds the uniform q * G * lda * 4 as soffset
+  int goff[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) goff[t] = (int)(((int64_t)gsub * g.lda + min((unsigned)sp[t], dmax)) * 4);
+  const int qstride = (int)((int64_t)G * g.lda * 4);
+
   const int64_t tw = (int64_t)gridDim.x * nw;
   int64_t st = (int64_t)blockIdx.x * nw + wave;   // step index: rows [st * R, st * R + R)
   const char* A8 = reinterpret_cast<const char*>(g.A);
   const int64_t step_bytes = (int64_t)R * g.lda * 4;
 
-  float x[NG][4];
+  // Buffer loads against a per-step descriptor (uniform base in SGPRs, the
+  // 32-bit lane offsets as voffset).  The descriptor's range is the rows that
+  // exist: a partial last step reads zeros past row N - 1 (those rows are
+  // encoded but never stored), and a step past the end has an empty range and
+  // touches no memory, so every prefetch is issued unconditionally.
+  const int64_t last_step = (N - 1) / R;
   auto gather = [&](int64_t s, float (&v)[NG][4]) {
-    const int64_t row0 = s * R;
-    const char* base = A8 + s * step_bytes;   // wavefront-uniform
-    if (row0 + R <= N) {
+    const int64_t sc = min(s, last_step);
+    const int64_t rows = s > last_step ? 0 : min((int64_t)R, N - s * R);
+    const int32_t nbytes = rows > 0 ? (int32_t)min(step_bytes, (rows - 1) * g.lda * 4 + (int64_t)g.D * 4) : 0;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(A8 + sc * step_bytes), 0, nbytes, kBufferDword3);
 #pragma unroll
-      for (int q = 0; q < NG; ++q)
+    for (int q = 0; q < NG; ++q)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) v[q][t] = *reinterpret_cast<const float*>(base + goff[q][t]);
-    } else {   // last, partial step: rows past N re-read row N - 1
+      for (int t = 0; t < 4; ++t)
+        v[q][t] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, goff[t], q * qstride, 0));
+  };
+  float x[NG][4], xn[NG][4];
+  gather(st, x);
+  gather(st + tw, xn);
+
+  const float* th = g.thr + c * kNodes;
+  const float t0 = th[0], t1 = th[1], t2 = th[2], t3 = th[3], t4 = th[4], t5 = th[5], t6 = th[6],
+              t7 = th[7], t8 = th[8], t9 = th[9], t10 = th[10], t11 = th[11], t12 = th[12], t13 = th[13],
+              t14 = th[14];
+
+  // ---------------- dequantization constants, reduced inside each wavefront
+  // (lane l holds codebook l % C; every wavefront reaches the same values)
+  const int e_c = (int)((sbits >> 23) & 0xffu) - 127;   // exponent of scale_c, an exact power of two
+  int emin = e_c;
 #pragma unroll
-      for (int q = 0; q < NG; ++q) {
-        const int64_t over = max((int64_t)(q * G + gsub) - (N - 1 - row0), (int64_t)0);
+  for (int o = 32; o >= 1; o >>= 1) emin = min(emin, __shfl_xor(emin, o));
+  const int sh = (ELEM == kI8) ? min(e_c - emin, 30) : 0;
+  int pw = (lane < C) ? (sh <= 14 ? (1 << sh) : (1 << 15)) : 0;
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          v[q][t] = *reinterpret_cast<const float*>(base + goff[q][t] - over * g.lda * 4);
+  for (int o = 32; o >= 1; o >>= 1) pw += __shfl_xor(pw, o);
+  const bool narrow = (ELEM == kI8) && (127 * pw <= 32767);
+  const int rs = (ELEM == kF32) ? g.rs32 : (narrow ? g.rs16 : g.rs8);
+  const float step = __builtin_ldexpf(1.0f, emin);
+  if (wave == 0) {
+    if (lane < C) s_shc[lane] = sh;
+    if (ELEM == kI8) {
+      // bias32: double sum over codebooks in ascending order (every lane computes it)
+      double sum = 0.0;
+      for (int cc = 0; cc < C; ++cc)
+        sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ofs), cc));
+      if (lane == 0) s_misc[0] = __float_as_int((float)sum);
+    }
+  }
+
+  // ---------------- table staging: rows (c, k) plus the all-zero row C * 16
+  const int rows = C * 16;
+  const bool vec_all = units > 0 && units <= kTabUnits * (int)blockDim.x;
+  if (vec_all) {
+    // unit u is bytes [16 (u % upr), 16 (u % upr) + 16) of table row u / upr
+#pragma unroll
+    for (int j = 0; j < kTabUnits; ++j) {
+      const int u = tid + j * (int)blockDim.x;
+      const int row = min(u, units - 1) / upr;
+      const int col = (min(u, units - 1) - row * upr) * 16;   // byte offset in the global row
+      const int shr = __shfl(sh, row >> 4);   // lane row / 16 holds that codebook's shift
+      if (u < units) {
+        if (ELEM == kI8 && narrow) {
+          u32x4g lo, hi;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const int v = (int)tv[j][w];
+            const uint32_t p0 = ((uint32_t)(__builtin_amdgcn_sbfe(v, 0, 8) << shr) & 0xffffu) |
+                                ((uint32_t)(__builtin_amdgcn_sbfe(v, 8, 8) << shr) << 16);
+            const uint32_t p1 = ((uint32_t)(__builtin_amdgcn_sbfe(v, 16, 8) << shr) & 0xffffu) |
+                                ((uint32_t)(__builtin_amdgcn_sbfe(v, 24, 8) << shr) << 16);
+            if (w < 2) { lo[2 * w] = p0; lo[2 * w + 1] = p1; } else { hi[2 * w - 4] = p0; hi[2 * w - 3] = p1; }
+          }
+          *reinterpret_cast<glds_u32x4*>(s_tab + row * rs + 2 * col) = lo;
+          *reinterpret_cast<glds_u32x4*>(s_tab + row * rs + 2 * col + 16) = hi;
+        } else {
+          *reinterpret_cast<glds_u32x4*>(s_tab + row * rs + col) = tv[j];
+        }
       }
     }
-  };
-  if (st * R < N) gather(st, x);
-
-  // ---------------- prologue (the first step's gathers are already in flight)
-  if (tid == 0) { s_misc[4] = 1 << 30; s_misc[5] = 0; }
-  __syncthreads();
-  const uint32_t* sb = reinterpret_cast<const uint32_t*>(g.scale);
-  if (ELEM == kI8 && tid < C) atomicMin((int*)&s_misc[4], (int)((sb[tid] >> 23) & 0xffu) - 127);
-  __syncthreads();
-  if (tid < C) {
-    const int sh = (ELEM == kI8) ? min((int)((sb[tid] >> 23) & 0xffu) - 127 - s_misc[4], 30) : 0;
-    s_shc[tid] = sh;
-    if (ELEM == kI8) atomicAdd((int*)&s_misc[5], sh <= 14 ? (1 << sh) : (1 << 15));
+    for (int w = tid; w < (rs >> 2); w += blockDim.x) *reinterpret_cast<glds_u32*>(s_tab + rows * rs + 4 * w) = 0u;
   }
-  __syncthreads();
-  const bool narrow = (ELEM == kI8) && (127 * s_misc[5] <= 32767);
-  const int rs = (ELEM == kF32) ? g.rs32 : (narrow ? g.rs16 : g.rs8);
-  if (ELEM == kI8 && wave == 0) {
-    // bias32: double sum over codebooks in ascending order (one coalesced load,
-    // then the ordered sum through readlane; every lane computes the same value)
-    const float ov = g.offset[min(lane, C - 1)];
-    double sum = 0.0;
-    for (int cc = 0; cc < C; ++cc) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), cc));
-    if (lane == 0) {
-      s_misc[2] = __float_as_int((float)sum);
-      s_misc[3] = __float_as_int(__builtin_ldexpf(1.0f, s_misc[4]));
-    }
-  }
-  {
-    // table rows (c, k) plus the zero row C*16; columns padded to octets with zeros
-    const int rows = C * 16;
+  if (!vec_all) {
+    // general staging (tables larger than the up-front units, or rows that are
+    // not whole 16-byte units): 8 LDS dwords per thread per round, all global
+    // loads of a round issued first; columns padded to octets with zeros
+    __syncthreads();   // shifts visible
     const int wpr = (ELEM == kF32) ? 8 * no : (narrow ? 4 * no : 2 * no);  // dwords per LDS row
     int wlog = 0;
     while ((1 << wlog) < wpr) ++wlog;
-    // 8 LDS dwords per thread per round, all global loads issued first (clamped
-    // addresses, masked afterwards) so the round costs one memory latency
     const int total = (rows + 1) << wlog;
     const int8_t* q8 = reinterpret_cast<const int8_t*>(g.lut);
     const float* qf = reinterpret_cast<const float*>(g.lut);
@@ -185,10 +246,10 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
           const uint32_t lo = (uint8_t)q8[min(e0 + 2 * w, last)], hi = (uint8_t)q8[min(e0 + 2 * w + 1, last)];
           v[j] = lo | (hi << 8);
         } else {
-          uint32_t x = 0;
+          uint32_t xx = 0;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) x |= (uint32_t)(uint8_t)q8[min(e0 + 4 * w + e, last)] << (8 * e);
-          v[j] = x;
+          for (int e = 0; e < 4; ++e) xx |= (uint32_t)(uint8_t)q8[min(e0 + 4 * w + e, last)] << (8 * e);
+          v[j] = xx;
         }
       }
 #pragma unroll
@@ -196,35 +257,35 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
         const int u = base + j * blockDim.x;
         const int row = u >> wlog, w = u & ((1 << wlog) - 1);
         if (u >= total || w >= wpr) continue;
-        uint32_t x = 0;
+        uint32_t xx = 0;
         if (row < rows) {
           if (ELEM == kF32) {
-            x = w < M ? v[j] : 0u;
+            xx = w < M ? v[j] : 0u;
           } else if (narrow) {
-            const int sh = s_shc[row >> 4];
+            const int shr = s_shc[row >> 4];
             const int m = 2 * w;
-            const int lo = m < M ? ((int)(int8_t)(v[j] & 0xffu) << sh) : 0;
-            const int hi = m + 1 < M ? ((int)(int8_t)(v[j] >> 8) << sh) : 0;
-            x = ((uint32_t)lo & 0xffffu) | ((uint32_t)hi << 16);
+            const int lo = m < M ? ((int)(int8_t)(v[j] & 0xffu) << shr) : 0;
+            const int hi = m + 1 < M ? ((int)(int8_t)(v[j] >> 8) << shr) : 0;
+            xx = ((uint32_t)lo & 0xffffu) | ((uint32_t)hi << 16);
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (4 * w + e < M) x |= v[j] & (0xffu << (8 * e));
+              if (4 * w + e < M) xx |= v[j] & (0xffu << (8 * e));
           }
         }
-        *reinterpret_cast<glds_u32*>(s_tab + row * rs + 4 * w) = x;
+        *reinterpret_cast<glds_u32*>(s_tab + row * rs + 4 * w) = xx;
       }
     }
+  }
+  {
     // padding codebook slots of every row point at the zero row
     glds_i32* all_off = reinterpret_cast<glds_i32*>(smem + g.off_wave);
     for (int u = tid; u < nw * g.R * NSP; u += blockDim.x) all_off[u] = rows * rs;
   }
   __syncthreads();
 
-  const float bias = __int_as_float(uni(s_misc[2]));
-  const float step = __int_as_float(uni(s_misc[3]));
+  const float bias = __int_as_float(uni(s_misc[0]));
   const int cbase = c * 16 * rs;
-
   // ---------------- accumulate lane mapping: LPR lanes per row, 8 columns per lane-slot
   const int lpr_log2 = g.lpr_log2;
   const int LPR = 1 << lpr_log2;
@@ -243,16 +304,16 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   }
   const int nslot = (C + 3) & ~3;
 
-  for (; st * R < N; st += tw) {
+  // One step: walk step st from `cur`, reuse `cur` for the gathers of step
+  // st + 2 tw (so two steps of gathers stay in flight with two buffers), then
+  // accumulate step st.
+  auto step_body = [&](float (&cur)[NG][4]) {
     const int64_t row0 = st * R;
-    float xn[NG][4];
-    if ((st + tw) * R < N) gather(st + tw, xn);
-
     // encode: one walk per (row, codebook) of this lane
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
-      const int k = walk(x[q][0], x[q][1], x[q][2], x[q][3], t0, t1, t2, t3, t4, t5, t6, t7, t8, t9, t10,
-                         t11, t12, t13, t14);
+      const int k = walk(cur[q][0], cur[q][1], cur[q][2], cur[q][3], t0, t1, t2, t3, t4, t5, t6, t7, t8, t9,
+                         t10, t11, t12, t13, t14);
       const int r = q * G + gsub;
       s_off[r * NSP + c] = cbase + k * rs;
       if (g.idx_out) {
@@ -260,6 +321,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
         if (row < N) g.idx_out[row * C + c] = (uint8_t)k;
       }
     }
+    gather(st + 2 * tw, cur);
     wsync();
 
     for (int rb = 0; rb < R; rb += RA) {
@@ -407,10 +469,14 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
       }
     }
     wsync();  // the next step overwrites this wavefront's offsets
-#pragma unroll
-    for (int q = 0; q < NG; ++q)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[q][e] = xn[q][e];
+  };
+
+  while (st * R < N) {
+    step_body(x);
+    st += tw;
+    if (st * R >= N) break;
+    step_body(xn);
+    st += tw;
   }
 }
 
