@@ -35,7 +35,7 @@ def log(*a):
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("kernels.hip", "fused_gather.hip", "api.hip", "internal.hpp"):
+    for f in ("kernels.hip", "fused_gather.hip", "api.hip", "internal.hpp"):   # the fused path's sources
         with open(os.path.join(ROOT, "paper_2207_05808_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -250,12 +250,62 @@ bool plan_gfused(const Shape& s, GArgs* g, int* ng_out, int* uq_out, int* nw_out
   return true;
 }
 
+// Column-tiled accumulate (tiled_accum.hip): 8 wavefronts, 4 row passes per
+// wavefront per work item, table tiles of CT codebooks sized for two
+// workgroups per CU.
+bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
+  const bool f32 = s.elem == kF32;
+  const int eg = f32 ? 4 : 1;                 // global bytes per table entry
+  if ((int64_t)s.C * kK * s.M * eg >= (1ll << 31)) return false;   // 32-bit buffer offsets
+  const int nw = 8, nj = 4;
+  const int cpl = f32 ? 4 : 8;                // columns per lane
+  const int lpr = s.M > 8 * cpl ? 16 : 8;     // lanes per output row
+  TArgs a{};
+  a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;
+  a.N = s.N; a.C = s.C; a.M = s.M;
+  a.lpr_log2 = ilog2(lpr);
+  a.Mt = cpl * lpr;
+  a.RB = nw * (64 / lpr) * nj;
+  const int upc = 16 / eg;                    // columns per 16-byte global unit
+  const int units_per_cb = kK * (a.Mt / upc);
+  int ct = 4;   // largest multiple of 4 whose units and index words fit the staging registers
+  while (ct * 2 <= round_up(s.C, 4) && (ct * 2) * units_per_cb <= 4 * nw * 64 && a.RB * (ct * 2) / 4 <= 2 * nw * 64)
+    ct *= 2;
+  a.CT = ct;
+  a.ntm = (s.M + a.Mt - 1) / a.Mt;
+  a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
+  a.vec_lut = aligned(s.lut, 16) && (s.M % upc == 0);
+  a.vec_idx = (s.C % 4 == 0) && aligned(s.idx_in, 4);
+  a.vec_out = (s.M % 4 == 0) && (s.y == nullptr || aligned(s.y, 16)) && (s.acc == nullptr || aligned(s.acc, 16));
+  int off = 0;
+  auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
+  a.off_tab = take(a.CT * kK * a.Mt * (f32 ? 4 : 2));
+  a.off_idx = take(a.RB * a.CT);
+  a.off_sh = take(s.C * 4);
+  a.off_misc = take(16);
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  *t = a;
+  *nj_out = nj;
+  *nw_out = nw;
+  return true;
+}
+
 int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   Plan p;
   const int rc = plan(s, &p, single_tile_only);
   if (rc != MADDNESS_OK) return rc;
   return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, stream));
 }
+
+// Accumulate-only work: the column-tiled kernel, else the general path.
+int accumulate(const Shape& s, hipStream_t stream) {
+  TArgs t;
+  int nj, nw;
+  if (plan_tacc(s, &t, &nj, &nw)) return status_from(launch_tacc(s.elem, nj, t, nw, device_cus(), stream));
+  return run(s, false, stream);
+}
+
 
 // ----------------------------------------------------------------- checks
 int check_encode_args(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split,
@@ -302,7 +352,7 @@ int two_phase(Shape s, uint8_t* idx_user, hipStream_t stream) {
     q.mode = kAccum;
     q.idx_in = idx;
     q.idx_out = nullptr;
-    rc = run(q, false, stream);
+    rc = accumulate(q, stream);
   }
   if (temp && hipFreeAsync(idx, stream) != hipSuccess && rc == MADDNESS_OK) rc = MADDNESS_EHIP;
   return rc;
@@ -351,7 +401,7 @@ int maddness_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C, const int8
   Shape s = shape(kAccum, kI8);
   s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.scale = scale; s.offset = offset; s.M = M;
   s.acc = acc_out; s.y = y_out;
-  return run(s, false, static_cast<hipStream_t>(stream));
+  return accumulate(s, static_cast<hipStream_t>(stream));
 }
 
 int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C, const float* lut, int32_t M,
@@ -361,7 +411,7 @@ int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C, const 
   if (!idx || !y_out || !aligned(lut, 4) || !aligned(y_out, 4)) return MADDNESS_EINVAL;
   Shape s = shape(kAccum, kF32);
   s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.M = M; s.y = y_out;
-  return run(s, false, static_cast<hipStream_t>(stream));
+  return accumulate(s, static_cast<hipStream_t>(stream));
 }
 
 int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,

@@ -87,6 +87,32 @@ struct GArgs {
 
 hipError_t launch_gfused(int elem, int ng, int uq, const GArgs& g, int nw, int cus, hipStream_t stream);
 
+// Arguments of the column-tiled accumulate kernel (tiled_accum.hip): one work
+// item is RB rows x Mt output columns; the table is staged CT codebooks at a
+// time.
+struct TArgs {
+  const uint8_t* idx;     // [N][C]
+  const void* lut;        // [C][16][M] int8 or fp32
+  const float* scale;     // [C] (int8 tables)
+  const float* offset;    // [C] (int8 tables)
+  float* y;               // [N][M] or null (int8 tables with acc)
+  int32_t* acc;           // [N][M] or null
+  int64_t N;
+  int C, M;
+  int lpr_log2;           // lanes per output row: 8 or 16
+  int Mt;                 // columns per tile: 8 (int8) or 4 (fp32) per lane
+  int CT;                 // codebooks per LDS tile (multiple of 4)
+  int RB;                 // rows per work item: waves * (64 / lanes per row) * NJ
+  int ntm;                // column tiles
+  int64_t nwork;          // ntm * ceil(N / RB)
+  int vec_lut;            // table rows move in 16-byte units
+  int vec_idx;            // index rows move in 4-byte units (C % 4 == 0)
+  int vec_out;            // outputs allow 16-byte stores
+  int off_tab, off_idx, off_sh, off_misc, lds_total;  // LDS byte offsets
+};
+
+hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream);
+
 // Compute units of the current device (queried once per process).
 int device_cus();
 

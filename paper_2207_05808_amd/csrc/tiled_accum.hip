@@ -1,0 +1,373 @@
+// Column-tiled lookup-accumulate (§1 of McCarter & Dronen: the product is the
+// sum over codebooks of the table rows the encoder selected) for tables larger
+// than LDS and for the accumulate-only entry points.
+//
+// A work item is RB rows x Mt output columns.  The lanes of a wavefront form
+// groups of LPR lanes, one group per output row; lane g of a group covers Mt /
+// LPR consecutive columns (8 for int8 tables, 4 for fp32), so the group reads
+// one contiguous LPR x 16-byte segment of a table row (with LPR = 16: 256
+// bytes, every LDS bank once).  The table is staged CT codebooks at a time,
+// [CT * 16 rows][Mt columns], with the matching [RB][CT] tile of indices; the
+// next tile's table units and indices are loaded into registers while the
+// current tile is summed.  Accumulators stay in registers across codebook
+// tiles, so fp32 sums keep the ascending codebook order.
+//  * int8 tables whose shifted codes cannot overflow 16 bits in total
+//    (127 * sum_c 2^(e_c - e_min) <= 32767) are staged as int16 q << (e_c -
+//    e_min) and summed with packed 16-bit adds: modular arithmetic whose exact
+//    total fits, so the sum equals the int32 sum;
+//  * other int8 tables are staged as int16 q and summed in int32 with shifts;
+//  * fp32 tables are summed with ordered fp32 adds.
+// The last codebook tile is padded to a multiple of 4 codebooks with all-zero
+// table rows.
+#include "internal.hpp"
+
+#include <climits>
+#include <mutex>
+#include <type_traits>
+
+namespace mdn {
+
+namespace {
+
+typedef uint32_t tu32x4 __attribute__((ext_vector_type(4)));
+typedef float tf32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char tlds_t;
+typedef __attribute__((address_space(3))) uint32_t tlds_u32;
+typedef __attribute__((address_space(3))) int32_t tlds_i32;
+typedef __attribute__((address_space(3))) tu32x4 tlds_u32x4;
+typedef __attribute__((address_space(3))) tf32x4 tlds_f32x4;
+
+constexpr int kBufDword3 = 0x00020000;   // raw, unswizzled buffer descriptor (gfx9 family)
+constexpr int kTU = 4;                   // 16-byte table units per thread per tile (vector staging)
+constexpr int kIU = 2;                   // 4-byte index words per thread per tile (vector staging)
+constexpr int kOob = INT_MAX;            // buffer offset past any descriptor range: reads zero
+
+__device__ __forceinline__ int tuni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ uint32_t tpk_add16(uint32_t a, uint32_t b) {
+  typedef short s2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, (s2)(__builtin_bit_cast(s2, a) + __builtin_bit_cast(s2, b)));
+}
+
+// four int8 codes -> two dwords of int16 (q << sh), column order kept
+__device__ __forceinline__ void widen4(uint32_t v, int sh, uint32_t& lo, uint32_t& hi) {
+  const int x = (int)v;
+  lo = ((uint32_t)(__builtin_amdgcn_sbfe(x, 0, 8) << sh) & 0xffffu) |
+       ((uint32_t)(__builtin_amdgcn_sbfe(x, 8, 8) << sh) << 16);
+  hi = ((uint32_t)(__builtin_amdgcn_sbfe(x, 16, 8) << sh) & 0xffffu) |
+       ((uint32_t)(__builtin_amdgcn_sbfe(x, 24, 8) << sh) << 16);
+}
+
+}  // namespace
+
+// LDS layout (bytes): [table tile: CT*16 rows of Mt entries (int16 or fp32)]
+// [index tile: RB x CT bytes][shift per codebook][misc]
+template <int ELEM, int NJ>
+__global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  tlds_t* smem = (tlds_t*)smem_raw;
+
+  const int tid = threadIdx.x;
+  const int nt = blockDim.x;
+  const int lane = tid & 63;
+  const int wave = tuni(tid >> 6);
+  const int nw = nt >> 6;
+  const int C = a.C, M = a.M, CT = a.CT, Mt = a.Mt, RB = a.RB;
+  const int64_t N = a.N;
+  const int lpr_log2 = a.lpr_log2;
+  const int RS = 64 >> lpr_log2;          // output rows per wavefront pass
+  const int r4 = lane >> lpr_log2;        // row within the pass
+  const int cg = lane & ((1 << lpr_log2) - 1);
+  constexpr int EB = (ELEM == kF32) ? 4 : 2;     // LDS bytes per staged entry
+  constexpr int EG = (ELEM == kF32) ? 4 : 1;     // global bytes per entry
+  constexpr int CPL = 16 / EB;                   // columns per lane (one 16-byte LDS read)
+  const int rby = Mt * EB;                       // LDS bytes per table row (a power of two)
+  const int rby_log2 = 31 - __builtin_clz(rby);
+
+  tlds_t* s_tab = smem + a.off_tab;
+  tlds_t* s_idx = smem + a.off_idx;
+  tlds_i32* s_sh = reinterpret_cast<tlds_i32*>(smem + a.off_sh);
+  tlds_i32* s_misc = reinterpret_cast<tlds_i32*>(smem + a.off_misc);   // bias32, e_min, sum of 2^sh
+
+  // ---------------- block exponents, shifts and bias32 (int8 tables)
+  bool narrow = false;
+  float step = 1.0f, bias = 0.0f;
+  if (ELEM == kI8) {
+    if (tid == 0) { s_misc[1] = INT_MAX; s_misc[2] = 0; }
+    __syncthreads();
+    const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
+    for (int c = tid; c < C; c += nt) atomicMin((int*)&s_misc[1], (int)((sb[c] >> 23) & 0xffu) - 127);
+    __syncthreads();
+    const int emin = tuni(s_misc[1]);
+    for (int c = tid; c < C; c += nt) {
+      const int sh = min((int)((sb[c] >> 23) & 0xffu) - 127 - emin, 30);
+      s_sh[c] = sh;
+      atomicAdd((int*)&s_misc[2], sh <= 14 ? (1 << sh) : (1 << 15));
+    }
+    if (wave == 0) {
+      // bias32: double sum over codebooks in ascending order
+      double sum = 0.0;
+      for (int c0 = 0; c0 < C; c0 += 64) {
+        const float ov = a.offset[min(c0 + lane, C - 1)];
+        const int n = min(64, C - c0);
+        for (int j = 0; j < n; ++j) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), j));
+      }
+      if (lane == 0) s_misc[0] = __float_as_int((float)sum);
+    }
+    __syncthreads();
+    narrow = 127 * tuni(s_misc[2]) <= 32767;
+    step = __builtin_ldexpf(1.0f, emin);
+    bias = __int_as_float(tuni(s_misc[0]));
+  }
+
+  // ---------------- staging helpers
+  const int upc = 16 / EG;              // columns per 16-byte global unit
+  const int upr = Mt / upc;             // units per table row of the tile
+  const int units = CT * 16 * upr;      // units per tile
+  const int iw = CT >> 2;               // index words per row of the index tile
+  const int iwords = RB * iw;
+  const bool vec = a.vec_lut && a.vec_idx;
+  const __amdgpu_buffer_rsrc_t trs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M * EG), kBufDword3);
+  tu32x4 tv[kTU];
+  uint32_t iv[kIU];
+
+  // registers <- tile (c0) of work item (r0, m0); invalid units and words read zero
+  auto load_tile = [&](int c0, int64_t r0, int m0) {
+#pragma unroll
+    for (int j = 0; j < kTU; ++j) {
+      const int u = tid + j * nt;
+      const int row = u / upr, part = u - row * upr;
+      const int c = c0 + (row >> 4), m = m0 + part * upc;
+      const bool ok = u < units && c < C && m < M;
+      const int off = ok ? ((c * 16 + (row & 15)) * M + m) * EG : kOob;
+      tv[j] = __builtin_amdgcn_raw_buffer_load_b128(trs, off, 0, 0);
+    }
+    const int64_t rows = min((int64_t)RB, N - r0);
+    const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(a.idx + r0 * C), 0, (int)min(rows * C, (int64_t)INT_MAX), kBufDword3);
+#pragma unroll
+    for (int j = 0; j < kIU; ++j) {
+      const int d = tid + j * nt;
+      const int i = d / iw, q = d - i * iw;
+      const bool ok = d < iwords && c0 + 4 * q < C;
+      iv[j] = __builtin_amdgcn_raw_buffer_load_b32(irs, ok ? i * C + c0 + 4 * q : kOob, 0, 0);
+    }
+  };
+  // registers -> LDS
+  auto store_tile = [&](int c0) {
+#pragma unroll
+    for (int j = 0; j < kTU; ++j) {
+      const int u = tid + j * nt;
+      if (u < units) {
+        const int row = u / upr, part = u - row * upr;
+        if (ELEM == kF32) {
+          *reinterpret_cast<tlds_u32x4*>(s_tab + (row << rby_log2) + part * 16) = tv[j];
+        } else {
+          const int c = min(c0 + (row >> 4), C - 1);
+          const int sh = narrow ? s_sh[c] : 0;
+          uint32_t w[8];
+          widen4(tv[j].x, sh, w[0], w[1]);
+          widen4(tv[j].y, sh, w[2], w[3]);
+          widen4(tv[j].z, sh, w[4], w[5]);
+          widen4(tv[j].w, sh, w[6], w[7]);
+          const tu32x4 lo = {w[0], w[1], w[2], w[3]}, hi = {w[4], w[5], w[6], w[7]};
+          *reinterpret_cast<tlds_u32x4*>(s_tab + (row << rby_log2) + part * 32) = lo;
+          *reinterpret_cast<tlds_u32x4*>(s_tab + (row << rby_log2) + part * 32 + 16) = hi;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kIU; ++j) {
+      const int d = tid + j * nt;
+      if (d < iwords) *reinterpret_cast<tlds_u32*>(s_idx + 4 * d) = iv[j];
+    }
+  };
+  // general staging, straight from global memory (rows not in whole 16-byte
+  // units, or index rows not in whole words)
+  auto stage_direct = [&](int c0, int64_t r0, int m0) {
+    const int8_t* q8 = reinterpret_cast<const int8_t*>(a.lut);
+    const float* qf = reinterpret_cast<const float*>(a.lut);
+    const int ent = CT * 16 * Mt;
+    for (int e = tid; e < ent; e += nt) {
+      const int row = e / Mt, col = e - row * Mt;
+      const int c = c0 + (row >> 4), m = m0 + col;
+      const bool ok = c < C && m < M;
+      const int64_t g = ((int64_t)c * 16 + (row & 15)) * M + m;
+      if (ELEM == kF32) {
+        *reinterpret_cast<__attribute__((address_space(3))) float*>(s_tab + (row << rby_log2) + 4 * col) =
+            ok ? qf[g] : 0.0f;
+      } else {
+        const int sh = narrow ? s_sh[min(c, C - 1)] : 0;
+        *reinterpret_cast<__attribute__((address_space(3))) int16_t*>(s_tab + (row << rby_log2) + 2 * col) =
+            ok ? (int16_t)((int)q8[g] << sh) : (int16_t)0;
+      }
+    }
+    for (int e = tid; e < RB * CT; e += nt) {
+      const int i = e / CT, cc = e - i * CT;
+      const bool ok = r0 + i < N && c0 + cc < C;
+      s_idx[e] = ok ? (char)a.idx[(r0 + i) * C + c0 + cc] : (char)0;
+    }
+  };
+
+  // ---------------- work items: (column tile, row block), column tile fastest
+  int ib[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) ib[j] = (j * nw + wave) * RS + r4;
+
+  // MODE 0: fp32 tables; 1: int16 packed sums; 2: int32 sums with shifts
+  auto run = [&](auto mode_tag) {
+    constexpr int MODE = decltype(mode_tag)::value;
+    for (int64_t w = blockIdx.x; w < a.nwork; w += gridDim.x) {
+      const int mt = (int)(w % a.ntm);
+      const int64_t r0 = (w / a.ntm) * RB;
+      const int m0 = mt * Mt;
+
+      constexpr int NACC = (MODE == 2) ? 8 : 4;
+      uint32_t acc[NJ][NACC];   // fp32 bits, packed int16 pairs, or int32
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int e = 0; e < NACC; ++e) acc[j][e] = 0u;
+
+      if (vec) load_tile(0, r0, m0);
+      for (int c0 = 0; c0 < C; c0 += CT) {
+        __syncthreads();   // every reader of the previous tile is done
+        if (vec) store_tile(c0); else stage_direct(c0, r0, m0);
+        __syncthreads();
+        if (vec && c0 + CT < C) load_tile(c0 + CT, r0, m0);   // in flight during the sums below
+        const int ncb = (min(CT, C - c0) + 3) & ~3;
+        for (int cc = 0; cc < ncb; cc += 4) {
+          uint32_t kk[NJ];
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) kk[j] = *reinterpret_cast<const tlds_u32*>(s_idx + ib[j] * CT + cc);
+          int shb[4] = {0, 0, 0, 0};
+          if (MODE == 2) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) shb[b] = tuni(s_sh[min(c0 + cc + b, C - 1)]);   // zero rows: any shift
+          }
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            tu32x4 v[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int row = (cc + b) * 16 + ((kk[j] >> (8 * b)) & 15u);
+              v[b] = *reinterpret_cast<const tlds_u32x4*>(s_tab + (row << rby_log2) + cg * 16);
+            }
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {   // codebooks strictly in ascending order
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                if (MODE == 0) {
+                  acc[j][e] = __float_as_uint(__uint_as_float(acc[j][e]) + __uint_as_float(v[b][e]));
+                } else if (MODE == 1) {
+                  acc[j][e] = tpk_add16(acc[j][e], v[b][e]);
+                } else {
+                  acc[j][2 * e] += (uint32_t)(__builtin_amdgcn_sbfe((int)v[b][e], 0, 16) << shb[b]);
+                  acc[j][2 * e + 1] += (uint32_t)(((int)v[b][e] >> 16) << shb[b]);
+                }
+              }
+            }
+          }
+        }
+      }
+
+      // ---------------- epilogue
+      const int col0 = m0 + cg * CPL;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int64_t row = r0 + ib[j];
+        if (row >= N || col0 >= M) continue;
+        if (MODE == 0) {
+          float* yr = a.y + row * M + col0;
+          if (a.vec_out && col0 + 4 <= M) {
+            __builtin_nontemporal_store((tf32x4){__uint_as_float(acc[j][0]), __uint_as_float(acc[j][1]),
+                                                 __uint_as_float(acc[j][2]), __uint_as_float(acc[j][3])},
+                                        reinterpret_cast<tf32x4*>(yr));
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (col0 + e < M) yr[e] = __uint_as_float(acc[j][e]);
+          }
+        } else {
+          int out[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            out[e] = (MODE == 1) ? ((e & 1) ? (int)acc[j][e >> 1] >> 16 : __builtin_amdgcn_sbfe((int)acc[j][e >> 1], 0, 16))
+                                 : (int)acc[j][e];
+          float yv[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) yv[e] = __builtin_fmaf((float)out[e], step, bias);
+          if (a.vec_out && col0 + 8 <= M) {
+            if (a.y) {
+              __builtin_nontemporal_store((tf32x4){yv[0], yv[1], yv[2], yv[3]},
+                                          reinterpret_cast<tf32x4*>(a.y + row * M + col0));
+              __builtin_nontemporal_store((tf32x4){yv[4], yv[5], yv[6], yv[7]},
+                                          reinterpret_cast<tf32x4*>(a.y + row * M + col0 + 4));
+            }
+            if (a.acc) {
+              __builtin_nontemporal_store((tu32x4){(uint32_t)out[0], (uint32_t)out[1], (uint32_t)out[2], (uint32_t)out[3]},
+                                          reinterpret_cast<tu32x4*>(a.acc + row * M + col0));
+              __builtin_nontemporal_store((tu32x4){(uint32_t)out[4], (uint32_t)out[5], (uint32_t)out[6], (uint32_t)out[7]},
+                                          reinterpret_cast<tu32x4*>(a.acc + row * M + col0 + 4));
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (col0 + e < M) {
+                if (a.y) a.y[row * M + col0 + e] = yv[e];
+                if (a.acc) a.acc[row * M + col0 + e] = out[e];
+              }
+          }
+        }
+      }
+    }
+  };
+  if (ELEM == kF32) run(std::integral_constant<int, 0>{});
+  else if (narrow) run(std::integral_constant<int, 1>{});
+  else run(std::integral_constant<int, 2>{});
+}
+
+// Per (kernel, block, LDS size): the LDS attribute is raised once and the
+// number of resident workgroups per CU is queried once.
+static int t_prepare(const void* fn, int block, int lds, hipError_t* err) {
+  struct Entry { const void* fn; int block, lds, n; };
+  static Entry cache[32];
+  static int used = 0;
+  static std::mutex mu;
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < used; ++i)
+    if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
+  if (lds > 64 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) { *err = e; return 0; }
+  }
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
+  if (used < 32) cache[used++] = Entry{fn, block, lds, n};
+  return n;
+}
+
+template <int ELEM, int NJ>
+static hipError_t tlaunch(const TArgs& t, int nw, int cus, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&tacc_kernel<ELEM, NJ>);
+  hipError_t err = hipSuccess;
+  const int per_cu = t_prepare(fn, nw * 64, t.lds_total, &err);
+  if (err != hipSuccess) return err;
+  int64_t blocks = t.nwork;
+  const int64_t resident = (int64_t)per_cu * cus;
+  if (blocks > resident) blocks = resident;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL((tacc_kernel<ELEM, NJ>), dim3((unsigned)blocks), dim3(nw * 64), t.lds_total, stream, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {
+  if (elem == kI8 && nj == 4) return tlaunch<kI8, 4>(t, nw, cus, stream);
+  if (elem == kI8 && nj == 8) return tlaunch<kI8, 8>(t, nw, cus, stream);
+  if (elem == kF32 && nj == 4) return tlaunch<kF32, 4>(t, nw, cus, stream);
+  if (elem == kF32 && nj == 8) return tlaunch<kF32, 8>(t, nw, cus, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace mdn
