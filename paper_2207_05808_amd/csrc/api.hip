@@ -279,8 +279,8 @@ bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
   a.vec_out = (s.M % 4 == 0) && (s.y == nullptr || aligned(s.y, 16)) && (s.acc == nullptr || aligned(s.acc, 16));
   int off = 0;
   auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
-  a.off_tab = take(a.CT * kK * a.Mt * (f32 ? 4 : 2));
-  a.off_idx = take(a.RB * a.CT);
+  a.off_tab = take(a.CT * kK * a.Mt * (f32 ? 4 : 2));   // 0: the kernel relies on it
+  a.off_idx = take(a.RB * a.CT * 4);
   a.off_sh = take(s.C * 4);
   a.off_misc = take(16);
   a.lds_total = off;

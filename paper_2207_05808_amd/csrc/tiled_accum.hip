@@ -49,19 +49,21 @@ __device__ __forceinline__ uint32_t tpk_add16(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, (s2)(__builtin_bit_cast(s2, a) + __builtin_bit_cast(s2, b)));
 }
 
-// four int8 codes -> two dwords of int16 (q << sh), column order kept
+// four int8 codes -> two dwords of int16 q << sh (0 <= sh <= 8), column order
+// kept: v_perm puts each code in the high byte of its 16-bit half, then a
+// packed arithmetic shift right by 8 - sh sign-extends and scales it
 __device__ __forceinline__ void widen4(uint32_t v, int sh, uint32_t& lo, uint32_t& hi) {
-  const int x = (int)v;
-  lo = ((uint32_t)(__builtin_amdgcn_sbfe(x, 0, 8) << sh) & 0xffffu) |
-       ((uint32_t)(__builtin_amdgcn_sbfe(x, 8, 8) << sh) << 16);
-  hi = ((uint32_t)(__builtin_amdgcn_sbfe(x, 16, 8) << sh) & 0xffffu) |
-       ((uint32_t)(__builtin_amdgcn_sbfe(x, 24, 8) << sh) << 16);
+  typedef short s2 __attribute__((ext_vector_type(2)));
+  const s2 r = {(short)(8 - sh), (short)(8 - sh)};
+  lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(s2, __builtin_amdgcn_perm(0u, v, 0x010c000cu)) >> r);
+  hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(s2, __builtin_amdgcn_perm(0u, v, 0x030c020cu)) >> r);
 }
 
 }  // namespace
 
 // LDS layout (bytes): [table tile: CT*16 rows of Mt entries (int16 or fp32)]
-// [index tile: RB x CT bytes][shift per codebook][misc]
+// [index tile: RB x CT int32, each the LDS byte offset of the selected table
+// row, (c_local * 16 + k) * row bytes][shift per codebook][misc]
 template <int ELEM, int NJ>
 __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
@@ -84,7 +86,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
   const int rby = Mt * EB;                       // LDS bytes per table row (a power of two)
   const int rby_log2 = 31 - __builtin_clz(rby);
 
-  tlds_t* s_tab = smem + a.off_tab;
+  tlds_t* s_tab = smem;   // the table tile starts the LDS block (off_tab == 0)
   tlds_t* s_idx = smem + a.off_idx;
   tlds_i32* s_sh = reinterpret_cast<tlds_i32*>(smem + a.off_sh);
   tlds_i32* s_misc = reinterpret_cast<tlds_i32*>(smem + a.off_misc);   // bias32, e_min, sum of 2^sh
@@ -122,9 +124,11 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 
   // ---------------- staging helpers
   const int upc = 16 / EG;              // columns per 16-byte global unit
-  const int upr = Mt / upc;             // units per table row of the tile
+  const int upr = Mt / upc;             // units per table row of the tile (a power of two)
+  const int upr_log2 = __builtin_ctz(upr);
   const int units = CT * 16 * upr;      // units per tile
-  const int iw = CT >> 2;               // index words per row of the index tile
+  const int iw = CT >> 2;               // index words per row of the index tile (a power of two)
+  const int iw_log2 = __builtin_ctz(iw);
   const int iwords = RB * iw;
   const bool vec = a.vec_lut && a.vec_idx;
   const __amdgpu_buffer_rsrc_t trs =
@@ -137,7 +141,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 #pragma unroll
     for (int j = 0; j < kTU; ++j) {
       const int u = tid + j * nt;
-      const int row = u / upr, part = u - row * upr;
+      const int row = u >> upr_log2, part = u & (upr - 1);
       const int c = c0 + (row >> 4), m = m0 + part * upc;
       const bool ok = u < units && c < C && m < M;
       const int off = ok ? ((c * 16 + (row & 15)) * M + m) * EG : kOob;
@@ -149,7 +153,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 #pragma unroll
     for (int j = 0; j < kIU; ++j) {
       const int d = tid + j * nt;
-      const int i = d / iw, q = d - i * iw;
+      const int i = d >> iw_log2, q = d & (iw - 1);
       const bool ok = d < iwords && c0 + 4 * q < C;
       iv[j] = __builtin_amdgcn_raw_buffer_load_b32(irs, ok ? i * C + c0 + 4 * q : kOob, 0, 0);
     }
@@ -160,7 +164,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
     for (int j = 0; j < kTU; ++j) {
       const int u = tid + j * nt;
       if (u < units) {
-        const int row = u / upr, part = u - row * upr;
+        const int row = u >> upr_log2, part = u & (upr - 1);
         if (ELEM == kF32) {
           *reinterpret_cast<tlds_u32x4*>(s_tab + (row << rby_log2) + part * 16) = tv[j];
         } else {
@@ -179,8 +183,14 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < kIU; ++j) {
-      const int d = tid + j * nt;
-      if (d < iwords) *reinterpret_cast<tlds_u32*>(s_idx + 4 * d) = iv[j];
+      const int d = tid + j * nt;   // index word d: row d / iw, codebooks 4 (d % iw) .. + 3 of the tile
+      if (d < iwords) {
+        const uint32_t cb = (uint32_t)(4 * (d & (iw - 1))) * 16u;
+        tu32x4 o;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) o[b] = (cb + 16u * b + ((iv[j] >> (8 * b)) & 15u)) << rby_log2;
+        *reinterpret_cast<tlds_u32x4*>(s_idx + 16 * d) = o;
+      }
     }
   };
   // general staging, straight from global memory (rows not in whole 16-byte
@@ -206,14 +216,22 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
     for (int e = tid; e < RB * CT; e += nt) {
       const int i = e / CT, cc = e - i * CT;
       const bool ok = r0 + i < N && c0 + cc < C;
-      s_idx[e] = ok ? (char)a.idx[(r0 + i) * C + c0 + cc] : (char)0;
+      const uint32_t k = ok ? (uint32_t)(a.idx[(r0 + i) * C + c0 + cc] & 15u) : 0u;
+      *reinterpret_cast<tlds_u32*>(s_idx + 4 * e) = ((uint32_t)cc * 16u + k) << rby_log2;
     }
   };
 
   // ---------------- work items: (column tile, row block), column tile fastest
+  // this lane's 16 bytes of any table row, and its rows' index-tile entries:
+  // a read address is then one add of an index-tile entry
+  const tlds_t* s_tab_lane = s_tab + cg * 16;
   int ib[NJ];
+  const tlds_t* s_idx_row[NJ];
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) ib[j] = (j * nw + wave) * RS + r4;
+  for (int j = 0; j < NJ; ++j) {
+    ib[j] = (j * nw + wave) * RS + r4;
+    s_idx_row[j] = s_idx + ib[j] * CT * 4;
+  }
 
   // MODE 0: fp32 tables; 1: int16 packed sums; 2: int32 sums with shifts
   auto run = [&](auto mode_tag) {
@@ -238,9 +256,9 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
         if (vec && c0 + CT < C) load_tile(c0 + CT, r0, m0);   // in flight during the sums below
         const int ncb = (min(CT, C - c0) + 3) & ~3;
         for (int cc = 0; cc < ncb; cc += 4) {
-          uint32_t kk[NJ];
+          tu32x4 kk[NJ];   // LDS offsets of the 4 selected table rows
 #pragma unroll
-          for (int j = 0; j < NJ; ++j) kk[j] = *reinterpret_cast<const tlds_u32*>(s_idx + ib[j] * CT + cc);
+          for (int j = 0; j < NJ; ++j) kk[j] = *reinterpret_cast<const tlds_u32x4*>(s_idx_row[j] + cc * 4);
           int shb[4] = {0, 0, 0, 0};
           if (MODE == 2) {
 #pragma unroll
@@ -250,10 +268,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
           for (int j = 0; j < NJ; ++j) {
             tu32x4 v[4];
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-              const int row = (cc + b) * 16 + ((kk[j] >> (8 * b)) & 15u);
-              v[b] = *reinterpret_cast<const tlds_u32x4*>(s_tab + (row << rby_log2) + cg * 16);
-            }
+            for (int b = 0; b < 4; ++b) v[b] = *reinterpret_cast<const tlds_u32x4*>(s_tab_lane + kk[j][b]);
 #pragma unroll
             for (int b = 0; b < 4; ++b) {   // codebooks strictly in ascending order
 #pragma unroll
