@@ -163,7 +163,10 @@ int plan(const Shape& s, Plan* out, bool single_tile_only) {
   a.Mt = best_Mt;
   a.lut_rs = best_rs;
   a.vec_rows = vec_rows;
-  a.enc_reg = enc && (64 % s.C == 0) && ((best_rw * s.C) % 64 == 0);
+  a.enc_reg = !enc ? 0
+              : ((64 % s.C == 0) && ((best_rw * s.C) % 64 == 0)) ? 1   // lanes = (row, codebook)
+              : (s.C % 64 == 0) ? 2                                   // lanes = codebooks, rows looped
+              : 0;                                                    // threshold walk in LDS
   a.c_log2 = ilog2(s.C);
   a.nchunks = (s.N + best_rw - 1) / best_rw;
   a.L = layout(s, nw, best_rw, a.Dp, a.Cp, acc ? s.C * kK * best_rs : 0);

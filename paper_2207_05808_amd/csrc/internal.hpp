@@ -55,7 +55,8 @@ struct KArgs {
   int c_shift;
   int vec_rows;          // 1: staged rows move in 16-byte units
   int vec_out;           // 1: outputs / LUT rows allow 16-byte (4-column) stores
-  int enc_reg;           // 1: C divides 64 and RW*C is a multiple of 64 (register tree walk)
+  int enc_reg;           // tree walk: 1 registers, lanes = (row, codebook) (C divides 64, RW*C % 64 == 0);
+                         // 2 registers, lanes = codebooks (C % 64 == 0); 0 thresholds read from LDS
   int c_log2;            // log2(C) when enc_reg
   LdsLayout L;
 };

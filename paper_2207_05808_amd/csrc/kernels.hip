@@ -302,13 +302,15 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     }
   }
   if (kEnc) {
+    // node-major [16][C] thresholds and level-major [4][C] split columns:
+    // lanes walking consecutive codebooks read consecutive banks at any node
     for (int u = tid; u < C * 16; u += blockDim.x) {
       const int c = u >> 4, j = u & 15;
-      s_thr[u] = (j < kNodes) ? a.thr[c * kNodes + j] : 0.0f;
+      s_thr[j * C + c] = (j < kNodes) ? a.thr[c * kNodes + j] : 0.0f;
     }
     for (int u = tid; u < C * kLevels; u += blockDim.x) {
       const unsigned sp = (unsigned)a.split[u];
-      s_split[u] = (int)min(sp, (unsigned)(a.D - 1));  // memory safety only
+      s_split[(u & 3) * C + (u >> 2)] = (int)min(sp, (unsigned)(a.D - 1));  // memory safety only
     }
   }
   if (kAcc && ELEM == kI8) {
@@ -381,19 +383,19 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
         t11 = 0, t12 = 0, t13 = 0, t14 = 0;
   int sc0 = 0, sc1 = 0, sc2 = 0, sc3 = 0;
   int cl = 0, er0 = 0, erstep = 1, enr = 0;
-  if (kEnc && a.enc_reg) {
+  if (kEnc && a.enc_reg == 1) {
     cl = lane & (C - 1);
     er0 = lane >> a.c_log2;
     erstep = 64 >> a.c_log2;
     enr = (RW * C) >> 6;
-    const lds_f32* th = s_thr + cl * 16;
-    t0 = th[0]; t1 = th[1]; t2 = th[2]; t3 = th[3]; t4 = th[4]; t5 = th[5]; t6 = th[6];
-    t7 = th[7]; t8 = th[8]; t9 = th[9]; t10 = th[10]; t11 = th[11]; t12 = th[12]; t13 = th[13];
-    t14 = th[14];
-    sc0 = s_split[cl * kLevels + 0];
-    sc1 = s_split[cl * kLevels + 1];
-    sc2 = s_split[cl * kLevels + 2];
-    sc3 = s_split[cl * kLevels + 3];
+    const lds_f32* th = s_thr + cl;
+    t0 = th[0]; t1 = th[C]; t2 = th[2 * C]; t3 = th[3 * C]; t4 = th[4 * C]; t5 = th[5 * C];
+    t6 = th[6 * C]; t7 = th[7 * C]; t8 = th[8 * C]; t9 = th[9 * C]; t10 = th[10 * C];
+    t11 = th[11 * C]; t12 = th[12 * C]; t13 = th[13 * C]; t14 = th[14 * C];
+    sc0 = s_split[cl];
+    sc1 = s_split[C + cl];
+    sc2 = s_split[2 * C + cl];
+    sc3 = s_split[3 * C + cl];
   }
   int maxsh = 0;
   float step = 1.0f, bias = 0.0f;
@@ -430,7 +432,7 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     wave_sync();
 
     // 2. encode: 4 comparisons per (row, codebook)
-    if (kEnc && a.enc_reg) {
+    if (kEnc && a.enc_reg == 1) {
       const lds_f32* xa = reinterpret_cast<const lds_f32*>(sA);
       for (int j = 0; j < enr; j += 2) {  // two rows per step: 8 independent loads
         const int ra = er0 + j * erstep;
@@ -443,19 +445,54 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
         const int ib = tree_walk(b0, b1, b2, b3, MDN_TREE_ARGS);
         if (j + 1 < enr) sI[rb * a.Cp + cl] = (uint8_t)ib;
       }
-    } else if (kEnc) {
+    } else if (kEnc && a.enc_reg == 2) {
+      // C a multiple of 64: lane l walks codebooks l, l + 64, ... for every
+      // row of the chunk, with that codebook's tree and split columns in
+      // registers (two rows per step: 8 independent loads)
       const lds_f32* xa = reinterpret_cast<const lds_f32*>(sA);
-      for (int p = lane; p < RW * C; p += 64) {
-        const int r = (C == 1) ? p : (int)__umulhi((uint32_t)p, a.c_magic);
-        const int c = p - r * C;
-        const lds_f32* xr = xa + r * a.Dp;
-        const lds_i32* sp = s_split + c * kLevels;
-        const lds_f32* th = s_thr + c * 16;
-        int i = (xr[sp[0]] > th[0]) ? 1 : 0;
-        i = 2 * i + ((xr[sp[1]] > th[1 + i]) ? 1 : 0);
-        i = 2 * i + ((xr[sp[2]] > th[3 + i]) ? 1 : 0);
-        i = 2 * i + ((xr[sp[3]] > th[7 + i]) ? 1 : 0);
-        sI[r * a.Cp + c] = (uint8_t)i;
+      for (int cb = lane; cb < C; cb += 64) {
+        const lds_f32* th = s_thr + cb;
+        const float u0 = th[0], u1 = th[C], u2 = th[2 * C], u3 = th[3 * C], u4 = th[4 * C], u5 = th[5 * C],
+                    u6 = th[6 * C], u7 = th[7 * C], u8 = th[8 * C], u9 = th[9 * C], u10 = th[10 * C],
+                    u11 = th[11 * C], u12 = th[12 * C], u13 = th[13 * C], u14 = th[14 * C];
+        const int q0 = s_split[cb], q1 = s_split[C + cb], q2 = s_split[2 * C + cb], q3 = s_split[3 * C + cb];
+        for (int r = 0; r < RW; r += 2) {
+          const int rb = min(r + 1, RW - 1);
+          const lds_f32* pa = xa + r * a.Dp;
+          const lds_f32* pb = xa + rb * a.Dp;
+          const float a0 = pa[q0], a1 = pa[q1], a2 = pa[q2], a3 = pa[q3];
+          const float b0 = pb[q0], b1 = pb[q1], b2 = pb[q2], b3 = pb[q3];
+          sI[r * a.Cp + cb] = (uint8_t)tree_walk(a0, a1, a2, a3, u0, u1, u2, u3, u4, u5, u6, u7, u8, u9, u10, u11,
+                                                 u12, u13, u14);
+          const int ib = tree_walk(b0, b1, b2, b3, u0, u1, u2, u3, u4, u5, u6, u7, u8, u9, u10, u11, u12, u13, u14);
+          if (r + 1 < RW) sI[rb * a.Cp + cb] = (uint8_t)ib;
+        }
+      }
+    } else if (kEnc) {
+      // four independent walks per lane at a time, level by level, so their
+      // dependent threshold reads overlap; (row, codebook) pairs past the
+      // chunk repeat the lane's first pair and are not stored
+      const lds_f32* xa = reinterpret_cast<const lds_f32*>(sA);
+      const int npair = RW * C;
+      for (int p0 = lane; p0 < npair; p0 += 256) {
+        int i[4], c[4], r[4];
+        const lds_f32* xr[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int p = (p0 + 64 * q < npair) ? p0 + 64 * q : p0;
+          r[q] = (C == 1) ? p : (int)__umulhi((uint32_t)p, a.c_magic);
+          c[q] = p - r[q] * C;
+          xr[q] = xa + r[q] * a.Dp;
+          i[q] = (xr[q][s_split[c[q]]] > s_thr[c[q]]) ? 1 : 0;
+        }
+#pragma unroll
+        for (int t = 1; t < kLevels; ++t)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            i[q] = 2 * i[q] + ((xr[q][s_split[t * C + c[q]]] > s_thr[((1 << t) - 1 + i[q]) * C + c[q]]) ? 1 : 0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (p0 + 64 * q < npair) sI[r[q] * a.Cp + c[q]] = (uint8_t)i[q];
       }
     }
     if (kEnc) {
