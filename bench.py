@@ -9,6 +9,10 @@ on a bounded sample of the same workload, and a dense fp32 GEMM of the same
 shape as context.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+
+Other workloads (--workload) time the same step on their shapes; their tables
+are larger than LDS, so a step is an encode launch plus a column-tiled
+accumulate launch.
 """
 from __future__ import annotations
 
@@ -34,20 +38,33 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
+    """Hash of what defines the timed kernel: its source file, its argument
+    struct and the planner that picks its launch shape."""
+    csrc = os.path.join(ROOT, "paper_2207_05808_amd", "csrc")
+
+    def block(text, start, end):
+        i = text.index(start)
+        return text[i:text.index(end, i) + len(end)]
+
     h = hashlib.sha256()
-    for f in ("kernels.hip", "fused_gather.hip", "api.hip", "internal.hpp"):   # the fused path's sources
-        with open(os.path.join(ROOT, "paper_2207_05808_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    with open(os.path.join(csrc, "fused_gather.hip"), "rb") as fh:
+        h.update(fh.read())
+    internal = open(os.path.join(csrc, "internal.hpp")).read()
+    h.update(block(internal, "struct GArgs {", "};").encode())
+    api = open(os.path.join(csrc, "api.hip")).read()
+    h.update(block(api, "bool plan_gfused(", "\n}\n").encode())
     return h.hexdigest()[:16]
 
 
 def algorithmic_bytes(spec, N) -> int:
     """Bytes the fused path must move per launch, each counted once: every row
     of A (4 D bytes; the split columns touch every 64-byte segment of a row),
-    every output (4 M bytes), the int8 table (16 C M bytes), and the trees
-    (4 split ints + 15 thresholds per codebook), scales and offsets."""
+    every output (4 M bytes), the table (16 C M entries, int8 or fp32), the
+    trees (4 split ints + 15 thresholds per codebook) and, for int8 tables,
+    the scales and offsets."""
     per_row = 4 * spec.D + 4 * spec.M
-    fixed = 16 * spec.C * spec.M + spec.C * (4 * 4 + 15 * 4) + 2 * 4 * spec.C
+    entry = 1 if spec.quantized else 4
+    fixed = 16 * spec.C * spec.M * entry + spec.C * (4 * 4 + 15 * 4) + (2 * 4 * spec.C if spec.quantized else 0)
     return N * per_row + fixed
 
 
@@ -70,21 +87,29 @@ def stored_traffic(workload: str, kh: str):
         return None
 
 
-def cpu_baseline(p, lut, scale, offset, budget_s: float):
+def cpu_baseline(p, budget_s: float):
     """The oracle as it stands, timed on whole passes over the workload's rows
     (or a prefix of them, if one pass would exceed the budget) until about
     `budget_s` seconds of host time have been spent."""
     import oracle
     o = oracle.get()
-    probe = min(p.N, 2048)
+    if p.spec.quantized:
+        lut, scale, offset = o.build_quantized_lut(p.P, p.B)
+        run = lambda A: o.matmul(A, p.split, p.thr, lut, scale, offset)
+        what = "int8"
+    else:
+        lut = o.build_lut_f32(p.P, p.B)
+        run = lambda A: o.matmul_f32(A, p.split, p.thr, lut)
+        what = "fp32"
+    probe = min(p.N, 256 if p.spec.C * p.spec.M > 100000 else 2048)
     t = time.perf_counter()
-    o.matmul(p.A[:probe], p.split, p.thr, lut, scale, offset)
+    run(p.A[:probe])
     per_row = max((time.perf_counter() - t) / probe, 1e-9)
     rows = int(min(p.N, max(probe, budget_s / per_row)))
     done, passes = 0, 0
     t = time.perf_counter()
     while True:
-        o.matmul(p.A[:rows], p.split, p.thr, lut, scale, offset)
+        run(p.A[:rows])
         done += rows
         passes += 1
         if time.perf_counter() - t >= budget_s:
@@ -92,7 +117,7 @@ def cpu_baseline(p, lut, scale, offset, budget_s: float):
     dt = time.perf_counter() - t
     return {"value": done / dt, "unit": "rows/s", "cores": o.max_threads(), "kind": "oracle",
             "sample": f"{passes} pass(es) over the first {rows} of {p.N} rows, full encode + "
-                      f"int8 lookup-accumulate, {dt:.1f} s wall"}
+                      f"{what} lookup-accumulate, {dt:.1f} s wall"}
 
 
 def main():
@@ -121,8 +146,6 @@ def main():
 
     name = args.workload or W.HEADLINE
     spec = W.SPECS[name]
-    if not spec.quantized:
-        raise SystemExit("bench.py times the int8 fused path; pick a quantized workload")
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     log(f"[bench] drawing workload {name}: N={spec.N} D={spec.D} C={spec.C} M={spec.M}")
@@ -134,12 +157,20 @@ def main():
     A_bufs = [torch.from_numpy(p.A).to(dev) for _ in range(2)]
     split = torch.from_numpy(p.split).to(dev)
     thr = torch.from_numpy(p.thr).to(dev)
-    lut, scale, offset = mdn.build_lut(torch.from_numpy(p.P).to(dev), torch.from_numpy(p.B).to(dev))
+    Pd, Bd = torch.from_numpy(p.P).to(dev), torch.from_numpy(p.B).to(dev)
+    if spec.quantized:
+        lut, scale, offset = mdn.build_lut(Pd, Bd)
+    else:
+        lut, scale, offset = mdn.build_lut_f32(Pd, Bd), None, None
+    del Pd
     y = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
 
     # arguments marshalled once per input buffer: a step is one C-ABI call
-    calls = [mdn.prepare_matmul(A_bufs[j], split, thr, lut, scale, offset, y_out=y) for j in range(2)]
+    if spec.quantized:
+        calls = [mdn.prepare_matmul(A_bufs[j], split, thr, lut, scale, offset, y_out=y) for j in range(2)]
+    else:
+        calls = [mdn.prepare_matmul_f32(A_bufs[j], split, thr, lut, y_out=y) for j in range(2)]
 
     def step(i):
         calls[i % 2]()
@@ -174,25 +205,57 @@ def main():
     achieved = abytes / avg_kern_s / 1e9
     kh = kernel_source_hash()
     traffic = stored_traffic(name, kh)
+    headline = name == W.HEADLINE
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes": abytes, "kernel_us": round(avg_kern_s * 1e6, 2),
-                "kernel": "gfused_kernel<int8> (maddness_matmul)", "kernel_source_hash": kh}
+                "kernel": ("gfused_kernel<int8> (maddness_matmul, one launch per step)" if headline else
+                           "whole step (maddness_matmul%s: encode + column-tiled accumulate launches)"
+                           % ("" if spec.quantized else "_f32")),
+                "kernel_source_hash": kh}
 
     result = {
         "metric": "rows/sec + achieved HBM GB/s (fraction of peak) for fused encode+LUT matmul",
         "value": round(value, 1), "unit": "rows/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "fp32 in / int8 table / int32 accumulate", "data": "synthetic",
+        "vs_baseline": None,
+        "dtype": "fp32 in / int8 table / int32 accumulate" if spec.quantized else "fp32 in / fp32 table / fp32 accumulate",
+        "data": "synthetic",
         "config": {"workload": name, "N": N, "D": spec.D, "C": spec.C, "K": 16, "M": spec.M,
-                   "table": "int8 block floating point", "parallelism": "single GPU"},
+                   "table": "int8 block floating point" if spec.quantized else "fp32",
+                   "parallelism": "single GPU"},
         "roofline": roofline,
     }
 
     if not args.no_context:
+        # the two steps as separate calls (encode to an index buffer, then the
+        # accumulate-only entry point), same region timing as the fused step
+        idx = torch.empty((N, spec.C), dtype=torch.uint8, device=dev)
+        split_calls = [lambda j=j: mdn.encode(A_bufs[j], split, thr, idx_out=idx, validate=False) for j in range(2)]
+        if spec.quantized:
+            acc_call = lambda: mdn.lut_accumulate(idx, lut, scale, offset, y_out=y, validate=False)
+        else:
+            acc_call = lambda: mdn.lut_accumulate_f32(idx, lut, y_out=y)
+
+        def region_us(fn, reps=20):
+            for i in range(3):
+                fn(i)
+            torch.cuda.synchronize()
+            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            r0.record(stream)
+            for i in range(reps):
+                fn(i)
+            r1.record(stream)
+            torch.cuda.synchronize()
+            return r0.elapsed_time(r1) / reps * 1e3
+
+        enc_us = region_us(lambda i: split_calls[i % 2]())
+        acc_us = region_us(lambda i: acc_call())
+        result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
+        del idx
+
         # dense fp32 GEMM of the same shape (torch -> hipBLASLt / rocBLAS), TF32 off
         torch.backends.cuda.matmul.allow_tf32 = False
-        Bd = torch.from_numpy(p.B).to(dev)
         out = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
         for _ in range(3):
             torch.mm(A_bufs[0], Bd, out=out)
@@ -205,10 +268,10 @@ def main():
         g1.record()
         torch.cuda.synchronize()
         gms = g0.elapsed_time(g1) / reps
-        result["context"] = {"dense_fp32_gemm_us": round(gms * 1e3, 2),
-                             "dense_fp32_gemm_tflops": round(2.0 * N * spec.D * spec.M / (gms / 1e3) / 1e12, 2),
-                             "fused_speedup_vs_gemm": round(gms / 1e3 / avg_kern_s, 3)}
-        del out, Bd
+        result["context"].update({"dense_fp32_gemm_us": round(gms * 1e3, 2),
+                                  "dense_fp32_gemm_tflops": round(2.0 * N * spec.D * spec.M / (gms / 1e3) / 1e12, 2),
+                                  "fused_speedup_vs_gemm": round(gms / 1e3 / avg_kern_s, 3)})
+        del out
 
     if args.copy_calibration_mb > 0:
         nb = args.copy_calibration_mb << 20
@@ -222,9 +285,7 @@ def main():
 
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s)")
-        import oracle
-        rl, rs, ro = oracle.get().build_quantized_lut(p.P, p.B)
-        result["cpu_baseline"] = cpu_baseline(p, rl, rs, ro, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(p, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
 

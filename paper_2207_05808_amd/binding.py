@@ -268,6 +268,29 @@ class PreparedCall:
         return self.outputs
 
 
+def prepare_matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None, stream=None, validate=False):
+    """Prepared maddness_matmul_f32; ``call()`` returns (y, idx or None)."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    _need(lut, "lut", torch.float32, 3)
+    _dense(lut, "lut")
+    C2, M = lut.shape[0], lut.shape[2]
+    if lut.shape[1] != K:
+        raise ValueError("lut must be [C,16,M]")
+    if C2 != C:
+        raise ValueError("lut codebooks differ from the trees'")
+    if validate:
+        _validate_trees(split_dims, D)
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
+    _need(y_out, "y_out", torch.float32, 2)
+    _dense(y_out, "y_out")
+    args = (_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut), M, _ptr(y_out),
+            _ptr(idx_out), _stream(stream))
+    keep = (A, split_dims, thresholds, lut, y_out, idx_out)
+    return PreparedCall("maddness_matmul_f32", args, keep, (y_out, idx_out))
+
+
 def prepare_matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, acc_out=None,
                    idx_out=None, stream=None, validate=False):
     """Prepared maddness_matmul; ``call()`` returns (y, acc or None, idx or None)."""
