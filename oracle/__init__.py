@@ -15,6 +15,7 @@ Functions and the passages they follow (the paper: McCarter & Dronen,
 * :func:`lut_accumulate_f32` -- same sum over an unquantized fp32 table.
 * :func:`build_table` -- §2.2 (T = P B).
 * :func:`quantize_table` -- §1 (8-bit block floating point), reading R6.
+* :func:`sigma` -- §2.2 (layer output: bias, then ReLU or row softmax), R19.
 """
 from __future__ import annotations
 
@@ -70,6 +71,7 @@ class Oracle:
         lib.oracle_dequant_params.argtypes = [vp, vp, i32, vp, vp, vp]
         lib.oracle_exponent_cap.argtypes = [i32]
         lib.oracle_block_exponent.argtypes = [ctypes.c_float, vp]
+        lib.oracle_sigma.argtypes = [vp, i64, i32, vp, i32, vp]
         self.lib = lib
 
     @staticmethod
@@ -175,6 +177,22 @@ class Oracle:
         e = np.zeros(1, dtype=np.int32)
         rc = self.lib.oracle_block_exponent(ctypes.c_float(s), e.ctypes.data)
         return None if rc != 0 else int(e[0])
+
+    def sigma(self, y, bias=None, act=0):
+        """Layer output sigma: 0 none, 1 bias, 2 bias + ReLU, 3 bias + row softmax
+        (float64 [N, M])."""
+        y = np.ascontiguousarray(y, dtype=np.float32)
+        N, M = y.shape
+        out = np.zeros((N, M), dtype=np.float64)
+        bp = None
+        if bias is not None:
+            bias = np.ascontiguousarray(bias, dtype=np.float32)
+            if bias.shape != (M,):
+                raise OracleError("bias must be [M]")
+            bp = bias.ctypes.data
+        rc = self.lib.oracle_sigma(y.ctypes.data, N, M, bp, int(act), out.ctypes.data)
+        self._check(rc, "oracle_sigma")
+        return out
 
     # convenience compositions (no arithmetic of their own)
     def matmul(self, A, split, thr, lut, scale, offset):

@@ -30,6 +30,8 @@
  *   R9  y = fl32( float(acc) * 2^e_min + bias32 ), one rounding (fmaf), with
  *       bias32 = fl32( sum_c offset_c accumulated in double, c ascending ).
  *   R10 unquantized mode: y = (((0 + T_0) + T_1) + ...) in fp32, c ascending.
+ *   R19 layer output sigma: z = fl32(y + bias_m); ReLU keeps z when z > 0 and
+ *       gives +0 otherwise; softmax is taken over the M outputs of a row.
  *
  * Every entry point returns 0 on success and a negative code on a violated
  * precondition (it never aborts): -1 bad size / pointer, -2 a scale that is
@@ -42,7 +44,7 @@
 #include <stdlib.h>
 
 #define ORACLE_K 16      /* prototypes per codebook: 2^4 leaves         */
-#define ORACLE_LEVELS 4  /* "exactly 4 comparisons" per subvector, §2.1 */
+#define ORACLE_LEVELS 4  /* one comparison per tree level, §2.1              */
 #define ORACLE_NODES 15  /* internal nodes of a balanced 4-level tree   */
 
 int oracle_version(void) { return 1; }
@@ -59,7 +61,8 @@ int oracle_max_threads(void) {
 /*
  * Encoding function (§1: each subvector is mapped to the index of one of K
  * prototypes, a log2(K)-bit integer; §1 and §2.1: MADDNESS does it with a
- * balanced binary regression tree, exactly 4 comparisons for K = 16).
+ * balanced binary regression tree, one comparison per level, four levels for
+ * K = 16).
  * Walk the tree of codebook c from the root: at level t the current node is
  * i (0 <= i < 2^t), its threshold is thresholds[c][2^t - 1 + i], and the
  * compared value is A[n][split[c][t]].  The next node is 2i + bit.
@@ -293,5 +296,46 @@ int oracle_round_table_f32(const double* T, int64_t n, float* out)
 {
     if (n < 0 || (n > 0 && (!T || !out))) return -1;
     for (int64_t j = 0; j < n; ++j) out[j] = (float)T[j];
+    return 0;
+}
+
+/*
+ * Layer output sigma(AB) (§2.2: the bias term composed with a nonlinearity,
+ * elementwise such as ReLU or row-wise such as softmax; reading R19).
+ * act: 0 none, 1 bias only, 2 bias then ReLU, 3 bias then softmax over each
+ * row.  y and bias are fp32 (bias may be NULL: no bias); out is [N][M]
+ * double.  The bias add is one fp32 rounding, z = fl32(y + bias[m]); ReLU is
+ * z if z > 0 else +0 (so -0 and NaN give +0); softmax is evaluated in double
+ * from the fp32 z: p_m = exp(z_m - max_j z_j) / sum_j exp(z_j - max_j z_j),
+ * the sum taken in ascending j.
+ */
+int oracle_sigma(const float* y, int64_t N, int32_t M, const float* bias,
+                 int32_t act, double* out)
+{
+    if (N < 0 || M <= 0 || act < 0 || act > 3) return -1;
+    if (N > 0 && (!y || !out)) return -1;
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        const float* yr = y + n * M;
+        double* o = out + n * M;
+        for (int32_t m = 0; m < M; ++m) {
+            float z = yr[m];
+            if (act >= 1 && bias) z = z + bias[m];
+            if (act == 2) z = (z > 0.0f) ? z : 0.0f;
+            o[m] = (double)z;
+        }
+        if (act == 3) {
+            double mx = o[0];
+            for (int32_t m = 1; m < M; ++m)
+                if (o[m] > mx) mx = o[m];
+            double sum = 0.0;
+            for (int32_t m = 0; m < M; ++m) {
+                o[m] = exp(o[m] - mx);
+                sum += o[m];
+            }
+            for (int32_t m = 0; m < M; ++m) o[m] = o[m] / sum;
+        }
+    }
     return 0;
 }

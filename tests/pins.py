@@ -423,9 +423,58 @@ def check_rejects_bad_inputs(orc):
         raise AssertionError("split column outside [0, D) accepted")
 
 
+def check_sigma_bias_relu(orc, seed=11):
+    """Layer output, elementwise part (§2.2, reading R19): the bias add is one
+    fp32 rounding (numpy float32 addition) and ReLU keeps z > 0 and gives +0
+    otherwise, -0 included."""
+    rng = np.random.default_rng(seed)
+    y = rng.standard_normal((37, 13)).astype(np.float32)
+    y[0, :4] = [0.0, -0.0, 1e-30, -1e-30]
+    b = rng.standard_normal(13).astype(np.float32)
+    z32 = y + b[None, :]                       # float32 + float32: one rounding
+    assert z32.dtype == np.float32
+    assert np.array_equal(orc.sigma(y, None, 0), y.astype(np.float64))
+    assert np.array_equal(orc.sigma(y, b, 1), z32.astype(np.float64))
+    r = orc.sigma(y, b, 2)
+    assert np.array_equal(r, np.maximum(z32, np.float32(0)).astype(np.float64))
+    assert not np.any(np.signbit(r))
+    r0 = orc.sigma(np.array([[-0.0, 0.0, -1.0, 2.5]], np.float32), None, 2)
+    assert np.array_equal(r0, [[0.0, 0.0, 0.0, 2.5]]) and not np.any(np.signbit(r0))
+
+
+def check_sigma_softmax(orc, seed=12):
+    """Layer output, row-wise part (§2.2, R19): two columns reduce to the
+    logistic function, rows match scipy's softmax and sum to one, a constant
+    row shift (an exactly representable bias) changes nothing, equal entries
+    give 1/M, large entries do not overflow, and the bias is per column."""
+    from scipy.special import expit
+    from scipy.special import softmax as sp_softmax
+    rng = np.random.default_rng(seed)
+    y2 = (rng.standard_normal((50, 2)) * 4).astype(np.float32)
+    p = orc.sigma(y2, None, 3)
+    assert np.allclose(p[:, 0], expit(y2[:, 0].astype(np.float64) - y2[:, 1].astype(np.float64)), rtol=1e-14, atol=0)
+    y = (rng.standard_normal((64, 37)) * 3).astype(np.float32)
+    p = orc.sigma(y, None, 3)
+    assert np.all(p > 0)
+    assert np.allclose(p.sum(axis=1), 1.0, rtol=0, atol=1e-14)
+    assert np.allclose(p, sp_softmax(y.astype(np.float64), axis=1), rtol=1e-13, atol=0)
+    yg = (np.round(rng.standard_normal((16, 9)) * 1024) / 1024).astype(np.float32)   # y + 256 exact
+    assert np.allclose(orc.sigma(yg, np.full(9, 256.0, np.float32), 3), orc.sigma(yg, None, 3), rtol=1e-14, atol=0)
+    assert np.allclose(orc.sigma(np.full((3, 7), 5.5, np.float32), None, 3), 1.0 / 7, rtol=1e-15, atol=0)
+    e = math.exp(-1.0)
+    for base in (1000.0, -1000.0):   # no overflow, no underflow to 0/0
+        big = orc.sigma(np.array([[base, base - 1.0, base]], np.float32), None, 3)
+        assert np.allclose(big[0], [1 / (2 + e), e / (2 + e), 1 / (2 + e)], rtol=1e-14, atol=0)
+    b = np.array([0.0, np.float32(math.log(3.0))], np.float32)
+    pb = orc.sigma(np.zeros((2, 2), np.float32), b, 3)
+    w = math.exp(float(b[1]))
+    assert np.allclose(pb, [[1 / (1 + w), w / (1 + w)]] * 2, rtol=1e-14, atol=0)
+
+
 ALL_CHECKS = [
     check_encode_brute_force, check_encode_search_tree, check_encode_nan, check_encode_permutation,
     check_encode_golden, check_one_hot_identity, check_decoder_table, check_output_rounding,
     check_scale_linearity, check_f32_order, check_table_build, check_quantizer,
     check_f32_reconstruction, check_quantized_reconstruction, check_rejects_bad_inputs,
+    check_sigma_bias_relu, check_sigma_softmax,
 ]

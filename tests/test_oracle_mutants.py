@@ -35,6 +35,12 @@ MUTANTS = [
     ("exponent one too large", "        offset[c] = o;\n        ec[c] = e;", "        offset[c] = o;\n        ec[c] = e + 1;"),
     ("exponent floor ignored", "if (e < emax - cap) e = emax - cap;", "(void)cap;"),
     ("offset not the midrange", "float o = (float)((lo + hi) / 2.0);", "float o = (float)lo;"),
+    ("layer bias subtracted", "z = z + bias[m];", "z = z - bias[m];"),
+    ("ReLU keeps -0", "z = (z > 0.0f) ? z : 0.0f;", "z = (z >= 0.0f) ? z : 0.0f;"),
+    ("softmax without the max shift", "o[m] = exp(o[m] - mx);", "o[m] = exp(o[m]);"),
+    ("softmax max not initialised from the row", "double mx = o[0];", "double mx = 0.0;"),
+    ("softmax normalised by the first term", "for (int32_t m = 0; m < M; ++m) o[m] = o[m] / sum;",
+     "for (int32_t m = M - 1; m >= 0; --m) o[m] = o[m] / o[0];"),
 ]
 
 
