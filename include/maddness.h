@@ -17,10 +17,11 @@
  *    library keeps no pointer after the call returns; the caller keeps the
  *    buffers alive until the work on `stream` has completed.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  The
- *    calls only enqueue work on it: no host synchronisation.  Only
- *    maddness_matmul / maddness_matmul_f32 may allocate (stream-ordered) a
- *    temporary index buffer, when idx_out is NULL and the table is too large
- *    for one LDS tile; every other call allocates nothing.
+ *    calls only enqueue work on it: no host synchronisation.  Only the fused
+ *    entry points (maddness_matmul, maddness_matmul_f32, maddness_matmul_act,
+ *    maddness_matmul_act_f32) may allocate (stream-ordered) a temporary index
+ *    buffer, when the table is too large for one LDS tile (and, for the first
+ *    two, idx_out is NULL); every other call allocates nothing.
  *  - Row-major layouts.  A has row stride `lda` (elements, lda >= D); every
  *    other array is dense.
  *  - Return value: MADDNESS_OK or an error status (never aborts, never
@@ -49,6 +50,15 @@ enum {
     MADDNESS_EHIP = 2,         /* a HIP runtime call or a launch failed     */
     MADDNESS_EUNSUPPORTED = 3, /* shape beyond what the kernels handle      */
     MADDNESS_ENOMEM = 4        /* temporary index buffer could not be made  */
+};
+
+/* Layer output sigma for maddness_matmul_act[_f32] (§2.2: the bias term
+   composed with an elementwise or a row-wise nonlinearity). */
+enum {
+    MADDNESS_ACT_NONE = 0,     /* y                                          */
+    MADDNESS_ACT_BIAS = 1,     /* z = y + bias[m]                            */
+    MADDNESS_ACT_RELU = 2,     /* z > 0 ? z : +0                             */
+    MADDNESS_ACT_SOFTMAX = 3   /* softmax of z over the M outputs of a row   */
 };
 
 #define MADDNESS_K 16          /* prototypes per codebook (4-bit indices)   */
@@ -139,6 +149,35 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda,
                         const int32_t* split_dims, const float* thresholds,
                         int32_t C, const float* lut, int32_t M, float* y_out,
                         uint8_t* idx_out, void* stream);
+
+/*
+ * Fused encode + lookup-accumulate followed by the layer output sigma
+ * (§2.2: deep learning needs sigma(A B), the bias term composed with a
+ * nonlinearity -- elementwise such as ReLU, or row-wise such as softmax for
+ * a classifier).  y is formed exactly as by maddness_matmul, then
+ *   z[n][m] = fl32(y[n][m] + col_bias[m])   (act >= MADDNESS_ACT_BIAS;
+ *                                            col_bias NULL: no bias)
+ *   MADDNESS_ACT_RELU:    out = z > 0 ? z : +0 (bit-exact, -0 and NaN give +0)
+ *   MADDNESS_ACT_SOFTMAX: out[n][m] = exp(z[n][m] - max_j z[n][j]) /
+ *                         sum_j exp(z[n][j] - max_j z[n][j]), evaluated in
+ *                         fp32 (expf, any summation order): each entry is
+ *                         within (|z - max| + M + 5) * 2^-24 relative of the
+ *                         exact value (plus underflow below 2^-126).
+ * col_bias [M] fp32, 4-byte aligned.  EINVAL: act outside 0..3, plus the
+ * conditions of maddness_matmul; ENOMEM as for maddness_matmul.
+ */
+int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda,
+                        const int32_t* split_dims, const float* thresholds,
+                        int32_t C, const int8_t* lut, const float* scale,
+                        const float* offset, int32_t M, const float* col_bias,
+                        int32_t act, float* y_out, void* stream);
+
+/* The same with an unquantized fp32 table (see maddness_matmul_f32). */
+int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda,
+                            const int32_t* split_dims, const float* thresholds,
+                            int32_t C, const float* lut, int32_t M,
+                            const float* col_bias, int32_t act, float* y_out,
+                            void* stream);
 
 /*
  * Offline table construction (§2.2: T = P B) followed by 8-bit block

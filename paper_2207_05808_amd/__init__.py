@@ -7,7 +7,8 @@ C ABI of include/maddness.h.
 The entry points load lazily, so ``paper_2207_05808_amd.workloads`` (the
 seeded input generator) imports without torch or the HIP library.
 """
-_BINDING = ("encode", "lut_accumulate", "lut_accumulate_f32", "matmul", "matmul_f32",
+_BINDING = ("encode", "lut_accumulate", "lut_accumulate_f32", "matmul", "matmul_f32", "matmul_act",
+            "matmul_act_f32",
             "build_lut", "build_lut_f32", "version", "prepare_matmul", "prepare_matmul_f32",
             "PreparedCall")
 

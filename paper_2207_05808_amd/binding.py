@@ -206,6 +206,74 @@ def matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None, want_id
     return y_out, idx_out
 
 
+ACT = {"none": 0, "bias": 1, "relu": 2, "softmax": 3}
+
+
+def _act(act):
+    if isinstance(act, str):
+        if act not in ACT:
+            raise ValueError(f"act must be one of {sorted(ACT)}")
+        return ACT[act]
+    return int(act)
+
+
+def _col_bias(col_bias, M):
+    if col_bias is None:
+        return None
+    _need(col_bias, "col_bias", torch.float32, 1)
+    _dense(col_bias, "col_bias")
+    if col_bias.shape[0] != M:
+        raise ValueError("col_bias must be [M]")
+    return col_bias
+
+
+def matmul_act(A, split_dims, thresholds, lut, scale, offset, col_bias=None, act="relu", y_out=None,
+               stream=None, validate=False):
+    """Fused encode + lookup-accumulate + layer output sigma (bias, then
+    "relu" / "softmax"; "bias" or "none" also accepted); returns y."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    C2, M = _lut_i8(lut, scale, offset)
+    if C2 != C:
+        raise ValueError("lut codebooks differ from the trees'")
+    col_bias = _col_bias(col_bias, M)
+    if validate:
+        _validate_trees(split_dims, D)
+        _validate_scales(scale)
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
+    _need(y_out, "y_out", torch.float32, 2)
+    _dense(y_out, "y_out")
+    st = _lib.lib().maddness_matmul_act(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut),
+                                        _ptr(scale), _ptr(offset), M, _ptr(col_bias), _act(act), _ptr(y_out),
+                                        _stream(stream))
+    _lib.check("maddness_matmul_act", st)
+    return y_out
+
+
+def matmul_act_f32(A, split_dims, thresholds, lut, col_bias=None, act="relu", y_out=None, stream=None,
+                   validate=False):
+    """matmul_act over an unquantized fp32 table; returns y."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    _need(lut, "lut", torch.float32, 3)
+    _dense(lut, "lut")
+    if lut.shape[0] != C or lut.shape[1] != K:
+        raise ValueError("lut must be [C,16,M]")
+    M = lut.shape[2]
+    col_bias = _col_bias(col_bias, M)
+    if validate:
+        _validate_trees(split_dims, D)
+    if y_out is None:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
+    _need(y_out, "y_out", torch.float32, 2)
+    _dense(y_out, "y_out")
+    st = _lib.lib().maddness_matmul_act_f32(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
+                                            _ptr(lut), M, _ptr(col_bias), _act(act), _ptr(y_out), _stream(stream))
+    _lib.check("maddness_matmul_act_f32", st)
+    return y_out
+
+
 def build_lut(P, B, stream=None):
     """Table T = P B, 8-bit block-FP quantized; returns (lut int8 [C,16,M], scale [C], offset [C])."""
     _need(P, "P", torch.float32, 3)

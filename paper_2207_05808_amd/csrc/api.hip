@@ -29,6 +29,7 @@ struct Shape {
   const void* lut; const float* scale; const float* offset; int M;
   const uint8_t* idx_in;
   float* y; int32_t* acc; uint8_t* idx_out;
+  const float* col_bias; int act;   // layer output sigma (fused entry points only)
 };
 
 // LDS layout for one workgroup of `nw` wavefronts.
@@ -231,6 +232,8 @@ bool plan_gfused(const Shape& s, GArgs* g, int* ng_out, int* uq_out, int* nw_out
   a.lpr_log2 = ilog2(best_lpr);
   a.vec_out = (s.M % 4 == 0) && aligned(s.y, 16) && (s.acc == nullptr || aligned(s.acc, 16));
   a.vec16 = aligned(s.lut, 16) && (s.elem == kF32 ? (s.M % 4 == 0) : (s.M % 16 == 0));
+  a.col_bias = s.col_bias;
+  a.act = s.act;
   if ((int64_t)a.R * s.lda * 4 >= (1ll << 31)) return false;   // 32-bit per-lane gather offsets
   const int64_t tab = (int64_t)(s.C * kK + 1) * (s.elem == kF32 ? a.rs32 : a.rs16);
   if (tab > kLdsBytes) return false;
@@ -242,6 +245,7 @@ bool plan_gfused(const Shape& s, GArgs* g, int* ng_out, int* uq_out, int* nw_out
     a.off_shc = take(s.C * 4);
     a.off_misc = take(32);
     a.off_wave = take((int64_t)nw * a.R * a.NSP * 4);
+    a.off_bias = take(s.act ? 8 * ((s.M + 7) / 8) * 4 : 0);   // bias row, whole octets of columns
     if (off <= kLdsBytes || nw == 1) break;
   }
   a.lds_total = off;
@@ -280,6 +284,8 @@ bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
   a.vec_lut = aligned(s.lut, 16) && (s.M % upc == 0);
   a.vec_idx = (s.C % 4 == 0) && aligned(s.idx_in, 4);
   a.vec_out = (s.M % 4 == 0) && (s.y == nullptr || aligned(s.y, 16)) && (s.acc == nullptr || aligned(s.acc, 16));
+  a.col_bias = s.col_bias;
+  a.act = (s.act == 3 && a.ntm > 1) ? 1 : s.act;   // rows over several tiles: softmax as a second pass
   int off = 0;
   auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
   a.off_tab = take(a.CT * kK * a.Mt * (f32 ? 4 : 2));   // 0: the kernel relies on it
@@ -305,7 +311,12 @@ int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
 int accumulate(const Shape& s, hipStream_t stream) {
   TArgs t;
   int nj, nw;
-  if (plan_tacc(s, &t, &nj, &nw)) return status_from(launch_tacc(s.elem, nj, t, nw, device_cus(), stream));
+  if (plan_tacc(s, &t, &nj, &nw)) {
+    const int rc = status_from(launch_tacc(s.elem, nj, t, nw, device_cus(), stream));
+    if (rc != MADDNESS_OK || t.act == s.act) return rc;
+    return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
+  }
+  if (s.act != 0) return MADDNESS_EUNSUPPORTED;   // the general path has no sigma epilogue
   return run(s, false, stream);
 }
 
@@ -461,6 +472,52 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda, const
   Plan p;
   if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
   return two_phase(s, idx_out, st);
+}
+
+int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
+                        const float* thresholds, int32_t C, const int8_t* lut, const float* scale,
+                        const float* offset, int32_t M, const float* col_bias, int32_t act, float* y_out,
+                        void* stream) {
+  if (act < MADDNESS_ACT_NONE || act > MADDNESS_ACT_SOFTMAX) return MADDNESS_EINVAL;
+  int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
+  if (rc != MADDNESS_OK) return rc;
+  rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!scale || !offset || !y_out || !aligned(scale, 4) || !aligned(offset, 4) || !aligned(y_out, 4) ||
+      (col_bias && !aligned(col_bias, 4)))
+    return MADDNESS_EINVAL;
+  Shape s = shape(kFused, kI8);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
+  s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out;
+  s.col_bias = col_bias; s.act = act;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GArgs g;
+  int ng, uq, nw;
+  if (plan_gfused(s, &g, &ng, &uq, &nw))
+    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
+  return two_phase(s, nullptr, st);
+}
+
+int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
+                            const float* thresholds, int32_t C, const float* lut, int32_t M,
+                            const float* col_bias, int32_t act, float* y_out, void* stream) {
+  if (act < MADDNESS_ACT_NONE || act > MADDNESS_ACT_SOFTMAX) return MADDNESS_EINVAL;
+  int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
+  if (rc != MADDNESS_OK) return rc;
+  rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!y_out || !aligned(lut, 4) || !aligned(y_out, 4) || (col_bias && !aligned(col_bias, 4)))
+    return MADDNESS_EINVAL;
+  Shape s = shape(kFused, kF32);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
+  s.lut = lut; s.M = M; s.y = y_out;
+  s.col_bias = col_bias; s.act = act;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GArgs g;
+  int ng, uq, nw;
+  if (plan_gfused(s, &g, &ng, &uq, &nw))
+    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
+  return two_phase(s, nullptr, st);
 }
 
 int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D, int32_t M, int8_t* lut_out,

@@ -43,6 +43,7 @@ typedef __attribute__((address_space(3))) uint32_t glds_u32;
 typedef __attribute__((address_space(3))) u32x4g glds_u32x4;
 typedef __attribute__((address_space(3))) u32x2g glds_u32x2;
 typedef __attribute__((address_space(3))) f32x4g glds_f32x4;
+typedef __attribute__((address_space(3))) float glds_f32;
 
 // third descriptor dword for a raw (untyped, unswizzled) buffer on gfx9-family chips
 constexpr int kBufferDword3 = 0x00020000;
@@ -282,6 +283,11 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
     glds_i32* all_off = reinterpret_cast<glds_i32*>(smem + g.off_wave);
     for (int u = tid; u < nw * g.R * NSP; u += blockDim.x) all_off[u] = rows * rs;
   }
+  if (g.act != 0) {
+    // layer bias row, zero past M (and everywhere without a bias)
+    glds_f32* sbias = reinterpret_cast<glds_f32*>(smem + g.off_bias);
+    for (int u = tid; u < 8 * no; u += blockDim.x) sbias[u] = (g.col_bias && u < M) ? g.col_bias[u] : 0.0f;
+  }
   __syncthreads();
 
   const float bias = __int_as_float(uni(s_misc[0]));
@@ -435,36 +441,89 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
 
       // epilogue: 8 columns per lane-slot
       const int64_t row = row0 + rr;
-      if (rr < R && row < N) {
+      const bool store = rr < R && row < N;
+      auto store_slot = [&](int u, const float (&o)[8]) {
         float* yrow = g.y + row * M;
         int32_t* arow = (ELEM == kI8 && g.acc) ? g.acc + row * M : nullptr;
 #pragma unroll
-        for (int u = 0; u < UQ; ++u) {
-          float out[8];
+        for (int h = 0; h < 2; ++h) {
+          const int qd = cg + 2 * LPR * u + h * LPR;
+          if (qd >= nq4) continue;
+          const int mh = 4 * qd;
+          if (g.vec_out && mh + 4 <= M) {
+            __builtin_nontemporal_store((f32x4g){o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]},
+                                        reinterpret_cast<f32x4g*>(yrow + mh));
+            if (arow)
+              __builtin_nontemporal_store((u32x4g){(uint32_t)iacc[u][4 * h], (uint32_t)iacc[u][4 * h + 1],
+                                                   (uint32_t)iacc[u][4 * h + 2], (uint32_t)iacc[u][4 * h + 3]},
+                                          reinterpret_cast<u32x4g*>(arow + mh));
+          } else {
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            out[e] = (ELEM == kI8) ? __builtin_fmaf((float)iacc[u][e], step, bias) : facc[u][e];
+            for (int e = 0; e < 4; ++e)
+              if (mh + e < M) {
+                yrow[mh + e] = o[4 * h + e];
+                if (arow) arow[mh + e] = iacc[u][4 * h + e];
+              }
+          }
+        }
+      };
+      if (g.act == 0) {
+        if (store) {
+#pragma unroll
+          for (int u = 0; u < UQ; ++u) {
+            float o[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              o[e] = (ELEM == kI8) ? __builtin_fmaf((float)iacc[u][e], step, bias) : facc[u][e];
+            store_slot(u, o);
+          }
+        }
+      } else {
+        // layer output sigma: z = y + bias, then ReLU, or a softmax over the
+        // row's LPR lanes (every lane takes part in the reductions)
+        float out[UQ][8];
+        const glds_f32* sbias = reinterpret_cast<const glds_f32*>(smem + g.off_bias);
+        float vmax = -__builtin_inff();
+#pragma unroll
+        for (int u = 0; u < UQ; ++u)
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
             const int qd = cg + 2 * LPR * u + h * LPR;
-            if (qd >= nq4) continue;
-            const int mh = 4 * qd;
-            if (g.vec_out && mh + 4 <= M) {
-              __builtin_nontemporal_store((f32x4g){out[4 * h], out[4 * h + 1], out[4 * h + 2], out[4 * h + 3]},
-                                          reinterpret_cast<f32x4g*>(yrow + mh));
-              if (arow)
-                __builtin_nontemporal_store((u32x4g){(uint32_t)iacc[u][4 * h], (uint32_t)iacc[u][4 * h + 1],
-                                                     (uint32_t)iacc[u][4 * h + 2], (uint32_t)iacc[u][4 * h + 3]},
-                                            reinterpret_cast<u32x4g*>(arow + mh));
-            } else {
+            const f32x4g bv = *reinterpret_cast<const glds_f32x4*>(sbias + 4 * min(qd, nq4 - 1));
 #pragma unroll
-              for (int e = 0; e < 4; ++e)
-                if (mh + e < M) {
-                  yrow[mh + e] = out[4 * h + e];
-                  if (arow) arow[mh + e] = iacc[u][4 * h + e];
-                }
+            for (int e = 0; e < 4; ++e) {
+              const float y0 = (ELEM == kI8) ? __builtin_fmaf((float)iacc[u][4 * h + e], step, bias)
+                                             : facc[u][4 * h + e];
+              float z = y0 + bv[e];
+              if (g.act == 2) z = (z > 0.0f) ? z : 0.0f;
+              out[u][4 * h + e] = z;
+              if (4 * qd + e < M) vmax = __builtin_fmaxf(vmax, z);
             }
           }
+        if (g.act == 3) {
+          for (int o = 1; o < LPR; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+          float sum = 0.0f;
+#pragma unroll
+          for (int u = 0; u < UQ; ++u)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int qd = cg + 2 * LPR * u + h * LPR;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float ex = (4 * qd + e < M) ? expf(out[u][4 * h + e] - vmax) : 0.0f;
+                out[u][4 * h + e] = ex;
+                sum += ex;
+              }
+            }
+          for (int o = 1; o < LPR; o <<= 1) sum += __shfl_xor(sum, o);
+#pragma unroll
+          for (int u = 0; u < UQ; ++u)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) out[u][e] = out[u][e] / sum;
+        }
+        if (store) {
+#pragma unroll
+          for (int u = 0; u < UQ; ++u) store_slot(u, out[u]);
         }
       }
     }

@@ -83,7 +83,9 @@ struct GArgs {
   int lpr_log2;           // accumulate: 2^lpr_log2 lanes per row, 8 columns each
   int vec_out;            // outputs allow 16-byte stores
   int vec16;              // table rows are whole 16-byte units (int8: M % 16 == 0; fp32: M % 4 == 0)
-  int off_shc, off_misc, off_wave, lds_total;  // LDS byte offsets
+  const float* col_bias;  // [M] or null (layer output sigma)
+  int act;                // 0 none, 1 bias, 2 bias + ReLU, 3 bias + row softmax
+  int off_shc, off_misc, off_wave, off_bias, lds_total;  // LDS byte offsets
 };
 
 hipError_t launch_gfused(int elem, int ng, int uq, const GArgs& g, int nw, int cus, hipStream_t stream);
@@ -109,8 +111,14 @@ struct TArgs {
   int vec_lut;            // table rows move in 16-byte units
   int vec_idx;            // index rows move in 4-byte units (C % 4 == 0)
   int vec_out;            // outputs allow 16-byte stores
+  const float* col_bias;  // [M] or null (layer output sigma)
+  int act;                // 0 none, 1 bias, 2 bias + ReLU, 3 bias + row softmax (one column tile only)
   int off_tab, off_idx, off_sh, off_misc, lds_total;  // LDS byte offsets
 };
+
+// Row softmax in place over y [N][M] (layer outputs whose rows span several
+// column tiles of the accumulate).
+hipError_t launch_softmax_rows(float* y, int64_t N, int M, int cus, hipStream_t stream);
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream);
 

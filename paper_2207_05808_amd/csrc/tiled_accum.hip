@@ -289,51 +289,70 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 
       // ---------------- epilogue
       const int col0 = m0 + cg * CPL;
+      const int LPR = 1 << lpr_log2;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const int64_t row = r0 + ib[j];
-        if (row >= N || col0 >= M) continue;
-        if (MODE == 0) {
-          float* yr = a.y + row * M + col0;
-          if (a.vec_out && col0 + 4 <= M) {
-            __builtin_nontemporal_store((tf32x4){__uint_as_float(acc[j][0]), __uint_as_float(acc[j][1]),
-                                                 __uint_as_float(acc[j][2]), __uint_as_float(acc[j][3])},
-                                        reinterpret_cast<tf32x4*>(yr));
+        int out[8];
+        float yv[8];
+#pragma unroll
+        for (int e = 0; e < CPL; ++e) {
+          if (MODE == 0) {
+            out[e] = 0;
+            yv[e] = __uint_as_float(acc[j][e]);
           } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (col0 + e < M) yr[e] = __uint_as_float(acc[j][e]);
-          }
-        } else {
-          int out[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
             out[e] = (MODE == 1) ? ((e & 1) ? (int)acc[j][e >> 1] >> 16 : __builtin_amdgcn_sbfe((int)acc[j][e >> 1], 0, 16))
                                  : (int)acc[j][e];
-          float yv[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) yv[e] = __builtin_fmaf((float)out[e], step, bias);
-          if (a.vec_out && col0 + 8 <= M) {
-            if (a.y) {
-              __builtin_nontemporal_store((tf32x4){yv[0], yv[1], yv[2], yv[3]},
-                                          reinterpret_cast<tf32x4*>(a.y + row * M + col0));
-              __builtin_nontemporal_store((tf32x4){yv[4], yv[5], yv[6], yv[7]},
-                                          reinterpret_cast<tf32x4*>(a.y + row * M + col0 + 4));
-            }
-            if (a.acc) {
-              __builtin_nontemporal_store((tu32x4){(uint32_t)out[0], (uint32_t)out[1], (uint32_t)out[2], (uint32_t)out[3]},
-                                          reinterpret_cast<tu32x4*>(a.acc + row * M + col0));
-              __builtin_nontemporal_store((tu32x4){(uint32_t)out[4], (uint32_t)out[5], (uint32_t)out[6], (uint32_t)out[7]},
-                                          reinterpret_cast<tu32x4*>(a.acc + row * M + col0 + 4));
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (col0 + e < M) {
-                if (a.y) a.y[row * M + col0 + e] = yv[e];
-                if (a.acc) a.acc[row * M + col0 + e] = out[e];
-              }
+            yv[e] = __builtin_fmaf((float)out[e], step, bias);
           }
+        }
+        if (a.act != 0) {
+          // layer output sigma: z = y + bias, then ReLU, or a softmax over the
+          // row's LPR lanes (a row lies in one column tile; every lane takes
+          // part in the reductions)
+          float vmax = -__builtin_inff();
+#pragma unroll
+          for (int e = 0; e < CPL; ++e) {
+            const bool ok = col0 + e < M;
+            float z = yv[e] + ((a.col_bias && ok) ? a.col_bias[col0 + e] : 0.0f);
+            if (a.act == 2) z = (z > 0.0f) ? z : 0.0f;
+            yv[e] = z;
+            if (ok) vmax = __builtin_fmaxf(vmax, z);
+          }
+          if (a.act == 3) {
+            for (int o = 1; o < LPR; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+            float sum = 0.0f;
+#pragma unroll
+            for (int e = 0; e < CPL; ++e) {
+              yv[e] = (col0 + e < M) ? expf(yv[e] - vmax) : 0.0f;
+              sum += yv[e];
+            }
+            for (int o = 1; o < LPR; o <<= 1) sum += __shfl_xor(sum, o);
+#pragma unroll
+            for (int e = 0; e < CPL; ++e) yv[e] = yv[e] / sum;
+          }
+        }
+        if (row >= N || col0 >= M) continue;
+        float* yr = a.y ? a.y + row * M + col0 : nullptr;
+        int32_t* ar = (MODE != 0 && a.acc) ? a.acc + row * M + col0 : nullptr;
+        if (a.vec_out && col0 + CPL <= M) {
+#pragma unroll
+          for (int h = 0; h < CPL / 4; ++h) {
+            if (yr)
+              __builtin_nontemporal_store((tf32x4){yv[4 * h], yv[4 * h + 1], yv[4 * h + 2], yv[4 * h + 3]},
+                                          reinterpret_cast<tf32x4*>(yr + 4 * h));
+            if (ar)
+              __builtin_nontemporal_store((tu32x4){(uint32_t)out[4 * h], (uint32_t)out[4 * h + 1],
+                                                   (uint32_t)out[4 * h + 2], (uint32_t)out[4 * h + 3]},
+                                          reinterpret_cast<tu32x4*>(ar + 4 * h));
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < CPL; ++e)
+            if (col0 + e < M) {
+              if (yr) yr[e] = yv[e];
+              if (ar) ar[e] = out[e];
+            }
         }
       }
     }
@@ -374,6 +393,31 @@ static hipError_t tlaunch(const TArgs& t, int nw, int cus, hipStream_t stream) {
   if (blocks > resident) blocks = resident;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL((tacc_kernel<ELEM, NJ>), dim3((unsigned)blocks), dim3(nw * 64), t.lds_total, stream, t);
+  return hipGetLastError();
+}
+
+// Row softmax in place, one wavefront per row (rows whose outputs span several
+// column tiles of the accumulate): max, exp and sum over the row's M entries.
+__global__ void __launch_bounds__(256) softmax_rows_kernel(float* y, int64_t N, int M) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nw_total = (int64_t)gridDim.x * (blockDim.x >> 6);
+  for (int64_t row = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); row < N; row += nw_total) {
+    float* yr = y + row * M;
+    float vmax = -__builtin_inff();
+    for (int m = lane; m < M; m += 64) vmax = __builtin_fmaxf(vmax, yr[m]);
+    for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+    float sum = 0.0f;
+    for (int m = lane; m < M; m += 64) sum += expf(yr[m] - vmax);
+    for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+    for (int m = lane; m < M; m += 64) yr[m] = expf(yr[m] - vmax) / sum;
+  }
+}
+
+hipError_t launch_softmax_rows(float* y, int64_t N, int M, int cus, hipStream_t stream) {
+  int64_t blocks = (N + 3) / 4;
+  if (blocks > (int64_t)cus * 8) blocks = (int64_t)cus * 8;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y, N, M);
   return hipGetLastError();
 }
 

@@ -87,6 +87,25 @@ def test_matmul_rejects(L):
     assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, NULL, NULL) == 1
 
 
+def test_matmul_act_rejects(L):
+    Ma = L.maddness_matmul_act
+    args = [FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, NULL, 2, FAKE, NULL]
+    for bad_act in (-1, 4):
+        bad = list(args); bad[12] = bad_act
+        assert Ma(*bad) == 1
+    bad = list(args); bad[11] = ctypes.c_void_p(0x1002)   # misaligned bias
+    assert Ma(*bad) == 1
+    bad = list(args); bad[13] = NULL                      # y_out required
+    assert Ma(*bad) == 1
+    bad = list(args); bad[6] = 600                        # too many codebooks
+    assert Ma(*bad) == 3
+    zero = list(args); zero[1] = 0                        # N == 0
+    assert Ma(*zero) == 0
+    F = L.maddness_matmul_act_f32
+    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 7, FAKE, NULL) == 1
+    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 3, NULL, NULL) == 1
+
+
 def test_build_lut_rejects(L):
     B = L.maddness_build_lut
     assert B(FAKE, FAKE, 0, 64, 10, FAKE, FAKE, FAKE, NULL) == 1
