@@ -253,6 +253,15 @@ def main():
         acc_us = region_us(lambda i: acc_call())
         result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
         del idx
+        # the same step with the layer output sigma fused (bias + ReLU, bias + row softmax)
+        cb = torch.from_numpy(np.random.default_rng(1).standard_normal(spec.M).astype(np.float32)).to(dev)
+        for act in ("relu", "softmax"):
+            if spec.quantized:
+                f = lambda i, a=act: mdn.matmul_act(A_bufs[i % 2], split, thr, lut, scale, offset, col_bias=cb,
+                                                    act=a, y_out=y)
+            else:
+                f = lambda i, a=act: mdn.matmul_act_f32(A_bufs[i % 2], split, thr, lut, col_bias=cb, act=a, y_out=y)
+            result["context"][f"step_with_{act}_us"] = round(region_us(f), 2)
 
         # dense fp32 GEMM of the same shape (torch -> hipBLASLt / rocBLAS), TF32 off
         torch.backends.cuda.matmul.allow_tf32 = False
