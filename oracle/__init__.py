@@ -16,6 +16,8 @@ Functions and the passages they follow (the paper: McCarter & Dronen,
 * :func:`build_table` -- §2.2 (T = P B).
 * :func:`quantize_table` -- §1 (8-bit block floating point), reading R6.
 * :func:`sigma` -- §2.2 (layer output: bias, then ReLU or row softmax), R19.
+* :func:`lut_accumulate_avg`, :func:`quantize_table_shared` -- §1 (rounded
+  8-bit summation over codebooks, one shared block exponent), reading R20.
 """
 from __future__ import annotations
 
@@ -72,6 +74,8 @@ class Oracle:
         lib.oracle_exponent_cap.argtypes = [i32]
         lib.oracle_block_exponent.argtypes = [ctypes.c_float, vp]
         lib.oracle_sigma.argtypes = [vp, i64, i32, vp, i32, vp]
+        lib.oracle_quantize_table_shared.argtypes = [vp, i32, i32, vp, vp, vp]
+        lib.oracle_lut_accumulate_avg.argtypes = [vp, i64, i32, vp, vp, vp, i32, vp, vp]
         self.lib = lib
 
     @staticmethod
@@ -151,6 +155,35 @@ class Oracle:
         self._check(rc, "oracle_quantize_table")
         return lut, scale, offset
 
+    def quantize_table_shared(self, T):
+        """The quantizer with one block exponent shared by all codebooks (R20)."""
+        T = np.ascontiguousarray(T, dtype=np.float64)
+        C, k, M = T.shape
+        assert k == K
+        lut = np.zeros((C, K, M), dtype=np.int8)
+        scale = np.zeros(C, dtype=np.float32)
+        offset = np.zeros(C, dtype=np.float32)
+        rc = self.lib.oracle_quantize_table_shared(T.ctypes.data, C, M, lut.ctypes.data,
+                                                   scale.ctypes.data, offset.ctypes.data)
+        self._check(rc, "oracle_quantize_table_shared")
+        return lut, scale, offset
+
+    def lut_accumulate_avg(self, idx, lut, scale, offset):
+        """Rounded 8-bit averaging accumulate (R20); returns (acc int32, y fp32)."""
+        idx = np.ascontiguousarray(idx, dtype=np.uint8)
+        lut = np.ascontiguousarray(lut, dtype=np.int8)
+        scale = np.ascontiguousarray(scale, dtype=np.float32)
+        offset = np.ascontiguousarray(offset, dtype=np.float32)
+        N, C = idx.shape
+        assert lut.shape[:2] == (C, K)
+        M = lut.shape[2]
+        acc = np.zeros((N, M), dtype=np.int32)
+        y = np.zeros((N, M), dtype=np.float32)
+        rc = self.lib.oracle_lut_accumulate_avg(idx.ctypes.data, N, C, lut.ctypes.data, scale.ctypes.data,
+                                                offset.ctypes.data, M, acc.ctypes.data, y.ctypes.data)
+        self._check(rc, "oracle_lut_accumulate_avg")
+        return acc, y
+
     def round_table_f32(self, T):
         T = np.ascontiguousarray(T, dtype=np.float64)
         out = np.zeros(T.shape, dtype=np.float32)
@@ -206,6 +239,9 @@ class Oracle:
 
     def build_quantized_lut(self, P, B):
         return self.quantize_table(self.build_table(P, B))
+
+    def build_shared_lut(self, P, B):
+        return self.quantize_table_shared(self.build_table(P, B))
 
     def build_lut_f32(self, P, B):
         return self.round_table_f32(self.build_table(P, B))

@@ -32,6 +32,10 @@
  *   R10 unquantized mode: y = (((0 + T_0) + T_1) + ...) in fp32, c ascending.
  *   R19 layer output sigma: z = fl32(y + bias_m); ReLU keeps z when z > 0 and
  *       gives +0 otherwise; softmax is taken over the M outputs of a row.
+ *   R20 rounded 8-bit summation: one shared block exponent; biased codes
+ *       u = q + 128, padded with 128 to P = 2^L codebooks, combined by a
+ *       balanced tree in codebook order of rounded averages (a + b + 1) >> 1;
+ *       the sum is estimated as P * (root - 128).
  *
  * Every entry point returns 0 on success and a negative code on a violated
  * precondition (it never aborts): -1 bad size / pointer, -2 a scale that is
@@ -246,12 +250,9 @@ int oracle_exponent_cap(int32_t C)
  * r_c <= 127 * 2^e.  Then e_c is raised to at least max_c e_c - cap, and
  * q = round-half-even((T - o_c) / 2^e_c), which always lies in [-127, 127].
  */
-int oracle_quantize_table(const double* T, int32_t C, int32_t M,
-                          int8_t* lut, float* scale, float* offset)
+static int quantize_table_cap(const double* T, int32_t C, int32_t M, int cap,
+                              int8_t* lut, float* scale, float* offset)
 {
-    if (C <= 0 || M <= 0 || !T || !lut || !scale || !offset) return -1;
-    int cap = oracle_exponent_cap(C);
-    if (cap < 0) return -1;
     const int64_t per = (int64_t)ORACLE_K * M;
     int32_t emax = -126;
     int32_t* ec = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
@@ -289,6 +290,27 @@ int oracle_quantize_table(const double* T, int32_t C, int32_t M,
     }
     free(ec);
     return 0;
+}
+
+int oracle_quantize_table(const double* T, int32_t C, int32_t M,
+                          int8_t* lut, float* scale, float* offset)
+{
+    if (C <= 0 || M <= 0 || !T || !lut || !scale || !offset) return -1;
+    int cap = oracle_exponent_cap(C);
+    if (cap < 0) return -1;
+    return quantize_table_cap(T, C, M, cap, lut, scale, offset);
+}
+
+/*
+ * The same quantizer with one block exponent shared by every codebook (the
+ * floor max_c e_c - cap taken with cap = 0), as the rounded 8-bit averaging
+ * accumulate below requires (reading R20).
+ */
+int oracle_quantize_table_shared(const double* T, int32_t C, int32_t M,
+                                 int8_t* lut, float* scale, float* offset)
+{
+    if (C <= 0 || M <= 0 || !T || !lut || !scale || !offset) return -1;
+    return quantize_table_cap(T, C, M, 0, lut, scale, offset);
 }
 
 /* Unquantized table: each T entry rounded to fp32 (round to nearest even). */
@@ -335,6 +357,57 @@ int oracle_sigma(const float* y, int64_t N, int32_t M, const float* bias,
                 sum += o[m];
             }
             for (int32_t m = 0; m < M; ++m) o[m] = o[m] / sum;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Rounded 8-bit summation over codebooks (§1 names it, for MADDNESS's 8-bit
+ * tables, without defining it; reading R20).  Every scale must be the same
+ * power of two 2^e (else -2).  Per output, the biased codes u_c = q_c + 128
+ * (in [1, 255]) of codebooks 0..C-1, followed by P - C copies of 128 (P the
+ * smallest power of two >= C), are reduced level by level: node i of the
+ * next level is (u_2i + u_2i+1 + 1) >> 1, a rounded byte average.  The root
+ * r estimates the mean code + 128, so acc = P * (r - 128) estimates
+ * sum_c q_c, and y = fl32(acc * 2^e + bias32) exactly as in R9.
+ */
+int oracle_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C,
+                              const int8_t* lut, const float* scale,
+                              const float* offset, int32_t M,
+                              int32_t* acc, float* y)
+{
+    if (N < 0 || C <= 0 || M <= 0 || C > 4096) return -1;
+    if (N > 0 && (!idx || !lut || !scale || !offset || !acc || !y)) return -1;
+    for (int32_t c = 1; c < C; ++c)
+        if (scale[c] != scale[0]) return -2;
+    int32_t sh_unused[4096];
+    int32_t emin = 0;
+    float bias32 = 0.0f;
+    int rc = oracle_dequant_params(scale, offset, C, sh_unused, &emin, &bias32);
+    if (rc != 0) return rc;
+    const float unit = ldexpf(1.0f, emin);   /* 2^e */
+    int32_t P = 1;
+    while (P < C) P *= 2;
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        int32_t u[4096];
+        for (int32_t m = 0; m < M; ++m) {
+            for (int32_t c = 0; c < P; ++c) {
+                if (c < C) {
+                    int k = idx[n * C + c];
+                    u[c] = (int32_t)lut[((int64_t)c * ORACLE_K + k) * M + m] + 128;
+                } else {
+                    u[c] = 128;
+                }
+            }
+            for (int32_t width = P; width > 1; width /= 2)
+                for (int32_t i = 0; i < width / 2; ++i)
+                    u[i] = (u[2 * i] + u[2 * i + 1] + 1) >> 1;
+            const int32_t a = P * (u[0] - 128);
+            acc[n * M + m] = a;
+            y[n * M + m] = fmaf((float)a, unit, bias32);
         }
     }
     return 0;

@@ -471,10 +471,104 @@ def check_sigma_softmax(orc, seed=12):
     assert np.allclose(pb, [[1 / (1 + w), w / (1 + w)]] * 2, rtol=1e-14, atol=0)
 
 
+def _shared_codes(C, M, seed):
+    rng = np.random.default_rng(seed)
+    lut = rng.integers(-127, 128, size=(C, K, M)).astype(np.int8)
+    scale = np.full(C, np.float32(2.0 ** -7), np.float32)
+    offset = (rng.standard_normal(C) * 0.25).astype(np.float32)
+    return lut, scale, offset
+
+
+def check_avg_closed_forms(orc, seed=13):
+    """Rounded 8-bit summation (§1, reading R20) in the cases the definition
+    reduces to by hand: one codebook is exact; two codebooks are one rounded
+    average, (u0 + u1 + 1) >> 1 with u = q + 128, times 2; three codebooks are
+    padded with a 128 leaf; equal codes over a power-of-two count are exact;
+    y uses the exact path's dequantization of acc."""
+    rng = np.random.default_rng(seed)
+    N, M = 50, 7
+    for C in (1, 2, 3, 4, 8):
+        lut, scale, offset = _shared_codes(C, M, seed + C)
+        idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+        acc, y = orc.lut_accumulate_avg(idx, lut, scale, offset)
+        q = np.stack([lut[c][idx[:, c]] for c in range(C)], axis=1).astype(np.int64)   # [N, C, M]
+        u = q + 128
+        if C == 1:
+            ref = q[:, 0]
+        elif C == 2:
+            ref = 2 * (((u[:, 0] + u[:, 1] + 1) >> 1) - 128)
+        elif C == 3:
+            left = (u[:, 0] + u[:, 1] + 1) >> 1
+            right = (u[:, 2] + 128 + 1) >> 1
+            ref = 4 * (((left + right + 1) >> 1) - 128)
+        else:
+            ref = None
+        if ref is not None:
+            assert np.array_equal(acc, ref)
+        sh, emin, bias32 = orc.dequant_params(scale, offset)
+        assert np.array_equal(y, (acc.astype(np.float32) * np.float32(2.0 ** emin) + bias32).astype(np.float32)) or \
+            np.array_equal(y, np.float32(2.0 ** emin) * acc.astype(np.float32) + bias32)
+    for C in (4, 16, 64):
+        lut = np.repeat(np.arange(-8, 8, dtype=np.int8)[None, :, None], C, axis=0).repeat(3, axis=2)
+        scale = np.full(C, np.float32(0.5), np.float32)
+        offset = np.zeros(C, np.float32)
+        idx = np.full((5, C), 11, np.uint8)                  # every codebook picks code 3
+        acc, _ = orc.lut_accumulate_avg(idx, lut, scale, offset)
+        assert np.all(acc == 3 * C)
+
+
+def check_avg_bounds(orc, seed=14):
+    """Each rounded average adds at most 1/2 to its exact value and its error
+    halves per level above, so 0 <= acc - sum_c q_c <= P L / 2 (P = 2^L >= C);
+    raising one code never lowers acc; mixed scales are rejected."""
+    rng = np.random.default_rng(seed)
+    for C in (5, 32, 100):
+        lut, scale, offset = _shared_codes(C, 9, seed + C)
+        idx = rng.integers(0, K, size=(200, C)).astype(np.uint8)
+        acc, _ = orc.lut_accumulate_avg(idx, lut, scale, offset)
+        exact, _ = orc.lut_accumulate(idx, lut, scale, offset)
+        P = 1 << int(math.ceil(math.log2(C)))
+        L = int(math.log2(P))
+        err = acc.astype(np.int64) - exact.astype(np.int64)
+        assert err.min() >= 0 and err.max() <= P * L // 2
+        lut2 = lut.copy()
+        bump = lut2 < 127
+        lut2[bump] += 1
+        acc2, _ = orc.lut_accumulate_avg(idx, lut2, scale, offset)
+        assert np.all(acc2 >= acc)
+    lut, scale, offset = _shared_codes(4, 3, 1)
+    scale[2] *= 2
+    try:
+        orc.lut_accumulate_avg(np.zeros((2, 4), np.uint8), lut, scale, offset)
+    except Exception:
+        pass
+    else:
+        raise AssertionError("mixed scales accepted")
+
+
+def check_shared_quantizer(orc, seed=15):
+    """The shared-exponent quantizer (R20): one scale for all codebooks, the
+    largest of the per-codebook minimal exponents; codes within [-127, 127]
+    and within half a step of T - offset; identical to the per-codebook
+    quantizer when those exponents already agree (one codebook)."""
+    rng = np.random.default_rng(seed)
+    T = rng.standard_normal((6, K, 11)) * np.array([0.1, 1, 3, 0.02, 7, 0.5])[:, None, None]
+    lut, scale, offset = orc.quantize_table_shared(T)
+    assert np.all(scale == scale[0])
+    lut_r, scale_r, _ = orc.quantize_table(T)
+    assert scale[0] == scale_r.max()
+    step = float(scale[0])
+    resid = T - offset[:, None, None].astype(np.float64) - lut.astype(np.float64) * step
+    assert np.abs(resid).max() <= step / 2 * (1 + 1e-12)
+    T1 = T[4:5]
+    assert all(np.array_equal(a, b) for a, b in zip(orc.quantize_table_shared(T1), orc.quantize_table(T1)))
+
+
 ALL_CHECKS = [
     check_encode_brute_force, check_encode_search_tree, check_encode_nan, check_encode_permutation,
     check_encode_golden, check_one_hot_identity, check_decoder_table, check_output_rounding,
     check_scale_linearity, check_f32_order, check_table_build, check_quantizer,
     check_f32_reconstruction, check_quantized_reconstruction, check_rejects_bad_inputs,
-    check_sigma_bias_relu, check_sigma_softmax,
+    check_sigma_bias_relu, check_sigma_softmax, check_avg_closed_forms, check_avg_bounds,
+    check_shared_quantizer,
 ]

@@ -41,6 +41,12 @@ MUTANTS = [
     ("softmax max not initialised from the row", "double mx = o[0];", "double mx = 0.0;"),
     ("softmax normalised by the first term", "for (int32_t m = 0; m < M; ++m) o[m] = o[m] / sum;",
      "for (int32_t m = M - 1; m >= 0; --m) o[m] = o[m] / o[0];"),
+    ("average rounds down", "u[i] = (u[2 * i] + u[2 * i + 1] + 1) >> 1;", "u[i] = (u[2 * i] + u[2 * i + 1]) >> 1;"),
+    ("padding leaves are zero", "                    u[c] = 128;\n", "                    u[c] = 0;\n"),
+    ("estimate scaled by C", "const int32_t a = P * (u[0] - 128);", "const int32_t a = C * (u[0] - 128);"),
+    ("code bias not removed", "const int32_t a = P * (u[0] - 128);", "const int32_t a = P * u[0];"),
+    ("shared quantizer keeps per-codebook exponents", "return quantize_table_cap(T, C, M, 0, lut, scale, offset);",
+     "return quantize_table_cap(T, C, M, oracle_exponent_cap(C), lut, scale, offset);"),
 ]
 
 
