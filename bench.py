@@ -252,6 +252,13 @@ def main():
         enc_us = region_us(lambda i: split_calls[i % 2]())
         acc_us = region_us(lambda i: acc_call())
         result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
+        if spec.quantized:
+            # the rounded 8-bit averaging accumulate (approximate) over a
+            # shared-exponent table of the same weights, on the same indices
+            slut, sscale, soffset = mdn.build_lut_shared(torch.from_numpy(p.P).to(dev), Bd)
+            avg_us = region_us(lambda i: mdn.lut_accumulate_avg(idx, slut, sscale, soffset, y_out=y))
+            result["context"]["accumulate_avg8_us"] = round(avg_us, 2)
+            del slut
         del idx
         # the same step with the layer output sigma fused (bias + ReLU, bias + row softmax)
         cb = torch.from_numpy(np.random.default_rng(1).standard_normal(spec.M).astype(np.float32)).to(dev)

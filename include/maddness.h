@@ -120,6 +120,25 @@ int maddness_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C,
                             int32_t* acc_out, float* y_out, void* stream);
 
 /*
+ * Rounded 8-bit summation over codebooks (§1 names it as the summation of
+ * MADDNESS's 8-bit tables; this library's reading, R20): an approximate
+ * alternative to the exact sum of maddness_lut_accumulate.  Every scale must
+ * be the same power of two 2^e (a precondition, as for the other device
+ * contents; maddness_build_lut_shared makes such tables).  Per output, the
+ * biased codes u_c = q_c + 128 of codebooks 0..C-1, followed by P - C copies
+ * of 128 (P = the smallest power of two >= C), are reduced by a balanced
+ * tree in codebook order whose nodes are rounded byte averages
+ * (a + b + 1) >> 1; with r the root,
+ *   acc = P * (r - 128),   y = fl32(acc * 2^e + bias32)   (bias32 as above).
+ * The estimate satisfies 0 <= acc - sum_c q_c <= P log2(P) / 2.
+ * Same arguments and errors as maddness_lut_accumulate.
+ */
+int maddness_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C,
+                                const int8_t* lut, const float* scale,
+                                const float* offset, int32_t M,
+                                int32_t* acc_out, float* y_out, void* stream);
+
+/*
  * Lookup-accumulate over an unquantized fp32 table [C][16][M]:
  *   y[n][m] = (((0 + T[0][idx0][m]) + T[1][idx1][m]) + ...) in fp32, codebooks
  * in ascending order (a fixed order, so the result is deterministic).
@@ -199,6 +218,12 @@ int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda,
 int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D,
                        int32_t M, int8_t* lut_out, float* scale_out,
                        float* offset_out, void* stream);
+
+/* The same quantization with one block exponent shared by every codebook
+   (cap = 0: e_c = max_c e_c), as maddness_lut_accumulate_avg requires. */
+int maddness_build_lut_shared(const float* P, const float* B, int32_t C,
+                              int32_t D, int32_t M, int8_t* lut_out,
+                              float* scale_out, float* offset_out, void* stream);
 
 /* Same table T = P B, each entry rounded to fp32 (unquantized mode). */
 int maddness_build_lut_f32(const float* P, const float* B, int32_t C,

@@ -8,7 +8,7 @@ The entry points load lazily, so ``paper_2207_05808_amd.workloads`` (the
 seeded input generator) imports without torch or the HIP library.
 """
 _BINDING = ("encode", "lut_accumulate", "lut_accumulate_f32", "matmul", "matmul_f32", "matmul_act",
-            "matmul_act_f32",
+            "matmul_act_f32", "lut_accumulate_avg", "build_lut_shared",
             "build_lut", "build_lut_f32", "version", "prepare_matmul", "prepare_matmul_f32",
             "PreparedCall")
 

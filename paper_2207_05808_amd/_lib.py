@@ -49,12 +49,14 @@ def lib() -> ctypes.CDLL:
         L.maddness_matmul_f32.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, i32, vp, vp, vp]
         L.maddness_matmul_act.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, vp, vp, i32, vp, i32, vp, vp]
         L.maddness_matmul_act_f32.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, i32, vp, i32, vp, vp]
+        L.maddness_lut_accumulate_avg.argtypes = [vp, i64, i32, vp, vp, vp, i32, vp, vp, vp]
+        L.maddness_build_lut_shared.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, vp]
         L.maddness_build_lut.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, vp]
         L.maddness_build_lut_f32.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         for f in ("maddness_version", "maddness_encode", "maddness_lut_accumulate",
                   "maddness_lut_accumulate_f32", "maddness_matmul", "maddness_matmul_f32",
                   "maddness_matmul_act", "maddness_matmul_act_f32", "maddness_build_lut",
-                  "maddness_build_lut_f32"):
+                  "maddness_build_lut_f32", "maddness_lut_accumulate_avg", "maddness_build_lut_shared"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib

@@ -139,6 +139,31 @@ def lut_accumulate(idx, lut, scale, offset, acc_out=None, y_out=None, want_acc=F
     return acc_out, y_out
 
 
+def lut_accumulate_avg(idx, lut, scale, offset, acc_out=None, y_out=None, want_acc=False, want_y=True,
+                       stream=None, validate=False):
+    """Rounded 8-bit summation over codebooks (approximate; one shared scale);
+    returns (acc or None, y or None)."""
+    _need(idx, "idx", torch.uint8, 2)
+    _dense(idx, "idx")
+    C, M = _lut_i8(lut, scale, offset)
+    N = idx.shape[0]
+    if idx.shape[1] != C:
+        raise ValueError("idx must be [N, C]")
+    if validate:
+        _validate_idx(idx)
+        _validate_scales(scale)
+        if not bool((scale == scale[0]).all()):
+            raise ValueError("the averaging accumulate needs one scale shared by every codebook")
+    if acc_out is None and want_acc:
+        acc_out = torch.empty((N, M), dtype=torch.int32, device=idx.device)
+    if y_out is None and want_y:
+        y_out = torch.empty((N, M), dtype=torch.float32, device=idx.device)
+    st = _lib.lib().maddness_lut_accumulate_avg(_ptr(idx), N, C, _ptr(lut), _ptr(scale), _ptr(offset), M,
+                                                _ptr(acc_out), _ptr(y_out), _stream(stream))
+    _lib.check("maddness_lut_accumulate_avg", st)
+    return acc_out, y_out
+
+
 def lut_accumulate_f32(idx, lut, y_out=None, stream=None, validate=False):
     """Gather-accumulate over an fp32 table [C][16][M]; returns y [N][M]."""
     _need(idx, "idx", torch.uint8, 2)
@@ -290,6 +315,25 @@ def build_lut(P, B, stream=None):
     st = _lib.lib().maddness_build_lut(_ptr(P), _ptr(B), C, D, M, _ptr(lut), _ptr(scale),
                                        _ptr(offset), _stream(stream))
     _lib.check("maddness_build_lut", st)
+    return lut, scale, offset
+
+
+def build_lut_shared(P, B, stream=None):
+    """build_lut with one block exponent shared by every codebook (for lut_accumulate_avg)."""
+    _need(P, "P", torch.float32, 3)
+    _need(B, "B", torch.float32, 2)
+    _dense(P, "P")
+    _dense(B, "B")
+    C, k, D = P.shape
+    if k != K or B.shape[0] != D:
+        raise ValueError("P must be [C,16,D] and B [D,M]")
+    M = B.shape[1]
+    lut = torch.empty((C, K, M), dtype=torch.int8, device=P.device)
+    scale = torch.empty((C,), dtype=torch.float32, device=P.device)
+    offset = torch.empty((C,), dtype=torch.float32, device=P.device)
+    st = _lib.lib().maddness_build_lut_shared(_ptr(P), _ptr(B), C, D, M, _ptr(lut), _ptr(scale),
+                                              _ptr(offset), _stream(stream))
+    _lib.check("maddness_build_lut_shared", st)
     return lut, scale, offset
 
 

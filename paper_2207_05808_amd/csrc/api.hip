@@ -307,6 +307,37 @@ int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, stream));
 }
 
+// Rounded 8-bit averaging accumulate (tiled_accum.hip): 8 wavefronts, one row
+// pass per wavefront, 16 columns per lane, tiles of 8 codebooks.
+bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
+  if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;   // 32-bit buffer offsets
+  const int nw = 8, nj = 1;
+  const int lpr = s.M > 128 ? 16 : 8;
+  TArgs a{};
+  a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;
+  a.N = s.N; a.C = s.C; a.M = s.M;
+  a.lpr_log2 = ilog2(lpr);
+  a.Mt = 16 * lpr;
+  a.RB = nw * (64 / lpr) * nj;
+  a.CT = 8;
+  a.ntm = (s.M + a.Mt - 1) / a.Mt;
+  a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
+  a.vec_lut = aligned(s.lut, 16) && (s.M % 16 == 0);
+  a.vec_idx = (s.C % 4 == 0) && aligned(s.idx_in, 4);
+  a.vec_out = (s.M % 4 == 0) && (s.y == nullptr || aligned(s.y, 16)) && (s.acc == nullptr || aligned(s.acc, 16));
+  int off = 0;
+  auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
+  a.off_tab = take(a.CT * kK * a.Mt);   // 0: the kernel relies on it
+  a.off_idx = take(a.RB * a.CT * 4);
+  a.off_sh = take(s.C * 4);
+  a.off_misc = take(16);
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  *t = a;
+  *nw_out = nw;
+  return true;
+}
+
 // Accumulate-only work: the column-tiled kernel, else the general path.
 int accumulate(const Shape& s, hipStream_t stream) {
   TArgs t;
@@ -416,6 +447,24 @@ int maddness_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C, const int8
   s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.scale = scale; s.offset = offset; s.M = M;
   s.acc = acc_out; s.y = y_out;
   return accumulate(s, static_cast<hipStream_t>(stream));
+}
+
+int maddness_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C, const int8_t* lut,
+                                const float* scale, const float* offset, int32_t M, int32_t* acc_out,
+                                float* y_out, void* stream) {
+  int rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!idx || !scale || !offset || (!acc_out && !y_out)) return MADDNESS_EINVAL;
+  if (!aligned(scale, 4) || !aligned(offset, 4) || (acc_out && !aligned(acc_out, 4)) ||
+      (y_out && !aligned(y_out, 4)))
+    return MADDNESS_EINVAL;
+  Shape s = shape(kAccum, kI8);
+  s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.scale = scale; s.offset = offset; s.M = M;
+  s.acc = acc_out; s.y = y_out;
+  TArgs t;
+  int nw;
+  if (!plan_tavg(s, &t, &nw)) return MADDNESS_EUNSUPPORTED;
+  return status_from(launch_tavg(1, t, nw, device_cus(), static_cast<hipStream_t>(stream)));
 }
 
 int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C, const float* lut, int32_t M,
@@ -531,6 +580,17 @@ int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D, int
   int cap = 0;
   while (127.0 * C * (double)(1ll << (cap + 1)) < 16777216.0) ++cap;
   return status_from(launch_build_lut(P, B, C, D, M, lut_out, scale_out, offset_out, cap,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int maddness_build_lut_shared(const float* P, const float* B, int32_t C, int32_t D, int32_t M, int8_t* lut_out,
+                              float* scale_out, float* offset_out, void* stream) {
+  if (C <= 0 || D <= 0 || M <= 0 || !P || !B || !lut_out || !scale_out || !offset_out)
+    return MADDNESS_EINVAL;
+  if (!aligned(P, 4) || !aligned(B, 4) || !aligned(scale_out, 4) || !aligned(offset_out, 4))
+    return MADDNESS_EINVAL;
+  if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
+  return status_from(launch_build_lut(P, B, C, D, M, lut_out, scale_out, offset_out, 0,
                                       static_cast<hipStream_t>(stream)));
 }
 

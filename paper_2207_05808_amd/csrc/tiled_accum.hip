@@ -290,6 +290,9 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
       // ---------------- epilogue
       const int col0 = m0 + cg * CPL;
       const int LPR = 1 << lpr_log2;
+      float cb[CPL];   // this lane's column biases, loaded once (stores to y may alias them)
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) cb[e] = (a.act != 0 && a.col_bias && col0 + e < M) ? a.col_bias[col0 + e] : 0.0f;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const int64_t row = r0 + ib[j];
@@ -314,7 +317,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 #pragma unroll
           for (int e = 0; e < CPL; ++e) {
             const bool ok = col0 + e < M;
-            float z = yv[e] + ((a.col_bias && ok) ? a.col_bias[col0 + e] : 0.0f);
+            float z = yv[e] + cb[e];
             if (a.act == 2) z = (z > 0.0f) ? z : 0.0f;
             yv[e] = z;
             if (ok) vmax = __builtin_fmaxf(vmax, z);
@@ -362,6 +365,245 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
   else run(std::integral_constant<int, 2>{});
 }
 
+// Rounded 8-bit summation over codebooks (§1 names it; reading R20): the
+// codes of a row, biased to bytes u = q + 128 and padded with 128 to P = 2^L
+// codebooks, are reduced by a balanced tree of rounded byte averages in
+// codebook order, four columns per v_lerp_u8; the root r gives
+// acc = P (r - 128).  Layout as in tacc_kernel with one byte per entry: 16
+// columns per lane, LPR lanes per output row, tiles of 8 codebooks.  Each
+// tile is one level-3 subtree (or the level-L root when P < 8); tiles merge
+// through a binary-counter stack of higher tree levels held in registers;
+// pad tiles (all 128) finish the tree when C is not a power of two.
+// stack levels above a tile: LV = 4 covers P / 8 <= 8 tiles (C <= 64), 5
+// covers C <= 128, 7 covers C <= 512
+
+__device__ __forceinline__ uint32_t avg4(uint32_t a, uint32_t b) { return __builtin_amdgcn_lerp(a, b, 0x01010101u); }
+
+template <int NJ, int LV>
+__global__ void __launch_bounds__(512, 4) tavg_kernel(const TArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  tlds_t* smem = (tlds_t*)smem_raw;
+
+  const int tid = threadIdx.x;
+  const int nt = blockDim.x;
+  const int lane = tid & 63;
+  const int wave = tuni(tid >> 6);
+  const int nw = nt >> 6;
+  const int C = a.C, M = a.M, Mt = a.Mt, RB = a.RB;
+  constexpr int CT = 8;
+  const int64_t N = a.N;
+  const int lpr_log2 = a.lpr_log2;
+  const int RS = 64 >> lpr_log2;
+  const int r4 = lane >> lpr_log2;
+  const int cg = lane & ((1 << lpr_log2) - 1);
+  const int rby_log2 = 31 - __builtin_clz(Mt);   // one byte per entry: row bytes = Mt
+  tlds_t* s_tab = smem;   // the table tile starts the LDS block (off_tab == 0)
+  tlds_t* s_idx = smem + a.off_idx;
+  tlds_i32* s_misc = reinterpret_cast<tlds_i32*>(smem + a.off_misc);
+
+  // block exponent (one shared by every codebook) and bias32
+  if (tid == 0) s_misc[1] = INT_MAX;
+  __syncthreads();
+  const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
+  for (int c = tid; c < C; c += nt) atomicMin((int*)&s_misc[1], (int)((sb[c] >> 23) & 0xffu) - 127);
+  if (wave == 0) {
+    double sum = 0.0;
+    for (int c0 = 0; c0 < C; c0 += 64) {
+      const float ov = a.offset[min(c0 + lane, C - 1)];
+      const int n = min(64, C - c0);
+      for (int j = 0; j < n; ++j) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), j));
+    }
+    if (lane == 0) s_misc[0] = __float_as_int((float)sum);
+  }
+  __syncthreads();
+  const float step = __builtin_ldexpf(1.0f, tuni(s_misc[1]));
+  const float bias = __int_as_float(tuni(s_misc[0]));
+  int L = 0;
+  while ((1 << L) < C) ++L;
+  const int P = 1 << L;
+  const int ntile = (C + CT - 1) / CT;
+  const int ntile_all = max(1, P / CT);
+
+  const int upr = Mt >> 4;              // 16-byte units per table row of the tile
+  const int upr_log2 = __builtin_ctz(upr);
+  const int units = CT * 16 * upr;
+  const int iwords = RB * 2;            // two index words (8 codebooks) per row
+  const bool vec = a.vec_lut && a.vec_idx;
+  const __amdgpu_buffer_rsrc_t trs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M), kBufDword3);
+  tu32x4 tv[kTU];
+  uint32_t iv[kIU];
+  auto load_tile = [&](int c0, int64_t r0, int m0) {
+#pragma unroll
+    for (int j = 0; j < kTU; ++j) {
+      const int u = tid + j * nt;
+      const int row = u >> upr_log2, part = u & (upr - 1);
+      const int c = c0 + (row >> 4), m = m0 + part * 16;
+      const bool ok = u < units && c < C && m < M;
+      tv[j] = __builtin_amdgcn_raw_buffer_load_b128(trs, ok ? (c * 16 + (row & 15)) * M + m : kOob, 0, 0);
+    }
+    const int64_t rows = min((int64_t)RB, N - r0);
+    const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(a.idx + r0 * C), 0, (int)min(rows * C, (int64_t)INT_MAX), kBufDword3);
+#pragma unroll
+    for (int j = 0; j < kIU; ++j) {
+      const int d = tid + j * nt;
+      const int i = d >> 1, q = d & 1;
+      const bool ok = d < iwords && c0 + 4 * q < C;
+      iv[j] = __builtin_amdgcn_raw_buffer_load_b32(irs, ok ? i * C + c0 + 4 * q : kOob, 0, 0);
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int j = 0; j < kTU; ++j) {
+      const int u = tid + j * nt;
+      if (u < units) {
+        const int row = u >> upr_log2, part = u & (upr - 1);
+        const tu32x4 b = tv[j] ^ (tu32x4){0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};  // q + 128
+        *reinterpret_cast<tlds_u32x4*>(s_tab + (row << rby_log2) + part * 16) = b;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kIU; ++j) {
+      const int d = tid + j * nt;
+      if (d < iwords) {
+        const uint32_t cb = (uint32_t)(4 * (d & 1)) * 16u;
+        tu32x4 o;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) o[b] = (cb + 16u * b + ((iv[j] >> (8 * b)) & 15u)) << rby_log2;
+        *reinterpret_cast<tlds_u32x4*>(s_idx + 16 * d) = o;
+      }
+    }
+  };
+  auto stage_direct = [&](int c0, int64_t r0, int m0) {
+    const uint8_t* q8 = reinterpret_cast<const uint8_t*>(a.lut);
+    for (int e = tid; e < CT * 16 * Mt; e += nt) {
+      const int row = e >> rby_log2, col = e & (Mt - 1);
+      const int c = c0 + (row >> 4), m = m0 + col;
+      const bool ok = c < C && m < M;
+      s_tab[(row << rby_log2) + col] = (char)(ok ? (q8[((int64_t)c * 16 + (row & 15)) * M + m] ^ 0x80u) : 0x80u);
+    }
+    for (int e = tid; e < RB * CT; e += nt) {
+      const int i = e >> 3, cc = e & 7;
+      const bool ok = r0 + i < N && c0 + cc < C;
+      const uint32_t k = ok ? (uint32_t)(a.idx[(r0 + i) * C + c0 + cc] & 15u) : 0u;
+      *reinterpret_cast<tlds_u32*>(s_idx + 4 * e) = ((uint32_t)cc * 16u + k) << rby_log2;
+    }
+  };
+
+  const tlds_t* s_tab_lane = s_tab + cg * 16;
+  int ib[NJ];
+  const tlds_t* s_idx_row[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    ib[j] = (j * nw + wave) * RS + r4;
+    s_idx_row[j] = s_idx + ib[j] * CT * 4;
+  }
+
+  for (int64_t w = blockIdx.x; w < a.nwork; w += gridDim.x) {
+    const int mt = (int)(w % a.ntm);
+    const int64_t r0 = (w / a.ntm) * RB;
+    const int m0 = mt * Mt;
+    tu32x4 stk[NJ][LV];   // stack[l]: a pending node at tree level 3 + l
+    tu32x4 root[NJ];
+    // merge a level-3 node x of tile t into the stack (carry chain of t's low bits)
+    auto merge = [&](int j, tu32x4 x, int t) {
+      bool carry = true;
+#pragma unroll
+      for (int l = 0; l < LV; ++l) {
+        if (carry) {
+          if ((t >> l) & 1) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = avg4(stk[j][l][e], x[e]);
+          } else {
+            stk[j][l] = x;
+            carry = false;
+          }
+        }
+      }
+    };
+
+    if (vec) load_tile(0, r0, m0);
+    for (int t = 0; t < ntile; ++t) {
+      __syncthreads();
+      if (vec) store_tile(); else stage_direct(t * CT, r0, m0);
+      __syncthreads();
+      if (vec && t + 1 < ntile) load_tile((t + 1) * CT, r0, m0);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const tu32x4 k0 = *reinterpret_cast<const tlds_u32x4*>(s_idx_row[j]);
+        const tu32x4 k1 = *reinterpret_cast<const tlds_u32x4*>(s_idx_row[j] + 16);
+        tu32x4 v[8];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          v[b] = *reinterpret_cast<const tlds_u32x4*>(s_tab_lane + k0[b]);
+          v[4 + b] = *reinterpret_cast<const tlds_u32x4*>(s_tab_lane + k1[b]);
+        }
+        tu32x4 a0, a1, a2, a3, b0, b1, x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          a0[e] = avg4(v[0][e], v[1][e]);
+          a1[e] = avg4(v[2][e], v[3][e]);
+          a2[e] = avg4(v[4][e], v[5][e]);
+          a3[e] = avg4(v[6][e], v[7][e]);
+          b0[e] = avg4(a0[e], a1[e]);
+          b1[e] = avg4(a2[e], a3[e]);
+          x[e] = avg4(b0[e], b1[e]);
+        }
+        if (L >= 3) merge(j, x, t);
+        else root[j] = (L == 0) ? v[0] : (L == 1) ? a0 : b0;
+      }
+    }
+    if (L >= 3) {
+      const tu32x4 pad = {0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
+      for (int t = ntile; t < ntile_all; ++t)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) merge(j, pad, t);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+        for (int l = 0; l < LV; ++l)
+          if (l == L - 3) root[j] = stk[j][l];
+      }
+    }
+
+    // epilogue: acc = P (r - 128) for the lane's 16 columns
+    const int col0 = m0 + cg * 16;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int64_t row = r0 + ib[j];
+      if (row >= N || col0 >= M) continue;
+      int out[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) out[e] = P * ((int)((root[j][e >> 2] >> (8 * (e & 3))) & 0xffu) - 128);
+      float* yr = a.y ? a.y + row * M + col0 : nullptr;
+      int32_t* ar = a.acc ? a.acc + row * M + col0 : nullptr;
+      if (a.vec_out && col0 + 16 <= M) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          if (yr)
+            __builtin_nontemporal_store((tf32x4){__builtin_fmaf((float)out[4 * h], step, bias),
+                                                 __builtin_fmaf((float)out[4 * h + 1], step, bias),
+                                                 __builtin_fmaf((float)out[4 * h + 2], step, bias),
+                                                 __builtin_fmaf((float)out[4 * h + 3], step, bias)},
+                                        reinterpret_cast<tf32x4*>(yr + 4 * h));
+          if (ar)
+            __builtin_nontemporal_store((tu32x4){(uint32_t)out[4 * h], (uint32_t)out[4 * h + 1],
+                                                 (uint32_t)out[4 * h + 2], (uint32_t)out[4 * h + 3]},
+                                        reinterpret_cast<tu32x4*>(ar + 4 * h));
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (col0 + e < M) {
+            if (yr) yr[e] = __builtin_fmaf((float)out[e], step, bias);
+            if (ar) ar[e] = out[e];
+          }
+      }
+    }
+  }
+}
+
 // Per (kernel, block, LDS size): the LDS attribute is raised once and the
 // number of resident workgroups per CU is queried once.
 static int t_prepare(const void* fn, int block, int lds, hipError_t* err) {
@@ -397,8 +639,46 @@ static hipError_t tlaunch(const TArgs& t, int nw, int cus, hipStream_t stream) {
 }
 
 // Row softmax in place, one wavefront per row (rows whose outputs span several
-// column tiles of the accumulate): max, exp and sum over the row's M entries.
+// column tiles of the accumulate): the row is read once into registers (up to
+// 64 values per lane, 4-column chunks when M % 4 == 0), max and sum are
+// reduced across the wavefront, and the row is written once.
+constexpr int kSoftChunks = 16;   // 4-column chunks per lane: M <= 4096
+
 __global__ void __launch_bounds__(256) softmax_rows_kernel(float* y, int64_t N, int M) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nw_total = (int64_t)gridDim.x * (blockDim.x >> 6);
+  const int nq = M >> 2;   // whole 4-column chunks (M % 4 == 0 and M <= 4096 on this path)
+  for (int64_t row = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); row < N; row += nw_total) {
+    tf32x4* yr = reinterpret_cast<tf32x4*>(y + row * M);
+    tf32x4 v[kSoftChunks];
+    float vmax = -__builtin_inff();
+#pragma unroll
+    for (int i = 0; i < kSoftChunks; ++i) {
+      const int q = lane + 64 * i;
+      v[i] = q < nq ? __builtin_nontemporal_load(yr + q) : (tf32x4){-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
+      vmax = __builtin_fmaxf(vmax, __builtin_fmaxf(__builtin_fmaxf(v[i].x, v[i].y), __builtin_fmaxf(v[i].z, v[i].w)));
+    }
+    for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kSoftChunks; ++i) {
+      if (lane + 64 * i < nq) {
+        v[i].x = expf(v[i].x - vmax); v[i].y = expf(v[i].y - vmax);
+        v[i].z = expf(v[i].z - vmax); v[i].w = expf(v[i].w - vmax);
+        sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+      }
+    }
+    for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+#pragma unroll
+    for (int i = 0; i < kSoftChunks; ++i) {
+      const int q = lane + 64 * i;
+      if (q < nq) __builtin_nontemporal_store((tf32x4){v[i].x / sum, v[i].y / sum, v[i].z / sum, v[i].w / sum}, yr + q);
+    }
+  }
+}
+
+// General rows (any M): three strided passes over the row.
+__global__ void __launch_bounds__(256) softmax_rows_any_kernel(float* y, int64_t N, int M) {
   const int lane = threadIdx.x & 63;
   const int64_t nw_total = (int64_t)gridDim.x * (blockDim.x >> 6);
   for (int64_t row = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); row < N; row += nw_total) {
@@ -415,10 +695,35 @@ __global__ void __launch_bounds__(256) softmax_rows_kernel(float* y, int64_t N, 
 
 hipError_t launch_softmax_rows(float* y, int64_t N, int M, int cus, hipStream_t stream) {
   int64_t blocks = (N + 3) / 4;
-  if (blocks > (int64_t)cus * 8) blocks = (int64_t)cus * 8;
+  if (blocks > (int64_t)cus * 32) blocks = (int64_t)cus * 32;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y, N, M);
+  const bool vec = (M % 4 == 0) && (M <= 4 * 64 * kSoftChunks) && ((reinterpret_cast<uintptr_t>(y) & 15) == 0);
+  if (vec)
+    hipLaunchKernelGGL(softmax_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y, N, M);
+  else
+    hipLaunchKernelGGL(softmax_rows_any_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y, N, M);
   return hipGetLastError();
+}
+
+template <int NJ, int LV>
+static hipError_t alaunch(const TArgs& t, int nw, int cus, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&tavg_kernel<NJ, LV>);
+  hipError_t err = hipSuccess;
+  const int per_cu = t_prepare(fn, nw * 64, t.lds_total, &err);
+  if (err != hipSuccess) return err;
+  int64_t blocks = t.nwork;
+  const int64_t resident = (int64_t)per_cu * cus;
+  if (blocks > resident) blocks = resident;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL((tavg_kernel<NJ, LV>), dim3((unsigned)blocks), dim3(nw * 64), t.lds_total, stream, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_tavg(int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {
+  if (nj != 1) return hipErrorInvalidValue;
+  if (t.C <= 64) return alaunch<1, 4>(t, nw, cus, stream);
+  if (t.C <= 128) return alaunch<1, 5>(t, nw, cus, stream);
+  return alaunch<1, 7>(t, nw, cus, stream);
 }
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {

@@ -106,6 +106,17 @@ def test_matmul_act_rejects(L):
     assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 3, NULL, NULL) == 1
 
 
+def test_accumulate_avg_rejects(L):
+    A = L.maddness_lut_accumulate_avg
+    assert A(FAKE, 10, 4, FAKE, FAKE, FAKE, 10, NULL, NULL, NULL) == 1   # both outputs NULL
+    assert A(FAKE, 10, 4, FAKE, NULL, FAKE, 10, FAKE, FAKE, NULL) == 1   # NULL scale
+    assert A(FAKE, 10, 600, FAKE, FAKE, FAKE, 10, FAKE, FAKE, NULL) == 3
+    assert A(NULL, 0, 4, NULL, NULL, NULL, 10, NULL, NULL, NULL) == 0
+    S = L.maddness_build_lut_shared
+    assert S(FAKE, FAKE, 0, 64, 10, FAKE, FAKE, FAKE, NULL) == 1
+    assert S(FAKE, FAKE, 600, 64, 10, FAKE, FAKE, FAKE, NULL) == 3
+
+
 def test_build_lut_rejects(L):
     B = L.maddness_build_lut
     assert B(FAKE, FAKE, 0, 64, 10, FAKE, FAKE, FAKE, NULL) == 1
