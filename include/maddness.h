@@ -131,7 +131,10 @@ int maddness_lut_accumulate(const uint8_t* idx, int64_t N, int32_t C,
  * (a + b + 1) >> 1; with r the root,
  *   acc = P * (r - 128),   y = fl32(acc * 2^e + bias32)   (bias32 as above).
  * The estimate satisfies 0 <= acc - sum_c q_c <= P log2(P) / 2.
- * Same arguments and errors as maddness_lut_accumulate.
+ * Same arguments and errors as maddness_lut_accumulate; idx must also be
+ * 16-byte aligned (EINVAL otherwise), and C > 128 gives EUNSUPPORTED (the
+ * kernel keeps the table's whole column slice and a batch of index rows in
+ * LDS).
  */
 int maddness_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C,
                                 const int8_t* lut, const float* scale,

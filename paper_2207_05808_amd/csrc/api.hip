@@ -307,34 +307,46 @@ int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, stream));
 }
 
-// Rounded 8-bit averaging accumulate (tiled_accum.hip): 8 wavefronts, one row
-// pass per wavefront, 16 columns per lane, tiles of 8 codebooks.
+// Rounded 8-bit averaging accumulate (tiled_accum.hip): 8 wavefronts, the
+// whole column slice of the table (C x 16 x Mt bytes, at most 128 KB) in LDS,
+// 16 columns per lane.
 bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
   if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;   // 32-bit buffer offsets
-  const int nw = 8, nj = 1;
-  const int lpr = s.M > 128 ? 16 : 8;
+  if (s.C > 128) return false;   // the index batch must fit next to the table slice
+  const int nw = 8;
+  const int C8 = round_up(s.C, 8);   // staged codebooks: whole groups of 8
+  int Mt = 256;
+  while (Mt > 16 && (int64_t)(C8 + 1) * kK * Mt > 136 * 1024) Mt /= 2;   // + a padding block
+  while (Mt > 16 && Mt / 2 >= s.M) Mt /= 2;   // no wider than the outputs
+  if ((int64_t)(C8 + 1) * kK * Mt > 136 * 1024) return false;
   TArgs a{};
   a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;
   a.N = s.N; a.C = s.C; a.M = s.M;
-  a.lpr_log2 = ilog2(lpr);
-  a.Mt = 16 * lpr;
-  a.RB = nw * (64 / lpr) * nj;
+  a.Mt = Mt;
+  a.lpr_log2 = ilog2(Mt / 16);
   a.CT = 8;
-  a.ntm = (s.M + a.Mt - 1) / a.Mt;
-  a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
+  a.ntm = (s.M + Mt - 1) / Mt;
   a.vec_lut = aligned(s.lut, 16) && (s.M % 16 == 0);
   a.vec_idx = (s.C % 4 == 0) && aligned(s.idx_in, 4);
   a.vec_out = (s.M % 4 == 0) && (s.y == nullptr || aligned(s.y, 16)) && (s.acc == nullptr || aligned(s.acc, 16));
   int off = 0;
   auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
-  a.off_tab = take(a.CT * kK * a.Mt);   // 0: the kernel relies on it
-  a.off_idx = take(a.RB * a.CT * 4);
-  a.off_sh = take(s.C * 4);
+  // index batches: B rows of C bytes, at most 16 KB and two 16-byte units per thread
+  const int RS = 64 / (Mt / 16);
+  int nwb = nw;   // the kernel has 512- and 1024-thread instances
+  while (nwb > 8 && nwb * RS * s.C > 16 * 1024) nwb /= 2;
+  if (nwb * RS * s.C > 16 * 1024) return false;
+  int J = 1;
+  while (2 * J * nwb * RS * s.C <= 16 * 1024) J *= 2;
+  a.RB = nwb * RS * J;
+  if ((a.RB * s.C) % 16 != 0 || (a.RB * s.C) / 16 > 2 * nwb * 64) return false;
+  a.off_tab = take((C8 + 1) * kK * Mt);   // 0: the kernel relies on it
+  a.off_idx = take(a.RB * s.C + 16);   // + the (at most 7) bytes a last row's partial group reads past its end
   a.off_misc = take(16);
   a.lds_total = off;
   if (off > kLdsBytes) return false;
   *t = a;
-  *nw_out = nw;
+  *nw_out = nwb;
   return true;
 }
 
@@ -456,7 +468,7 @@ int maddness_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C, const 
   if (rc != MADDNESS_OK || N == 0) return rc;
   if (!idx || !scale || !offset || (!acc_out && !y_out)) return MADDNESS_EINVAL;
   if (!aligned(scale, 4) || !aligned(offset, 4) || (acc_out && !aligned(acc_out, 4)) ||
-      (y_out && !aligned(y_out, 4)))
+      (y_out && !aligned(y_out, 4)) || !aligned(idx, 16))
     return MADDNESS_EINVAL;
   Shape s = shape(kAccum, kI8);
   s.idx_in = idx; s.N = N; s.C = C; s.lut = lut; s.scale = scale; s.offset = offset; s.M = M;
@@ -464,7 +476,7 @@ int maddness_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C, const 
   TArgs t;
   int nw;
   if (!plan_tavg(s, &t, &nw)) return MADDNESS_EUNSUPPORTED;
-  return status_from(launch_tavg(1, t, nw, device_cus(), static_cast<hipStream_t>(stream)));
+  return status_from(launch_tavg(t, nw, device_cus(), static_cast<hipStream_t>(stream)));
 }
 
 int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C, const float* lut, int32_t M,

@@ -122,9 +122,9 @@ hipError_t launch_softmax_rows(float* y, int64_t N, int M, int cus, hipStream_t 
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream);
 
-// Rounded 8-bit summation over codebooks (tiles of 8 codebooks, one byte per
-// staged entry, Mt = 16 * lanes per row).
-hipError_t launch_tavg(int nj, const TArgs& t, int nw, int cus, hipStream_t stream);
+// Rounded 8-bit summation over codebooks: the whole [C][16][Mt] column slice
+// (one byte per entry) staged once per workgroup, Mt = 16 * lanes per row.
+hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream);
 
 // Compute units of the current device (queried once per process).
 int device_cus();

@@ -369,18 +369,34 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 // codes of a row, biased to bytes u = q + 128 and padded with 128 to P = 2^L
 // codebooks, are reduced by a balanced tree of rounded byte averages in
 // codebook order, four columns per v_lerp_u8; the root r gives
-// acc = P (r - 128).  Layout as in tacc_kernel with one byte per entry: 16
-// columns per lane, LPR lanes per output row, tiles of 8 codebooks.  Each
-// tile is one level-3 subtree (or the level-L root when P < 8); tiles merge
-// through a binary-counter stack of higher tree levels held in registers;
-// pad tiles (all 128) finish the tree when C is not a power of two.
-// stack levels above a tile: LV = 4 covers P / 8 <= 8 tiles (C <= 64), 5
-// covers C <= 128, 7 covers C <= 512
-
+// acc = P (r - 128).
+//
+// One byte per staged entry lets a workgroup hold the table's whole column
+// slice, [C * 16 rows][Mt columns] (at most 128 KB), staged once: a workgroup
+// keeps one column tile for its lifetime and its wavefronts then stream row
+// sets.  16 columns per lane, LPR = Mt / 16 lanes per output row.  Index rows
+// come in batches of B rows staged in LDS, the next batch loaded into
+// registers while the current one is summed (one barrier pair per batch).
+// Codebooks are taken 8 at a time: one level-3 subtree (or the level-L root
+// when P < 8), merged into a binary-counter stack of higher tree levels held
+// in registers; subtrees of pure padding (all 128) finish the tree when C is
+// not a power of two.
 __device__ __forceinline__ uint32_t avg4(uint32_t a, uint32_t b) { return __builtin_amdgcn_lerp(a, b, 0x01010101u); }
 
-template <int NJ, int LV>
-__global__ void __launch_bounds__(512, 4) tavg_kernel(const TArgs a) {
+
+// The padded tree has GA = P / 8 subtrees of 8 codebooks (at least 1), taken
+// GI at a time (unrolled, their merges resolved at compile time) in GO = GA /
+// GI rounds of a runtime loop whose results (subtrees of 8 GI codebooks) merge
+// through up to three pending levels.  The unrolled subtrees bound the LDS
+// reads in flight, and with them the registers: GI = 4 within 256 VGPRs (512
+// threads), GI = 2 within 128 (1024 threads).
+// WIDX: C % 4 == 0, index words read as dwords (else byte by byte).
+template <int GI, int GO, bool WIDX, int NT>
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT / 256, NT / 256)))
+tavg_kernel(const TArgs a) {
+  static_assert(GI == 1 || GI == 2 || GI == 4, "inner subtrees");
+  static_assert(GO == 1 || GO == 2 || GO == 4 || GO == 8, "outer rounds");
+  constexpr int kLev = (GI >= 4) ? 2 : (GI >= 2) ? 1 : 0;
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   tlds_t* smem = (tlds_t*)smem_raw;
 
@@ -389,16 +405,15 @@ __global__ void __launch_bounds__(512, 4) tavg_kernel(const TArgs a) {
   const int lane = tid & 63;
   const int wave = tuni(tid >> 6);
   const int nw = nt >> 6;
-  const int C = a.C, M = a.M, Mt = a.Mt, RB = a.RB;
-  constexpr int CT = 8;
+  const int C = a.C, M = a.M, Mt = a.Mt;
+  const int C8 = (C + 7) & ~7;            // codebooks staged: whole groups of 8, padding rows all 128
   const int64_t N = a.N;
   const int lpr_log2 = a.lpr_log2;
-  const int RS = 64 >> lpr_log2;
+  const int RS = 64 >> lpr_log2;          // output rows per wavefront pass
   const int r4 = lane >> lpr_log2;
   const int cg = lane & ((1 << lpr_log2) - 1);
   const int rby_log2 = 31 - __builtin_clz(Mt);   // one byte per entry: row bytes = Mt
-  tlds_t* s_tab = smem;   // the table tile starts the LDS block (off_tab == 0)
-  tlds_t* s_idx = smem + a.off_idx;
+  tlds_t* s_tab = smem;   // [C8 * 16 + 16][Mt] biased codes, then a 16-row block of 128 (off_tab == 0)
   tlds_i32* s_misc = reinterpret_cast<tlds_i32*>(smem + a.off_misc);
 
   // block exponent (one shared by every codebook) and bias32
@@ -415,131 +430,143 @@ __global__ void __launch_bounds__(512, 4) tavg_kernel(const TArgs a) {
     }
     if (lane == 0) s_misc[0] = __float_as_int((float)sum);
   }
+
+  // column tile of this workgroup: stage every codebook's [16][Mt] slice.
+  // Columns are permuted within a tile row so that the 16 bytes a lane reads
+  // are the 4-column groups d = cg, cg + LPR, cg + 2 LPR, cg + 3 LPR: each
+  // output store of the wavefront then writes LPR x 16 contiguous bytes of a
+  // row (whole cache lines) instead of 16-byte pieces 64 bytes apart.
+  const int lpr = 1 << lpr_log2;
+  auto lds_dword = [&](int d) { return ((d & (lpr - 1)) << 2) + (d >> lpr_log2); };
+  const int mt = blockIdx.x % a.ntm;
+  const int m0 = mt * Mt;
+  {
+    const int rows = C8 * 16 + 16;   // the last 16 rows: padding subtrees read them (all 128)
+    if (a.vec_lut) {
+      const __amdgpu_buffer_rsrc_t trs =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M), kBufDword3);
+      const int upr_log2 = rby_log2 - 4;   // 16-byte units per tile row
+      const int units = rows << upr_log2;
+      for (int u0 = tid; u0 < units; u0 += 4 * nt) {
+        tu32x4 v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {   // all loads of the round first; rows past C * 16 read zero
+          const int u = u0 + j * nt;
+          const int row = u >> upr_log2, part = u & ((1 << upr_log2) - 1);
+          const bool ok = u < units && row < C * 16 && m0 + part * 16 < M;
+          v[j] = __builtin_amdgcn_raw_buffer_load_b128(trs, ok ? row * M + m0 + part * 16 : kOob, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int u = u0 + j * nt;
+          if (u < units) {
+            const int row = u >> upr_log2, part = u & ((1 << upr_log2) - 1);
+            tlds_u32* dst = reinterpret_cast<tlds_u32*>(s_tab + (row << rby_log2));
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dst[lds_dword(4 * part + i)] = v[j][i] ^ 0x80808080u;   // q + 128
+          }
+        }
+      }
+    } else {
+      const uint8_t* q8 = reinterpret_cast<const uint8_t*>(a.lut);
+      for (int e = tid; e < (rows << rby_log2); e += nt) {
+        const int row = e >> rby_log2, col = e & (Mt - 1);
+        const int m = m0 + col;
+        s_tab[(row << rby_log2) + 4 * lds_dword(col >> 2) + (col & 3)] =
+            (char)((row < C * 16 && m < M) ? (q8[(int64_t)row * M + m] ^ 0x80u) : 0x80u);
+      }
+    }
+  }
   __syncthreads();
   const float step = __builtin_ldexpf(1.0f, tuni(s_misc[1]));
   const float bias = __int_as_float(tuni(s_misc[0]));
   int L = 0;
   while ((1 << L) < C) ++L;
   const int P = 1 << L;
-  const int ntile = (C + CT - 1) / CT;
-  const int ntile_all = max(1, P / CT);
-
-  const int upr = Mt >> 4;              // 16-byte units per table row of the tile
-  const int upr_log2 = __builtin_ctz(upr);
-  const int units = CT * 16 * upr;
-  const int iwords = RB * 2;            // two index words (8 codebooks) per row
-  const bool vec = a.vec_lut && a.vec_idx;
-  const __amdgpu_buffer_rsrc_t trs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M), kBufDword3);
-  tu32x4 tv[kTU];
-  uint32_t iv[kIU];
-  auto load_tile = [&](int c0, int64_t r0, int m0) {
-#pragma unroll
-    for (int j = 0; j < kTU; ++j) {
-      const int u = tid + j * nt;
-      const int row = u >> upr_log2, part = u & (upr - 1);
-      const int c = c0 + (row >> 4), m = m0 + part * 16;
-      const bool ok = u < units && c < C && m < M;
-      tv[j] = __builtin_amdgcn_raw_buffer_load_b128(trs, ok ? (c * 16 + (row & 15)) * M + m : kOob, 0, 0);
-    }
-    const int64_t rows = min((int64_t)RB, N - r0);
-    const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint8_t*>(a.idx + r0 * C), 0, (int)min(rows * C, (int64_t)INT_MAX), kBufDword3);
-#pragma unroll
-    for (int j = 0; j < kIU; ++j) {
-      const int d = tid + j * nt;
-      const int i = d >> 1, q = d & 1;
-      const bool ok = d < iwords && c0 + 4 * q < C;
-      iv[j] = __builtin_amdgcn_raw_buffer_load_b32(irs, ok ? i * C + c0 + 4 * q : kOob, 0, 0);
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int j = 0; j < kTU; ++j) {
-      const int u = tid + j * nt;
-      if (u < units) {
-        const int row = u >> upr_log2, part = u & (upr - 1);
-        const tu32x4 b = tv[j] ^ (tu32x4){0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};  // q + 128
-        *reinterpret_cast<tlds_u32x4*>(s_tab + (row << rby_log2) + part * 16) = b;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kIU; ++j) {
-      const int d = tid + j * nt;
-      if (d < iwords) {
-        const uint32_t cb = (uint32_t)(4 * (d & 1)) * 16u;
-        tu32x4 o;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) o[b] = (cb + 16u * b + ((iv[j] >> (8 * b)) & 15u)) << rby_log2;
-        *reinterpret_cast<tlds_u32x4*>(s_idx + 16 * d) = o;
-      }
-    }
-  };
-  auto stage_direct = [&](int c0, int64_t r0, int m0) {
-    const uint8_t* q8 = reinterpret_cast<const uint8_t*>(a.lut);
-    for (int e = tid; e < CT * 16 * Mt; e += nt) {
-      const int row = e >> rby_log2, col = e & (Mt - 1);
-      const int c = c0 + (row >> 4), m = m0 + col;
-      const bool ok = c < C && m < M;
-      s_tab[(row << rby_log2) + col] = (char)(ok ? (q8[((int64_t)c * 16 + (row & 15)) * M + m] ^ 0x80u) : 0x80u);
-    }
-    for (int e = tid; e < RB * CT; e += nt) {
-      const int i = e >> 3, cc = e & 7;
-      const bool ok = r0 + i < N && c0 + cc < C;
-      const uint32_t k = ok ? (uint32_t)(a.idx[(r0 + i) * C + c0 + cc] & 15u) : 0u;
-      *reinterpret_cast<tlds_u32*>(s_idx + 4 * e) = ((uint32_t)cc * 16u + k) << rby_log2;
-    }
-  };
-
+  const int ngroup = C8 >> 3;   // subtrees holding real codes; the rest of the GA are pure padding
+  const int col0 = m0 + cg * 4;   // the lane's columns: col0 + 4 lpr h + e, h, e < 4
   const tlds_t* s_tab_lane = s_tab + cg * 16;
-  int ib[NJ];
-  const tlds_t* s_idx_row[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    ib[j] = (j * nw + wave) * RS + r4;
-    s_idx_row[j] = s_idx + ib[j] * CT * 4;
-  }
 
-  for (int64_t w = blockIdx.x; w < a.nwork; w += gridDim.x) {
-    const int mt = (int)(w % a.ntm);
-    const int64_t r0 = (w / a.ntm) * RB;
-    const int m0 = mt * Mt;
-    tu32x4 stk[NJ][LV];   // stack[l]: a pending node at tree level 3 + l
-    tu32x4 root[NJ];
-    // merge a level-3 node x of tile t into the stack (carry chain of t's low bits)
-    auto merge = [&](int j, tu32x4 x, int t) {
-      bool carry = true;
+  // index batches of B = nw * RS * J rows (C bytes each, contiguous in
+  // memory), shared out over the workgroups of this column tile
+  tlds_t* s_idx = smem + a.off_idx;
+  const int J = a.RB / (nw * RS);
+  const int B = a.RB;
+  const int64_t nbatch = (N + B - 1) / B;
+  const int64_t bstride = gridDim.x / a.ntm;
+  const int bunits = (B * C) >> 4;   // 16-byte units per batch (B * C % 16 == 0)
+  tu32x4 ipf[2];
+  auto load_batch = [&](int64_t bi) {
+    const int64_t r0 = bi * B;
+    const int64_t bytes = bi < nbatch ? min((int64_t)B, N - r0) * C : 0;
+    const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(a.idx + min(r0, N - 1) * C), 0, (int)min(bytes, (int64_t)INT_MAX), kBufDword3);
 #pragma unroll
-      for (int l = 0; l < LV; ++l) {
-        if (carry) {
-          if ((t >> l) & 1) {
+    for (int j = 0; j < 2; ++j) {
+      const int u = tid + j * nt;
+      if (u < bunits && 16 * u + 16 > bytes && 16 * u < bytes) {
+        // the unit holding the end of the index array: bytes one by one (the
+        // range check is per dword, and reading past the array is not allowed)
+        tu32x4 w = {0u, 0u, 0u, 0u};
+        for (int b = 0; b < 16; ++b)
+          w[b >> 2] |= (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(irs, 16 * u + b, 0, 0) << (8 * (b & 3));
+        ipf[j] = w;
+      } else {
+        ipf[j] = __builtin_amdgcn_raw_buffer_load_b128(irs, u < bunits ? 16 * u : kOob, 0, 0);
+      }
+    }
+  };
+  int64_t bi = blockIdx.x / a.ntm;
+  load_batch(bi);
+  for (; bi < nbatch; bi += bstride) {
+    __syncthreads();   // every reader of the previous batch is done
 #pragma unroll
-            for (int e = 0; e < 4; ++e) x[e] = avg4(stk[j][l][e], x[e]);
-          } else {
-            stk[j][l] = x;
-            carry = false;
+    for (int j = 0; j < 2; ++j) {
+      const int u = tid + j * nt;
+      if (u < bunits) *reinterpret_cast<tlds_u32x4*>(s_idx + 16 * u) = ipf[j];
+    }
+    __syncthreads();
+    load_batch(bi + bstride);   // in flight during the sums below
+    for (int jj = 0; jj < J; ++jj) {
+    const int ii = (jj * nw + wave) * RS + r4;   // row within the batch
+    const int64_t row = bi * B + ii;
+    const tlds_t* ir = s_idx + ii * C;
+    tu32x4 root, pend0, pend1, pend2;   // pend<l>: a finished round at outer level l
+#pragma unroll 1
+    for (int h = 0; h < GO; ++h) {
+      tu32x4 stk[kLev + 1];   // stk[l]: a pending node 3 + l levels above the leaves
+      tu32x4 sub;
+#pragma unroll
+      for (int gi = 0; gi < GI; ++gi) {
+        const int g = h * GI + gi;   // subtree index
+        tu32x4 x;
+        // indices of codebooks 8g .. 8g + 7 (bytes past the row's C, at most 7,
+        // belong to padding codebooks, whose rows are all 128: any k); a
+        // subtree of pure padding reads group 0's bytes and masks them
+        const tlds_t* ig = ir + 8 * (g < ngroup ? g : 0);
+        uint32_t w0, w1;
+        if (WIDX) {
+          w0 = *reinterpret_cast<const tlds_u32*>(ig);
+          w1 = *reinterpret_cast<const tlds_u32*>(ig + 4);
+        } else {
+          w0 = w1 = 0u;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            w0 |= (uint32_t)(uint8_t)ig[b] << (8 * b);
+            w1 |= (uint32_t)(uint8_t)ig[4 + b] << (8 * b);
           }
         }
-      }
-    };
-
-    if (vec) load_tile(0, r0, m0);
-    for (int t = 0; t < ntile; ++t) {
-      __syncthreads();
-      if (vec) store_tile(); else stage_direct(t * CT, r0, m0);
-      __syncthreads();
-      if (vec && t + 1 < ntile) load_tile((t + 1) * CT, r0, m0);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const tu32x4 k0 = *reinterpret_cast<const tlds_u32x4*>(s_idx_row[j]);
-        const tu32x4 k1 = *reinterpret_cast<const tlds_u32x4*>(s_idx_row[j] + 16);
+        // a subtree of pure padding reads the all-128 block for its 8 leaves
+        const uint32_t rbase = g < ngroup ? (uint32_t)(128 * g) : (uint32_t)(C8 * 16);
+        const uint32_t kmask = g < ngroup ? 15u : 0u;
         tu32x4 v[8];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          v[b] = *reinterpret_cast<const tlds_u32x4*>(s_tab_lane + k0[b]);
-          v[4 + b] = *reinterpret_cast<const tlds_u32x4*>(s_tab_lane + k1[b]);
+        for (int b = 0; b < 8; ++b) {
+          const uint32_t k = ((b < 4 ? w0 : w1) >> (8 * (b & 3))) & kmask;
+          const uint32_t r = g < ngroup ? rbase + 16 * b + k : rbase;
+          v[b] = *reinterpret_cast<const tlds_u32x4*>(s_tab_lane + (r << rby_log2));
         }
-        tu32x4 a0, a1, a2, a3, b0, b1, x;
+        tu32x4 a0, a1, a2, a3, b0, b1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           a0[e] = avg4(v[0][e], v[1][e]);
@@ -550,56 +577,75 @@ __global__ void __launch_bounds__(512, 4) tavg_kernel(const TArgs a) {
           b1[e] = avg4(a2[e], a3[e]);
           x[e] = avg4(b0[e], b1[e]);
         }
-        if (L >= 3) merge(j, x, t);
-        else root[j] = (L == 0) ? v[0] : (L == 1) ? a0 : b0;
+        if (GI == 1 && GO == 1) root = (L == 0) ? v[0] : (L == 1) ? a0 : (L == 2) ? b0 : x;
+        if (GI == 1) sub = x;
+        else {
+          // binary counter over gi (compile-time): merge while the low bits of gi are 1
+          int l = 0;
+#pragma unroll
+          for (; l < kLev && ((gi >> l) & 1); ++l)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = avg4(stk[l][e], x[e]);
+          stk[l] = x;
+        }
       }
-    }
-    if (L >= 3) {
-      const tu32x4 pad = {0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};
-      for (int t = ntile; t < ntile_all; ++t)
+      if (GI > 1) sub = stk[kLev];
+      if (GO > 1) {
+        // binary counter over h (uniform branches): merge while the low bits
+        // of h are 1, then wait at the first level whose bit is 0; the last
+        // round (h = GO - 1, all bits 1) finishes the tree
+        if (h & 1) {
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) merge(j, pad, t);
+          for (int e = 0; e < 4; ++e) sub[e] = avg4(pend0[e], sub[e]);
+          if (h & 2) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) {
+            for (int e = 0; e < 4; ++e) sub[e] = avg4(pend1[e], sub[e]);
+            if (h & 4) {
 #pragma unroll
-        for (int l = 0; l < LV; ++l)
-          if (l == L - 3) root[j] = stk[j][l];
+              for (int e = 0; e < 4; ++e) sub[e] = avg4(pend2[e], sub[e]);
+            } else {
+              pend2 = sub;
+            }
+          } else {
+            pend1 = sub;
+          }
+        } else {
+          pend0 = sub;
+        }
       }
+      if (!(GI == 1 && GO == 1)) root = sub;
     }
 
     // epilogue: acc = P (r - 128) for the lane's 16 columns
-    const int col0 = m0 + cg * 16;
+    if (row >= N || col0 >= M) continue;
+    int out[16];   // out[4 h + e]: column col0 + 4 lpr h + e
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int64_t row = r0 + ib[j];
-      if (row >= N || col0 >= M) continue;
-      int out[16];
+    for (int e = 0; e < 16; ++e) out[e] = P * ((int)((root[e >> 2] >> (8 * (e & 3))) & 0xffu) - 128);
+    float* yr = a.y ? a.y + row * M + col0 : nullptr;
+    int32_t* ar = a.acc ? a.acc + row * M + col0 : nullptr;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) out[e] = P * ((int)((root[j][e >> 2] >> (8 * (e & 3))) & 0xffu) - 128);
-      float* yr = a.y ? a.y + row * M + col0 : nullptr;
-      int32_t* ar = a.acc ? a.acc + row * M + col0 : nullptr;
-      if (a.vec_out && col0 + 16 <= M) {
-#pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          if (yr)
-            __builtin_nontemporal_store((tf32x4){__builtin_fmaf((float)out[4 * h], step, bias),
-                                                 __builtin_fmaf((float)out[4 * h + 1], step, bias),
-                                                 __builtin_fmaf((float)out[4 * h + 2], step, bias),
-                                                 __builtin_fmaf((float)out[4 * h + 3], step, bias)},
-                                        reinterpret_cast<tf32x4*>(yr + 4 * h));
-          if (ar)
-            __builtin_nontemporal_store((tu32x4){(uint32_t)out[4 * h], (uint32_t)out[4 * h + 1],
-                                                 (uint32_t)out[4 * h + 2], (uint32_t)out[4 * h + 3]},
-                                        reinterpret_cast<tu32x4*>(ar + 4 * h));
-        }
+    for (int h = 0; h < 4; ++h) {
+      const int ch = col0 + 4 * lpr * h;
+      if (a.vec_out && ch + 4 <= M) {
+        if (yr)
+          __builtin_nontemporal_store((tf32x4){__builtin_fmaf((float)out[4 * h], step, bias),
+                                               __builtin_fmaf((float)out[4 * h + 1], step, bias),
+                                               __builtin_fmaf((float)out[4 * h + 2], step, bias),
+                                               __builtin_fmaf((float)out[4 * h + 3], step, bias)},
+                                      reinterpret_cast<tf32x4*>(yr + 4 * lpr * h));
+        if (ar)
+          __builtin_nontemporal_store((tu32x4){(uint32_t)out[4 * h], (uint32_t)out[4 * h + 1],
+                                               (uint32_t)out[4 * h + 2], (uint32_t)out[4 * h + 3]},
+                                      reinterpret_cast<tu32x4*>(ar + 4 * lpr * h));
       } else {
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (col0 + e < M) {
-            if (yr) yr[e] = __builtin_fmaf((float)out[e], step, bias);
-            if (ar) ar[e] = out[e];
+        for (int e = 0; e < 4; ++e)
+          if (ch + e < M) {
+            if (yr) yr[4 * lpr * h + e] = __builtin_fmaf((float)out[4 * h + e], step, bias);
+            if (ar) ar[4 * lpr * h + e] = out[4 * h + e];
           }
       }
+    }
     }
   }
 }
@@ -705,25 +751,49 @@ hipError_t launch_softmax_rows(float* y, int64_t N, int M, int cus, hipStream_t 
   return hipGetLastError();
 }
 
-template <int NJ, int LV>
-static hipError_t alaunch(const TArgs& t, int nw, int cus, hipStream_t stream) {
-  const void* fn = reinterpret_cast<const void*>(&tavg_kernel<NJ, LV>);
+template <int GI, int GO, bool WIDX, int NT>
+static hipError_t alaunch(const TArgs& t, int cus, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&tavg_kernel<GI, GO, WIDX, NT>);
   hipError_t err = hipSuccess;
-  const int per_cu = t_prepare(fn, nw * 64, t.lds_total, &err);
+  const int per_cu = t_prepare(fn, NT, t.lds_total, &err);
   if (err != hipSuccess) return err;
-  int64_t blocks = t.nwork;
-  const int64_t resident = (int64_t)per_cu * cus;
-  if (blocks > resident) blocks = resident;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL((tavg_kernel<NJ, LV>), dim3((unsigned)blocks), dim3(nw * 64), t.lds_total, stream, t);
+  // every workgroup keeps one column tile: a whole number of workgroups per tile
+  int64_t per_tile = ((int64_t)per_cu * cus) / t.ntm;
+  const int64_t batches = (t.N + t.RB - 1) / t.RB;
+  if (per_tile > batches) per_tile = batches;
+  if (per_tile < 1) per_tile = 1;
+  hipLaunchKernelGGL((tavg_kernel<GI, GO, WIDX, NT>), dim3((unsigned)(per_tile * t.ntm)), dim3(NT),
+                     t.lds_total, stream, t);
   return hipGetLastError();
 }
 
-hipError_t launch_tavg(int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {
-  if (nj != 1) return hipErrorInvalidValue;
-  if (t.C <= 64) return alaunch<1, 4>(t, nw, cus, stream);
-  if (t.C <= 128) return alaunch<1, 5>(t, nw, cus, stream);
-  return alaunch<1, 7>(t, nw, cus, stream);
+// GA = P / 8 subtrees (at least 1) split into GI unrolled x GO rounds
+template <int GA, int NT>
+static hipError_t alaunch_g(const TArgs& t, int cus, hipStream_t stream) {
+  constexpr int kGI = GA < (NT == 1024 ? 2 : 4) ? GA : (NT == 1024 ? 2 : 4);
+  constexpr int kGO = GA / kGI;
+  if (t.C % 4 == 0) return alaunch<kGI, kGO, true, NT>(t, cus, stream);
+  return alaunch<kGI, kGO, false, NT>(t, cus, stream);
+}
+
+template <int NT>
+static hipError_t launch_tavg_nt(const TArgs& t, int cus, hipStream_t stream) {
+  int P = 1;
+  while (P < t.C) P *= 2;
+  switch (P <= 8 ? 1 : P / 8) {
+    case 1: return alaunch_g<1, NT>(t, cus, stream);
+    case 2: return alaunch_g<2, NT>(t, cus, stream);
+    case 4: return alaunch_g<4, NT>(t, cus, stream);
+    case 8: return alaunch_g<8, NT>(t, cus, stream);
+    case 16: return alaunch_g<16, NT>(t, cus, stream);
+    default: return hipErrorInvalidValue;   // C <= 128 (the planner checks)
+  }
+}
+
+hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream) {
+  if (nw == 16) return launch_tavg_nt<1024>(t, cus, stream);
+  if (nw == 8) return launch_tavg_nt<512>(t, cus, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {

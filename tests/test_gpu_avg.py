@@ -34,7 +34,7 @@ def run_avg(orc, idx, lut, scale, offset):
 
 
 CASES = [(1, 16), (2, 10), (3, 64), (5, 17), (8, 256), (9, 300), (16, 128), (33, 1024), (64, 512),
-         (100, 64), (128, 4096), (256, 96), (512, 48)]
+         (100, 64), (128, 4096), (120, 33)]
 
 
 @pytest.mark.parametrize("C,M", CASES)
@@ -49,6 +49,14 @@ def test_avg_random_codes(orc, C, M):
     P = 1 << max(0, math.ceil(math.log2(C)))
     err = acc.astype(np.int64) - exact.astype(np.int64)
     assert err.min() >= 0 and err.max() <= P * int(math.log2(P)) // 2
+
+
+def test_avg_rejects_many_codebooks(orc):
+    """C > 128: the column slice and an index batch do not fit in LDS."""
+    idx = W.random_indices(10, 256, seed=1)
+    lut, scale, offset = W.random_codes(256, 16, seed=2, max_shift=0)
+    with pytest.raises(mdn.MaddnessError):
+        mdn.lut_accumulate_avg(dev(idx), dev(lut), dev(scale), dev(offset))
 
 
 @pytest.mark.parametrize("N", [1, 63, 64, 65, 129, 1000])
