@@ -258,7 +258,13 @@ def main():
             slut, sscale, soffset = mdn.build_lut_shared(torch.from_numpy(p.P).to(dev), Bd)
             avg_us = region_us(lambda i: mdn.lut_accumulate_avg(idx, slut, sscale, soffset, y_out=y))
             result["context"]["accumulate_avg8_us"] = round(avg_us, 2)
-            del slut
+            # its accuracy cost: relative Frobenius distance to the exact sum
+            # over the same shared-exponent table
+            _, y_exact = mdn.lut_accumulate(idx, slut, sscale, soffset)
+            torch.cuda.synchronize()
+            d = (y.double() - y_exact.double()).norm() / y_exact.double().norm()
+            result["context"]["avg8_rel_frobenius_diff"] = float(f"{float(d):.4g}")
+            del slut, y_exact
         del idx
         # the same step with the layer output sigma fused (bias + ReLU, bias + row softmax)
         cb = torch.from_numpy(np.random.default_rng(1).standard_normal(spec.M).astype(np.float32)).to(dev)

@@ -18,6 +18,8 @@ Functions and the passages they follow (the paper: McCarter & Dronen,
 * :func:`sigma` -- §2.2 (layer output: bias, then ReLU or row softmax), R19.
 * :func:`lut_accumulate_avg`, :func:`quantize_table_shared` -- §1 (rounded
   8-bit summation over codebooks, one shared block exponent), reading R20.
+* :func:`encoder_gram`, :func:`encoder_scatter`, :func:`fit_lut_ridge` --
+  §2.2, Eq. 3 (model-aware table fit) with sigma affine, reading R21.
 """
 from __future__ import annotations
 
@@ -76,6 +78,9 @@ class Oracle:
         lib.oracle_sigma.argtypes = [vp, i64, i32, vp, i32, vp]
         lib.oracle_quantize_table_shared.argtypes = [vp, i32, i32, vp, vp, vp]
         lib.oracle_lut_accumulate_avg.argtypes = [vp, i64, i32, vp, vp, vp, i32, vp, vp]
+        lib.oracle_encoder_gram.argtypes = [vp, i64, i32, vp]
+        lib.oracle_encoder_scatter.argtypes = [vp, i64, i32, vp, i32, vp]
+        lib.oracle_fit_lut_ridge.argtypes = [vp, i64, i32, vp, i32, vp, ctypes.c_double, vp]
         self.lib = lib
 
     @staticmethod
@@ -226,6 +231,41 @@ class Oracle:
         rc = self.lib.oracle_sigma(y.ctypes.data, N, M, bp, int(act), out.ctypes.data)
         self._check(rc, "oracle_sigma")
         return out
+
+    def encoder_gram(self, idx):
+        """H = G^T G of the one-hot encoder output, int64 [16C, 16C] (Eq. 3, R21)."""
+        idx = np.ascontiguousarray(idx, dtype=np.uint8)
+        N, C = idx.shape
+        H = np.zeros((C * K, C * K), dtype=np.int64)
+        self._check(self.lib.oracle_encoder_gram(idx.ctypes.data, N, C, H.ctypes.data), "oracle_encoder_gram")
+        return H
+
+    def encoder_scatter(self, idx, Y):
+        """R = G^T Y, float64 [16C, M] (Eq. 3, R21)."""
+        idx = np.ascontiguousarray(idx, dtype=np.uint8)
+        Y = np.ascontiguousarray(Y, dtype=np.float32)
+        N, C = idx.shape
+        assert Y.shape[0] == N
+        M = Y.shape[1]
+        R = np.zeros((C * K, M), dtype=np.float64)
+        rc = self.lib.oracle_encoder_scatter(idx.ctypes.data, N, C, Y.ctypes.data, M, R.ctypes.data)
+        self._check(rc, "oracle_encoder_scatter")
+        return R
+
+    def fit_lut_ridge(self, idx, Y, T0, lam):
+        """Eq. 3 with sigma affine (R21): the table T minimising
+        ||Y - G T||^2 + lam ||T - T0||^2, float64 [C, 16, M]."""
+        idx = np.ascontiguousarray(idx, dtype=np.uint8)
+        Y = np.ascontiguousarray(Y, dtype=np.float32)
+        T0 = np.ascontiguousarray(T0, dtype=np.float32)
+        N, C = idx.shape
+        M = Y.shape[1]
+        assert Y.shape[0] == N and T0.shape == (C, K, M)
+        T = np.zeros((C, K, M), dtype=np.float64)
+        rc = self.lib.oracle_fit_lut_ridge(idx.ctypes.data, N, C, Y.ctypes.data, M, T0.ctypes.data,
+                                           ctypes.c_double(lam), T.ctypes.data)
+        self._check(rc, "oracle_fit_lut_ridge")
+        return T
 
     # convenience compositions (no arithmetic of their own)
     def matmul(self, A, split, thr, lut, scale, offset):

@@ -30,6 +30,14 @@
  *   R9  y = fl32( float(acc) * 2^e_min + bias32 ), one rounding (fmaf), with
  *       bias32 = fl32( sum_c offset_c accumulated in double, c ascending ).
  *   R10 unquantized mode: y = (((0 + T_0) + T_1) + ...) in fp32, c ascending.
+ *   R21 model-aware table fit (Eq. 3) with sigma affine (bias and identity,
+ *       so the bias cancels): minimise sum_n ||y_n - g_n^T T||^2 +
+ *       lambda ||T - T0||^2 over T, squared Frobenius norms with no 1/N, g_n
+ *       the one-hot encoder output (G[n][16c + k] = 1 iff idx[n][c] = k),
+ *       targets Y = AB and the prototype table T0 = P0 B given in fp32 and
+ *       taken exactly, lambda > 0; the minimiser solves the normal equations
+ *       (G^T G + lambda I) T = G^T Y + lambda T0, column by column, in
+ *       double.
  *   R19 layer output sigma: z = fl32(y + bias_m); ReLU keeps z when z > 0 and
  *       gives +0 otherwise; softmax is taken over the M outputs of a row.
  *   R20 rounded 8-bit summation: one shared block exponent; biased codes
@@ -411,4 +419,101 @@ int oracle_lut_accumulate_avg(const uint8_t* idx, int64_t N, int32_t C,
         }
     }
     return 0;
+}
+
+/*
+ * Gram matrix of the one-hot encoder output, H = G^T G (the matrix of the
+ * normal equations of Eq. 3 under reading R21): H[16c + k][16c' + k'] counts
+ * the rows n with idx[n][c] = k and idx[n][c'] = k'.  H is [16C][16C].
+ */
+int oracle_encoder_gram(const uint8_t* idx, int64_t N, int32_t C, int64_t* H)
+{
+    if (N < 0 || C <= 0 || !H || (N > 0 && !idx)) return -1;
+    const int64_t n16 = (int64_t)C * ORACLE_K;
+    for (int64_t j = 0; j < n16 * n16; ++j) H[j] = 0;
+    for (int64_t n = 0; n < N; ++n)
+        for (int32_t c = 0; c < C; ++c)
+            for (int32_t c2 = 0; c2 < C; ++c2) {
+                const int64_t r = (int64_t)c * ORACLE_K + idx[n * C + c];
+                const int64_t s = (int64_t)c2 * ORACLE_K + idx[n * C + c2];
+                H[r * n16 + s] += 1;
+            }
+    return 0;
+}
+
+/*
+ * R = G^T Y (right-hand side of the normal equations of Eq. 3, reading R21):
+ * R[16c + k][m] = sum over the rows n with idx[n][c] = k of Y[n][m], summed in
+ * double over n ascending.  R is [16C][M].
+ */
+int oracle_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C,
+                           const float* Y, int32_t M, double* R)
+{
+    if (N < 0 || C <= 0 || M <= 0 || !R || (N > 0 && (!idx || !Y))) return -1;
+    const int64_t n16 = (int64_t)C * ORACLE_K;
+    for (int64_t j = 0; j < n16 * M; ++j) R[j] = 0.0;
+    for (int64_t n = 0; n < N; ++n)
+        for (int32_t c = 0; c < C; ++c) {
+            const int64_t r = (int64_t)c * ORACLE_K + idx[n * C + c];
+            for (int32_t m = 0; m < M; ++m) R[r * M + m] += (double)Y[n * M + m];
+        }
+    return 0;
+}
+
+/*
+ * Model-aware table fit, Eq. 3 with sigma affine (reading R21): T [C][16][M]
+ * solves (H + lambda I) T = R + lambda T0 with H and R as above.  The
+ * matrix is symmetric positive definite for lambda > 0; it is factored as
+ * L L^T (Cholesky, textbook order: column j from the columns before it) and
+ * each of the M columns is solved by forward then backward substitution.
+ * Returns -1 on bad sizes, -2 when lambda is not a positive finite number.
+ */
+int oracle_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
+                         const float* Y, int32_t M, const float* T0,
+                         double lambda, double* T)
+{
+    if (N < 0 || C <= 0 || M <= 0 || C > 1024 || !T0 || !T) return -1;
+    if (!(lambda > 0.0) || !isfinite(lambda)) return -2;
+    const int64_t n16 = (int64_t)C * ORACLE_K;
+    int64_t* H = (int64_t*)malloc(sizeof(int64_t) * n16 * n16);
+    double* L = (double*)malloc(sizeof(double) * n16 * n16);
+    double* R = (double*)malloc(sizeof(double) * n16 * M);
+    double* z = (double*)malloc(sizeof(double) * n16);
+    int rc = (!H || !L || !R || !z) ? -1 : 0;
+    if (rc == 0) rc = oracle_encoder_gram(idx, N, C, H);
+    if (rc == 0) rc = oracle_encoder_scatter(idx, N, C, Y, M, R);
+    if (rc == 0) {
+        /* A = H + lambda I, factored in place into its lower triangle */
+        for (int64_t i = 0; i < n16; ++i)
+            for (int64_t j = 0; j < n16; ++j)
+                L[i * n16 + j] = (double)H[i * n16 + j] + (i == j ? lambda : 0.0);
+        for (int64_t j = 0; j < n16; ++j) {
+            double d = L[j * n16 + j];
+            for (int64_t k = 0; k < j; ++k) d -= L[j * n16 + k] * L[j * n16 + k];
+            d = sqrt(d);
+            L[j * n16 + j] = d;
+            for (int64_t i = j + 1; i < n16; ++i) {
+                double v = L[i * n16 + j];
+                for (int64_t k = 0; k < j; ++k) v -= L[i * n16 + k] * L[j * n16 + k];
+                L[i * n16 + j] = v / d;
+            }
+        }
+        for (int32_t m = 0; m < M; ++m) {
+            /* right-hand side column m: (G^T Y)[.][m] + lambda T0[.][m] */
+            for (int64_t i = 0; i < n16; ++i) z[i] = R[i * M + m] + lambda * (double)T0[i * M + m];
+            for (int64_t i = 0; i < n16; ++i) {          /* L z' = z */
+                double v = z[i];
+                for (int64_t k = 0; k < i; ++k) v -= L[i * n16 + k] * z[k];
+                z[i] = v / L[i * n16 + i];
+            }
+            for (int64_t i = n16 - 1; i >= 0; --i) {     /* L^T t = z' */
+                double v = z[i];
+                for (int64_t k = i + 1; k < n16; ++k) v -= L[k * n16 + i] * z[k];
+                z[i] = v / L[i * n16 + i];
+            }
+            for (int64_t i = 0; i < n16; ++i) T[i * M + m] = z[i];
+        }
+    }
+    free(H); free(L); free(R); free(z);
+    return rc;
 }

@@ -564,11 +564,146 @@ def check_shared_quantizer(orc, seed=15):
     assert all(np.array_equal(a, b) for a, b in zip(orc.quantize_table_shared(T1), orc.quantize_table(T1)))
 
 
+# ------------------------------------------------------- table fit (Eq. 3)
+def _fit_problem(N, C, M, seed, missing=()):
+    """Seeded indices, targets and prototype table for the fit pins; the
+    buckets listed in `missing` ((c, k) pairs) never occur."""
+    rng = np.random.default_rng(seed)
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    for c, k in missing:
+        col = idx[:, c]
+        col[col == k] = (k + 1) % K
+    Y = rng.standard_normal((N, M)).astype(np.float32)
+    T0 = rng.standard_normal((C, K, M)).astype(np.float32)
+    return idx, Y, T0
+
+
+def _gather(idx, T):
+    """sum_c T[c, idx[:, c], :] in float64 (the product G T without forming G)."""
+    T = np.asarray(T, dtype=np.float64)
+    return sum(T[c][idx[:, c]] for c in range(idx.shape[1]))
+
+
+def _ridge_objective(idx, Y, T, T0, lam):
+    r = Y.astype(np.float64) - _gather(idx, T)
+    d = np.asarray(T, np.float64) - np.asarray(T0, np.float64)
+    return float((r * r).sum() + lam * (d * d).sum())
+
+
+def check_encoder_gram(orc, seed=16):
+    """H = G^T G: block (c, c') is the 16 x 16 contingency table of the
+    indices of codebooks c and c' (numpy.histogram2d), so block (c, c) is
+    diagonal with the bucket counts (numpy.bincount), H is symmetric and sums
+    to N C^2."""
+    rng = np.random.default_rng(seed)
+    N, C = 300, 5
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    idx[:, 3] = np.minimum(idx[:, 3], 9)   # some buckets empty
+    H = orc.encoder_gram(idx)
+    assert H.shape == (C * K, C * K)
+    for c in range(C):
+        for c2 in range(C):
+            ref, _, _ = np.histogram2d(idx[:, c], idx[:, c2], bins=K, range=[[0, K], [0, K]])
+            assert np.array_equal(H[c * K:(c + 1) * K, c2 * K:(c2 + 1) * K], ref.astype(np.int64))
+        assert np.array_equal(np.diag(H[c * K:(c + 1) * K, c * K:(c + 1) * K]), np.bincount(idx[:, c], minlength=K))
+    assert np.array_equal(H, H.T) and H.sum() == N * C * C
+
+
+def check_encoder_scatter(orc, seed=17):
+    """R = G^T Y: row (c, k) is the sum of the target rows whose codebook-c
+    index is k (correctly rounded reference sums, math.fsum); every codebook's
+    block sums to the column totals of Y."""
+    rng = np.random.default_rng(seed)
+    N, C, M = 257, 4, 6
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    Y = (rng.standard_normal((N, M)) * 10).astype(np.float32)
+    R = orc.encoder_scatter(idx, Y)
+    bound = gamma(N, U64) * np.abs(Y.astype(np.float64)).sum(axis=0)
+    for c in range(C):
+        for k in range(K):
+            rows = Y[idx[:, c] == k].astype(np.float64)
+            ref = np.array([math.fsum(rows[:, m]) for m in range(M)])
+            assert np.all(np.abs(R[c * K + k] - ref) <= bound)
+        tot = np.array([math.fsum(Y[:, m].astype(np.float64)) for m in range(M)])
+        assert np.all(np.abs(R[c * K:(c + 1) * K].sum(axis=0) - tot) <= 2 * bound)
+
+
+def check_fit_closed_forms(orc, seed=18):
+    """Eq. 3 with sigma affine (R21) where the minimiser is known in closed
+    form: one codebook decouples into per-bucket ridge means (sum_k Y + lam
+    T0_k) / (n_k + lam); a bucket that never occurs keeps its prototype row;
+    targets that an integer table T* reproduces exactly, with T0 = T*, give
+    T*; and for every lam, ||T - T0|| <= ||G^T (Y - G T0)|| / lam per column
+    (the matrix H + lam I has smallest eigenvalue >= lam)."""
+    rng = np.random.default_rng(seed)
+    # one codebook
+    idx, Y, T0 = _fit_problem(200, 1, 5, seed, missing=[(0, 13)])
+    lam = 3.5
+    T = orc.fit_lut_ridge(idx, Y, T0, lam)
+    for k in range(K):
+        rows = Y[idx[:, 0] == k].astype(np.float64)
+        num = np.array([math.fsum(list(rows[:, m]) + [lam * float(T0[0, k, m])]) for m in range(5)])
+        ref = num / (len(rows) + lam)
+        assert np.allclose(T[0, k], ref, rtol=1e-12, atol=1e-14)
+    assert np.allclose(T[0, 13], T0[0, 13], rtol=1e-14, atol=0)
+    # several codebooks: an empty bucket keeps T0 exactly (up to the solve's rounding)
+    idx, Y, T0 = _fit_problem(400, 6, 4, seed + 1, missing=[(2, 5), (4, 0)])
+    T = orc.fit_lut_ridge(idx, Y, T0, 0.7)
+    assert np.allclose(T[2, 5], T0[2, 5], rtol=1e-13, atol=0) and np.allclose(T[4, 0], T0[4, 0], rtol=1e-13, atol=0)
+    # exact recovery
+    C, M = 5, 3
+    Ts = rng.integers(-8, 9, size=(C, K, M)).astype(np.float32)
+    idx = rng.integers(0, K, size=(300, C)).astype(np.uint8)
+    Yx = _gather(idx, Ts).astype(np.float32)
+    assert np.array_equal(Yx.astype(np.float64), _gather(idx, Ts))   # integer sums: exact in fp32
+    for lam in (1e-3, 1.0, 1e4):
+        T = orc.fit_lut_ridge(idx, Yx, Ts, lam)
+        assert np.abs(T - Ts).max() <= 1e-9
+    # the eigenvalue bound, at weak and strong regularisation
+    idx, Y, T0 = _fit_problem(500, 4, 3, seed + 2)
+    G = np.zeros((500, 4 * K))
+    G[np.arange(500)[:, None], K * np.arange(4)[None, :] + idx] = 1.0
+    resid = G.T @ (Y.astype(np.float64) - _gather(idx, T0))
+    for lam in (0.01, 1.0, 1e3, 1e9):
+        T = orc.fit_lut_ridge(idx, Y, T0, lam)
+        d = (T - T0.astype(np.float64)).reshape(4 * K, 3)
+        assert np.all(np.linalg.norm(d, axis=0) <= np.linalg.norm(resid, axis=0) / lam * (1 + 1e-9))
+
+
+def check_fit_optimality(orc, seed=19):
+    """The fitted table minimises the objective of Eq. 3 (R21) evaluated
+    directly (gather, squared residuals, penalty): at a minimiser of a
+    quadratic, f(T + e E) - f(T) equals e^2 (||G E||^2 + lam ||E||^2) for
+    every direction E (no first-order term), and a generic minimiser
+    (scipy BFGS on a tiny case) agrees."""
+    from scipy.optimize import minimize
+    rng = np.random.default_rng(seed)
+    idx, Y, T0 = _fit_problem(120, 3, 2, seed)
+    lam = 0.4
+    T = orc.fit_lut_ridge(idx, Y, T0, lam)
+    f0 = _ridge_objective(idx, Y, T, T0, lam)
+    for _ in range(6):
+        E = rng.standard_normal(T.shape)
+        for e in (1e-3, 1.0):
+            GE = _gather(idx, E)
+            quad = e * e * (float((GE * GE).sum()) + lam * float((E * E).sum()))
+            df = _ridge_objective(idx, Y, T + e * E, T0, lam) - f0
+            assert abs(df - quad) <= 1e-9 * (f0 + quad) + 1e-12
+    # brute-force minimisation of the same objective on a tiny case
+    idx, Y, T0 = _fit_problem(12, 2, 1, seed + 1)
+    lam = 0.25
+    T = orc.fit_lut_ridge(idx, Y, T0, lam)
+    res = minimize(lambda v: _ridge_objective(idx, Y, v.reshape(2, K, 1), T0, lam), T0.astype(np.float64).ravel(),
+                   method="BFGS", options={"gtol": 1e-10})
+    assert np.abs(res.x.reshape(2, K, 1) - T).max() <= 1e-5
+
+
 ALL_CHECKS = [
     check_encode_brute_force, check_encode_search_tree, check_encode_nan, check_encode_permutation,
     check_encode_golden, check_one_hot_identity, check_decoder_table, check_output_rounding,
     check_scale_linearity, check_f32_order, check_table_build, check_quantizer,
     check_f32_reconstruction, check_quantized_reconstruction, check_rejects_bad_inputs,
     check_sigma_bias_relu, check_sigma_softmax, check_avg_closed_forms, check_avg_bounds,
-    check_shared_quantizer,
+    check_shared_quantizer, check_encoder_gram, check_encoder_scatter, check_fit_closed_forms,
+    check_fit_optimality,
 ]

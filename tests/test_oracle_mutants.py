@@ -47,6 +47,15 @@ MUTANTS = [
     ("code bias not removed", "const int32_t a = P * (u[0] - 128);", "const int32_t a = P * u[0];"),
     ("shared quantizer keeps per-codebook exponents", "return quantize_table_cap(T, C, M, 0, lut, scale, offset);",
      "return quantize_table_cap(T, C, M, oracle_exponent_cap(C), lut, scale, offset);"),
+    ("gram pairs a codebook with itself", "const int64_t s = (int64_t)c2 * ORACLE_K + idx[n * C + c2];",
+     "const int64_t s = (int64_t)c2 * ORACLE_K + idx[n * C + c];"),
+    ("scatter adds column 0", "R[r * M + m] += (double)Y[n * M + m];", "R[r * M + m] += (double)Y[n * M];"),
+    ("ridge term missing from the matrix", "(i == j ? lambda : 0.0)", "(i == j ? 1e-300 : 0.0)"),
+    ("prototype term missing from the right-hand side", "z[i] = R[i * M + m] + lambda * (double)T0[i * M + m];",
+     "z[i] = R[i * M + m];"),
+    ("back substitution with the unfactored upper triangle", "v -= L[k * n16 + i] * z[k];",
+     "v -= L[i * n16 + k] * z[k];"),
+    ("ridge weight doubled in the matrix", "(i == j ? lambda : 0.0)", "(i == j ? 2.0 * lambda : 0.0)"),
 ]
 
 
