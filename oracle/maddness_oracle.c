@@ -37,7 +37,10 @@
  *       targets Y = AB and the prototype table T0 = P0 B given in fp32 and
  *       taken exactly, lambda > 0; the minimiser solves the normal equations
  *       (G^T G + lambda I) T = G^T Y + lambda T0, column by column, in
- *       double.
+ *       double: Cholesky factor L L^T, then forward and backward
+ *       substitution, every multiply-subtract one fused multiply-add, the
+ *       terms of an entry taken k ascending (factor, forward pass) or k
+ *       descending (backward pass).
  *   R19 layer output sigma: z = fl32(y + bias_m); ReLU keeps z when z > 0 and
  *       gives +0 otherwise; softmax is taken over the M outputs of a row.
  *   R20 rounded 8-bit summation: one shared block exponent; biased codes
@@ -466,6 +469,8 @@ int oracle_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C,
  * matrix is symmetric positive definite for lambda > 0; it is factored as
  * L L^T (Cholesky, textbook order: column j from the columns before it) and
  * each of the M columns is solved by forward then backward substitution.
+ * Each multiply-subtract is one fma(); the terms of an entry are taken k
+ * ascending, except in the backward pass (k descending).
  * Returns -1 on bad sizes, -2 when lambda is not a positive finite number.
  */
 int oracle_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
@@ -489,12 +494,12 @@ int oracle_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
                 L[i * n16 + j] = (double)H[i * n16 + j] + (i == j ? lambda : 0.0);
         for (int64_t j = 0; j < n16; ++j) {
             double d = L[j * n16 + j];
-            for (int64_t k = 0; k < j; ++k) d -= L[j * n16 + k] * L[j * n16 + k];
+            for (int64_t k = 0; k < j; ++k) d = fma(-L[j * n16 + k], L[j * n16 + k], d);
             d = sqrt(d);
             L[j * n16 + j] = d;
             for (int64_t i = j + 1; i < n16; ++i) {
                 double v = L[i * n16 + j];
-                for (int64_t k = 0; k < j; ++k) v -= L[i * n16 + k] * L[j * n16 + k];
+                for (int64_t k = 0; k < j; ++k) v = fma(-L[i * n16 + k], L[j * n16 + k], v);
                 L[i * n16 + j] = v / d;
             }
         }
@@ -503,12 +508,12 @@ int oracle_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
             for (int64_t i = 0; i < n16; ++i) z[i] = R[i * M + m] + lambda * (double)T0[i * M + m];
             for (int64_t i = 0; i < n16; ++i) {          /* L z' = z */
                 double v = z[i];
-                for (int64_t k = 0; k < i; ++k) v -= L[i * n16 + k] * z[k];
+                for (int64_t k = 0; k < i; ++k) v = fma(-L[i * n16 + k], z[k], v);
                 z[i] = v / L[i * n16 + i];
             }
             for (int64_t i = n16 - 1; i >= 0; --i) {     /* L^T t = z' */
                 double v = z[i];
-                for (int64_t k = i + 1; k < n16; ++k) v -= L[k * n16 + i] * z[k];
+                for (int64_t k = n16 - 1; k > i; --k) v = fma(-L[k * n16 + i], z[k], v);
                 z[i] = v / L[i * n16 + i];
             }
             for (int64_t i = 0; i < n16; ++i) T[i * M + m] = z[i];

@@ -53,8 +53,8 @@ MUTANTS = [
     ("ridge term missing from the matrix", "(i == j ? lambda : 0.0)", "(i == j ? 1e-300 : 0.0)"),
     ("prototype term missing from the right-hand side", "z[i] = R[i * M + m] + lambda * (double)T0[i * M + m];",
      "z[i] = R[i * M + m];"),
-    ("back substitution with the unfactored upper triangle", "v -= L[k * n16 + i] * z[k];",
-     "v -= L[i * n16 + k] * z[k];"),
+    ("back substitution with the unfactored upper triangle", "v = fma(-L[k * n16 + i], z[k], v);",
+     "v = fma(-L[i * n16 + k], z[k], v);"),
     ("ridge weight doubled in the matrix", "(i == j ? lambda : 0.0)", "(i == j ? 2.0 * lambda : 0.0)"),
 ]
 
