@@ -232,6 +232,56 @@ int maddness_build_lut_shared(const float* P, const float* B, int32_t C,
 int maddness_build_lut_f32(const float* P, const float* B, int32_t C,
                            int32_t D, int32_t M, float* lut_out, void* stream);
 
+/*
+ * 8-bit block floating point quantization (§1; the quantizer of
+ * maddness_build_lut) of a given table T [C][16][M] (double, device), e.g. a
+ * fitted one.  shared != 0 gives every codebook the same exponent (as
+ * maddness_build_lut_shared).  EINVAL / EUNSUPPORTED as for
+ * maddness_build_lut; T must be 8-byte aligned.
+ */
+int maddness_quantize_lut(const double* T, int32_t C, int32_t M, int32_t shared,
+                          int8_t* lut_out, float* scale_out, float* offset_out,
+                          void* stream);
+
+/*
+ * Model-aware table fit (§2.2, Eq. 3) with an affine layer output, where the
+ * bias cancels: the table T [C][16][M] minimising
+ *     sum_n || Y[n] - sum_c T[c][idx[n][c]] ||^2 + lambda || T - T0 ||^2
+ * over training rows n, Y = AB the layer's exact outputs [N][M] (fp32),
+ * idx [N][C] their encoder indices, T0 = P0 B the prototype table (fp32,
+ * [C][16][M]).  With G the one-hot encoder output (G[n][16c + k] = 1 iff
+ * idx[n][c] = k) the minimiser solves (G^T G + lambda I) T = G^T Y +
+ * lambda T0; it is computed in double (T_out, [C][16][M], 8-byte aligned) by
+ * a Cholesky factorisation and forward / backward substitution whose every
+ * multiply-subtract is one fused multiply-add, terms of an entry taken k
+ * ascending (factor, forward pass) or descending (backward pass).
+ * workspace: device memory of at least maddness_fit_lut_workspace_bytes(C)
+ * bytes, 256-byte aligned, caller-owned, contents undefined on return.
+ * lambda must be positive and finite (EINVAL).  C > 256 or N >= 2^31 gives
+ * EUNSUPPORTED.  Quantize the result with maddness_quantize_lut, or round it
+ * to fp32 for the unquantized mode.
+ */
+int64_t maddness_fit_lut_workspace_bytes(int32_t C);   /* -1 if C is out of range */
+int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
+                           const float* Y, int32_t M, const float* T0,
+                           double lambda, double* T_out, void* workspace,
+                           int64_t workspace_bytes, void* stream);
+
+/*
+ * The two sums the normal equations of Eq. 3 are built from:
+ * maddness_encoder_gram: H = G^T G [16C][16C] as int32 counts
+ *   (H[16c + k][16c' + k'] = number of rows with idx[n][c] = k and
+ *   idx[n][c'] = k'); exact.
+ * maddness_encoder_scatter: R = G^T Y [16C][M] in double, each entry the sum
+ *   of its rows in ascending row order.
+ * C > 256 (or N >= 2^31 for the counts) gives EUNSUPPORTED.
+ */
+int maddness_encoder_gram(const uint8_t* idx, int64_t N, int32_t C,
+                          int32_t* gram_out, void* stream);
+int maddness_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C,
+                             const float* Y, int32_t M, double* out,
+                             void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -422,3 +422,78 @@ def prepare_matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, ac
             _ptr(offset), M, _ptr(y_out), _ptr(acc_out), _ptr(idx_out), _stream(stream))
     keep = (A, split_dims, thresholds, lut, scale, offset, y_out, acc_out, idx_out)
     return PreparedCall("maddness_matmul", args, keep, (y_out, acc_out, idx_out))
+
+
+def quantize_lut(T, shared=False, stream=None):
+    """8-bit block floating point quantization of a given float64 table
+    [C,16,M] (e.g. a fitted one); returns (lut, scale, offset)."""
+    _need(T, "T", torch.float64, 3)
+    _dense(T, "T")
+    C, k, M = T.shape
+    if k != K:
+        raise ValueError("T must be [C,16,M]")
+    lut = torch.empty((C, K, M), dtype=torch.int8, device=T.device)
+    scale = torch.empty((C,), dtype=torch.float32, device=T.device)
+    offset = torch.empty((C,), dtype=torch.float32, device=T.device)
+    st = _lib.lib().maddness_quantize_lut(_ptr(T), C, M, 1 if shared else 0, _ptr(lut), _ptr(scale), _ptr(offset),
+                                          _stream(stream))
+    _lib.check("maddness_quantize_lut", st)
+    return lut, scale, offset
+
+
+def _fit_inputs(idx, Y):
+    _need(idx, "idx", torch.uint8, 2)
+    _dense(idx, "idx")
+    _need(Y, "Y", torch.float32, 2)
+    _dense(Y, "Y")
+    if Y.shape[0] != idx.shape[0]:
+        raise ValueError("Y must have one row per index row")
+    return idx.shape[0], idx.shape[1], Y.shape[1]
+
+
+def encoder_gram(idx, stream=None):
+    """H = G^T G of the one-hot encoder output: int32 [16C, 16C] counts."""
+    _need(idx, "idx", torch.uint8, 2)
+    _dense(idx, "idx")
+    N, C = idx.shape
+    H = torch.empty((C * K, C * K), dtype=torch.int32, device=idx.device)
+    st = _lib.lib().maddness_encoder_gram(_ptr(idx), N, C, _ptr(H), _stream(stream))
+    _lib.check("maddness_encoder_gram", st)
+    return H
+
+
+def encoder_scatter(idx, Y, stream=None):
+    """R = G^T Y: float64 [16C, M], each entry summed over its rows in order."""
+    N, C, M = _fit_inputs(idx, Y)
+    R = torch.empty((C * K, M), dtype=torch.float64, device=idx.device)
+    st = _lib.lib().maddness_encoder_scatter(_ptr(idx), N, C, _ptr(Y), M, _ptr(R), _stream(stream))
+    _lib.check("maddness_encoder_scatter", st)
+    return R
+
+
+def fit_lut_ridge(idx, Y, T0, lam, workspace=None, stream=None):
+    """Model-aware table fit (Eq. 3, affine output): the float64 table
+    [C,16,M] minimising ||Y - G T||^2 + lam ||T - T0||^2.  ``workspace``: an
+    optional preallocated uint8 device tensor of at least
+    fit_lut_workspace_bytes(C) bytes."""
+    N, C, M = _fit_inputs(idx, Y)
+    _need(T0, "T0", torch.float32, 3)
+    _dense(T0, "T0")
+    if tuple(T0.shape) != (C, K, M):
+        raise ValueError("T0 must be [C,16,M]")
+    need = int(_lib.lib().maddness_fit_lut_workspace_bytes(C))
+    if need < 0:
+        _lib.check("maddness_fit_lut_ridge", _lib.EUNSUPPORTED)
+    if workspace is None:
+        workspace = torch.empty((need + 256,), dtype=torch.uint8, device=idx.device)
+        if stream is not None:
+            workspace.record_stream(stream)   # freed only after the work queued on `stream`
+    base = workspace.data_ptr()
+    off = (-base) % 256
+    if workspace.numel() - off < need:
+        raise ValueError(f"workspace must hold {need} bytes at a 256-byte aligned address")
+    T = torch.empty((C, K, M), dtype=torch.float64, device=idx.device)
+    st = _lib.lib().maddness_fit_lut_ridge(_ptr(idx), N, C, _ptr(Y), M, _ptr(T0), float(lam), _ptr(T),
+                                           ctypes.c_void_p(base + off), need, _stream(stream))
+    _lib.check("maddness_fit_lut_ridge", st)
+    return T

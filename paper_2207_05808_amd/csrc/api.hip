@@ -4,6 +4,7 @@
 #include "internal.hpp"
 
 #include <stdint.h>
+#include <cmath>
 
 namespace mdn {
 namespace {
@@ -12,6 +13,7 @@ constexpr int kPFs[] = {1, 2, 4, 8, 9, 16};  // instantiated prefetch depths
 
 bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0; }
 int round_up(int v, int m) { return (v + m - 1) / m * m; }
+int64_t round_up64(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 int ilog2(int v) { int r = 0; while ((1 << r) < v) ++r; return r; }
 
 int pick_pf(int units) {  // smallest instantiated depth holding `units` 16-byte units per wavefront
@@ -603,6 +605,57 @@ int maddness_build_lut_shared(const float* P, const float* B, int32_t C, int32_t
     return MADDNESS_EINVAL;
   if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
   return status_from(launch_build_lut(P, B, C, D, M, lut_out, scale_out, offset_out, 0,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int maddness_quantize_lut(const double* T, int32_t C, int32_t M, int32_t shared, int8_t* lut_out,
+                          float* scale_out, float* offset_out, void* stream) {
+  if (C <= 0 || M <= 0 || !T || !lut_out || !scale_out || !offset_out) return MADDNESS_EINVAL;
+  if (!aligned(T, 8) || !aligned(scale_out, 4) || !aligned(offset_out, 4)) return MADDNESS_EINVAL;
+  if (127.0 * C >= 16777216.0) return MADDNESS_EINVAL;
+  if (C > kMaxC) return MADDNESS_EUNSUPPORTED;
+  int cap = 0;
+  if (!shared)
+    while (127.0 * C * (double)(1ll << (cap + 1)) < 16777216.0) ++cap;
+  return status_from(launch_quantize_lut(T, C, M, lut_out, scale_out, offset_out, cap,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+int maddness_encoder_gram(const uint8_t* idx, int64_t N, int32_t C, int32_t* gram_out, void* stream) {
+  if (N < 0 || C <= 0 || !gram_out || (N > 0 && !idx)) return MADDNESS_EINVAL;
+  if (!aligned(gram_out, 4)) return MADDNESS_EINVAL;
+  if (C > kMaxFitC || N >= (1ll << 31)) return MADDNESS_EUNSUPPORTED;   // int32 counts
+  return status_from(launch_gram(idx, N, C, gram_out, device_cus(), static_cast<hipStream_t>(stream)));
+}
+
+int maddness_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M, double* out,
+                             void* stream) {
+  if (N < 0 || C <= 0 || M <= 0 || !out || (N > 0 && (!idx || !Y))) return MADDNESS_EINVAL;
+  if (!aligned(out, 8) || (N > 0 && !aligned(Y, 4))) return MADDNESS_EINVAL;
+  if (C > kMaxFitC) return MADDNESS_EUNSUPPORTED;
+  return status_from(launch_scatter(idx, N, C, Y, M, out, static_cast<hipStream_t>(stream)));
+}
+
+int64_t maddness_fit_lut_workspace_bytes(int32_t C) {
+  if (C <= 0 || C > kMaxFitC) return -1;
+  const int64_t n = (int64_t)C * kK;
+  return round_up64(n * n * 4, 256) + n * n * 8;
+}
+
+int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M, const float* T0,
+                           double lambda, double* T_out, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (N < 0 || C <= 0 || M <= 0 || !T0 || !T_out || !workspace || (N > 0 && (!idx || !Y)))
+    return MADDNESS_EINVAL;
+  if (!(lambda > 0.0) || !std::isfinite(lambda)) return MADDNESS_EINVAL;
+  if (!aligned(T_out, 8) || !aligned(T0, 4) || !aligned(workspace, 256) || (N > 0 && !aligned(Y, 4)))
+    return MADDNESS_EINVAL;
+  if (C > kMaxFitC || N >= (1ll << 31)) return MADDNESS_EUNSUPPORTED;
+  const int64_t need = maddness_fit_lut_workspace_bytes(C);
+  if (workspace_bytes < need) return MADDNESS_EINVAL;
+  const int64_t n = (int64_t)C * kK;
+  int32_t* H = static_cast<int32_t*>(workspace);
+  double* A = reinterpret_cast<double*>(static_cast<char*>(workspace) + round_up64(n * n * 4, 256));
+  return status_from(launch_fit_ridge(idx, N, C, Y, M, T0, lambda, T_out, H, A, device_cus(),
                                       static_cast<hipStream_t>(stream)));
 }
 

@@ -10,6 +10,7 @@ constexpr int kK = 16;       // prototypes per codebook
 constexpr int kLevels = 4;   // tree depth
 constexpr int kNodes = 15;   // thresholds per codebook (heap order)
 constexpr int kMaxC = 512;   // codebooks supported by one launch
+constexpr int kMaxFitC = 256; // codebooks of the table fit (16 C <= 4096 unknowns per column)
 constexpr int kLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
 
 enum Mode : int { kEncode = 0, kAccum = 1, kFused = 2 };
@@ -139,5 +140,14 @@ hipError_t launch_build_lut(const float* P, const float* B, int C, int D, int M,
                             hipStream_t stream);
 hipError_t launch_build_lut_f32(const float* P, const float* B, int C, int D, int M,
                                 float* lut, hipStream_t stream);
+hipError_t launch_quantize_lut(const double* T, int C, int M, int8_t* lut, float* scale, float* offset,
+                               int cap, hipStream_t stream);
+
+// Model-aware table fit (Eq. 3, affine output); see lut_fit.hip.
+hipError_t launch_gram(const uint8_t* idx, int64_t N, int C, int32_t* H, int cus, hipStream_t stream);
+hipError_t launch_scatter(const uint8_t* idx, int64_t N, int C, const float* Y, int M, double* R,
+                          hipStream_t stream);
+hipError_t launch_fit_ridge(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* T0,
+                            double lam, double* T, int32_t* H, double* A, int cus, hipStream_t stream);
 
 }  // namespace mdn

@@ -27,6 +27,20 @@ __device__ __forceinline__ double table_entry(const float* __restrict__ P, const
   return s;
 }
 
+// where the quantizer's entries come from: T = P B computed on the fly, or a
+// given double table (a fitted one)
+struct SrcPB {
+  const float* P;
+  const float* B;
+  int D, M;
+  __device__ double at(int64_t row, int m) const { return table_entry(P, B, D, M, row, m); }
+};
+struct SrcT {
+  const double* T;
+  int M;
+  __device__ double at(int64_t row, int m) const { return T[row * M + m]; }
+};
+
 __device__ double block_reduce(double v, bool take_max, double* s_red) {
   const int tid = threadIdx.x;
   s_red[tid] = v;
@@ -43,16 +57,16 @@ __device__ double block_reduce(double v, bool take_max, double* s_red) {
   return r;
 }
 
+template <class Src>
 __global__ void __launch_bounds__(kBuildThreads)
-table_stats_kernel(const float* __restrict__ P, const float* __restrict__ B, int D, int M,
-                   float* __restrict__ scale_out, float* __restrict__ offset_out) {
+table_stats_kernel(const Src src, int M, float* __restrict__ scale_out, float* __restrict__ offset_out) {
   __shared__ double s_red[kBuildThreads];
   const int c = blockIdx.x;
   const int per = kK * M;
   double lo = __builtin_inf(), hi = -__builtin_inf();
   for (int e = threadIdx.x; e < per; e += kBuildThreads) {
     const int k = e / M, m = e - k * M;
-    const double t = table_entry(P, B, D, M, (int64_t)c * kK + k, m);
+    const double t = src.at((int64_t)c * kK + k, m);
     lo = fmin(lo, t);
     hi = fmax(hi, t);
   }
@@ -62,7 +76,7 @@ table_stats_kernel(const float* __restrict__ P, const float* __restrict__ B, int
   double r = 0.0;
   for (int e = threadIdx.x; e < per; e += kBuildThreads) {
     const int k = e / M, m = e - k * M;
-    const double t = table_entry(P, B, D, M, (int64_t)c * kK + k, m);
+    const double t = src.at((int64_t)c * kK + k, m);
     r = fmax(r, fabs(__dsub_rn(t, (double)o)));
   }
   r = block_reduce(r, true, s_red);
@@ -83,10 +97,10 @@ __device__ int max_parked_exponent(const float* __restrict__ scale_out, int C, i
   return *s_max;
 }
 
+template <class Src>
 __global__ void __launch_bounds__(kBuildThreads)
-table_codes_kernel(const float* __restrict__ P, const float* __restrict__ B, int C, int D, int M,
-                   int cap, const float* __restrict__ scale_out, const float* __restrict__ offset_out,
-                   int8_t* __restrict__ lut) {
+table_codes_kernel(const Src src, int C, int M, int cap, const float* __restrict__ scale_out,
+                   const float* __restrict__ offset_out, int8_t* __restrict__ lut) {
   __shared__ int s_max;
   const int emax = max_parked_exponent(scale_out, C, &s_max);
   const int64_t total = (int64_t)C * kK * M;
@@ -96,7 +110,7 @@ table_codes_kernel(const float* __restrict__ P, const float* __restrict__ B, int
     const int m = (int)(e - row * M);
     const int c = (int)(row / kK);
     const int ex = max(reinterpret_cast<const int*>(scale_out)[c], emax - cap);
-    const double t = table_entry(P, B, D, M, row, m);
+    const double t = src.at(row, m);
     const double q = rint(__dmul_rn(__dsub_rn(t, (double)offset_out[c]), __builtin_ldexp(1.0, -ex)));
     lut[e] = (int8_t)(int)fmin(127.0, fmax(-127.0, q));
   }
@@ -135,19 +149,29 @@ static unsigned grid_for(int64_t total) {
   return (unsigned)(g < 65536 ? (g > 0 ? g : 1) : 65536);
 }
 
-hipError_t launch_build_lut(const float* P, const float* B, int C, int D, int M, int8_t* lut,
-                            float* scale, float* offset, int cap, hipStream_t stream) {
-  hipLaunchKernelGGL(table_stats_kernel, dim3(C), dim3(kBuildThreads), 0, stream, P, B, D, M, scale,
-                     offset);
+template <class Src>
+static hipError_t quantize(const Src& src, int C, int M, int8_t* lut, float* scale, float* offset, int cap,
+                           hipStream_t stream) {
+  hipLaunchKernelGGL(table_stats_kernel<Src>, dim3(C), dim3(kBuildThreads), 0, stream, src, M, scale, offset);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(table_codes_kernel, dim3(grid_for((int64_t)C * kK * M)), dim3(kBuildThreads), 0,
-                     stream, P, B, C, D, M, cap, scale, offset, lut);
+  hipLaunchKernelGGL(table_codes_kernel<Src>, dim3(grid_for((int64_t)C * kK * M)), dim3(kBuildThreads), 0,
+                     stream, src, C, M, cap, scale, offset, lut);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // C <= 4 * 256 codebooks per single-workgroup scale pass
   hipLaunchKernelGGL(table_scale_kernel, dim3(1), dim3(256), 0, stream, scale, C, cap);
   return hipGetLastError();
+}
+
+hipError_t launch_build_lut(const float* P, const float* B, int C, int D, int M, int8_t* lut,
+                            float* scale, float* offset, int cap, hipStream_t stream) {
+  return quantize(SrcPB{P, B, D, M}, C, M, lut, scale, offset, cap, stream);
+}
+
+hipError_t launch_quantize_lut(const double* T, int C, int M, int8_t* lut, float* scale, float* offset, int cap,
+                               hipStream_t stream) {
+  return quantize(SrcT{T, M}, C, M, lut, scale, offset, cap, stream);
 }
 
 hipError_t launch_build_lut_f32(const float* P, const float* B, int C, int D, int M, float* lut,

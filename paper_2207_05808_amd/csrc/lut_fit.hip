@@ -1,0 +1,396 @@
+// Model-aware table fit, Eq. 3 of McCarter & Dronen (§2.2), with an affine
+// layer output (bias and identity, which cancel): the table T minimising
+// ||Y - G T||^2 + lambda ||T - T0||^2 solves the normal equations
+//     (G^T G + lambda I) T = G^T Y + lambda T0,
+// G the one-hot encoder output (G[n][16c + k] = 1 iff idx[n][c] = k), Y = AB
+// the layer's exact outputs on training rows and T0 = P0 B the prototype
+// table.  Offline: it turns training data into a table for the hot path.
+//
+// Steps (each its own launch family):
+//   gram    H = G^T G, integer counts: H[16c + k][16c' + k'] is the number of
+//           rows whose codebook-c index is k and codebook-c' index is k'.
+//           Workgroups own an 8 x 8 block of codebook pairs and a row chunk,
+//           count in LDS, then add their nonzero counts to H (integer
+//           atomics: the result does not depend on their order).
+//   scatter R = G^T Y in double, one wavefront per (codebook, 64 columns),
+//           lane = column, rows in ascending order: every entry is the sum
+//           of its rows in the order they come.
+//   solve   A = H + lambda I (double), B = R + lambda T0; A = L L^T by a
+//           blocked right-looking Cholesky factorisation (panels of 32:
+//           diagonal block in one workgroup, the rows below it, then the
+//           trailing update), then blocked forward and backward substitution
+//           over the M columns of B, in place.
+// Every multiply-subtract is one fused multiply-add, and every entry takes
+// its terms in the same order as the unblocked algorithm (k ascending in the
+// factor and forward pass, descending in the backward pass), so the result
+// does not depend on the blocking.
+#include "internal.hpp"
+
+#include <climits>
+
+namespace mdn {
+
+namespace {
+
+constexpr int kNB = 32;        // panel / block width of the factorisation and the solves
+constexpr int kGB = 8;         // codebooks per side of a Gram pair block
+constexpr int kGW = kGB * kK;  // 128: counts per side of a pair block
+
+__global__ void __launch_bounds__(256) fill_i32_kernel(int32_t* __restrict__ p, int64_t n) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) p[e] = 0;
+}
+
+// ------------------------------------------------------------------ gram
+__global__ void __launch_bounds__(256)
+gram_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, int nbc, int64_t chunk_rows,
+            int32_t* __restrict__ H) {
+  __shared__ int s_cnt[kGW * kGW];   // 64 KB
+  const int tid = threadIdx.x;
+  const int npair = nbc * nbc;
+  const int pair = blockIdx.x % npair;
+  const int64_t chunk = blockIdx.x / npair;
+  const int c1 = (pair / nbc) * kGB, c2 = (pair % nbc) * kGB;
+  const int n1 = min(kGB, C - c1), n2 = min(kGB, C - c2);
+  for (int e = tid; e < kGW * kGW; e += 256) s_cnt[e] = 0;
+  __syncthreads();
+  const int64_t r0 = chunk * chunk_rows;
+  const int64_t r1 = min(N, r0 + chunk_rows);
+  for (int64_t n = r0 + tid; n < r1; n += 256) {
+    const uint8_t* ir = idx + n * C;
+    int ka[kGB], kb[kGB];
+#pragma unroll
+    for (int a = 0; a < kGB; ++a) ka[a] = a < n1 ? (int)(ir[c1 + a] & 15) : 0;
+#pragma unroll
+    for (int b = 0; b < kGB; ++b) kb[b] = b < n2 ? (int)(ir[c2 + b] & 15) : 0;
+#pragma unroll
+    for (int a = 0; a < kGB; ++a)
+#pragma unroll
+      for (int b = 0; b < kGB; ++b)
+        if (a < n1 && b < n2) atomicAdd(&s_cnt[(a * kK + ka[a]) * kGW + b * kK + kb[b]], 1);
+  }
+  __syncthreads();
+  const int64_t n16 = (int64_t)C * kK;
+  for (int e = tid; e < kGW * kGW; e += 256) {
+    const int v = s_cnt[e];
+    const int ra = e / kGW, rb = e % kGW;
+    if (v != 0 && ra < n1 * kK && rb < n2 * kK) atomicAdd(&H[(c1 * kK + ra) * n16 + c2 * kK + rb], v);
+  }
+}
+
+// --------------------------------------------------------------- scatter
+// R[16c + k][m] = sum over rows n (ascending) with idx[n][c] = k of Y[n][m].
+// One wavefront per (codebook, 64-column tile); the row's index is uniform
+// across the wavefront, so the sum it feeds is chosen by a scalar branch.
+constexpr int kSR = 8;   // rows loaded ahead
+
+__global__ void __launch_bounds__(64)
+scatter_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, const float* __restrict__ Y, int M,
+               double* __restrict__ R) {
+  const int lane = threadIdx.x;
+  const int ntile = (M + 63) / 64;
+  const int c = blockIdx.x / ntile;
+  const int m = (blockIdx.x % ntile) * 64 + lane;
+  const bool ok = m < M;
+  double acc[kK];
+#pragma unroll
+  for (int k = 0; k < kK; ++k) acc[k] = 0.0;
+  for (int64_t n0 = 0; n0 < N; n0 += kSR) {
+    int kr[kSR];
+    double v[kSR];
+#pragma unroll
+    for (int j = 0; j < kSR; ++j) {
+      const int64_t n = n0 + j;
+      kr[j] = n < N ? (int)idx[n * C + c] : -1;
+      v[j] = (n < N && ok) ? (double)Y[n * M + m] : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < kSR; ++j) {
+      switch (__builtin_amdgcn_readfirstlane(kr[j])) {   // every lane holds the same value
+#define MDN_SCATTER_CASE(q) case q: acc[q] = __dadd_rn(acc[q], v[j]); break;
+        MDN_SCATTER_CASE(0) MDN_SCATTER_CASE(1) MDN_SCATTER_CASE(2) MDN_SCATTER_CASE(3)
+        MDN_SCATTER_CASE(4) MDN_SCATTER_CASE(5) MDN_SCATTER_CASE(6) MDN_SCATTER_CASE(7)
+        MDN_SCATTER_CASE(8) MDN_SCATTER_CASE(9) MDN_SCATTER_CASE(10) MDN_SCATTER_CASE(11)
+        MDN_SCATTER_CASE(12) MDN_SCATTER_CASE(13) MDN_SCATTER_CASE(14) MDN_SCATTER_CASE(15)
+#undef MDN_SCATTER_CASE
+        default: break;   // rows past N
+      }
+    }
+  }
+  if (ok)
+#pragma unroll
+    for (int k = 0; k < kK; ++k) R[((int64_t)c * kK + k) * M + m] = acc[k];
+}
+
+// -------------------------------------------------------------- assemble
+// A = H + lambda I (lower triangle and diagonal; the strict upper triangle
+// is never read), B = R + lambda T0 (in place in B).
+__global__ void __launch_bounds__(256)
+assemble_kernel(const int32_t* __restrict__ H, int64_t n, double lam, double* __restrict__ A,
+                double* __restrict__ B, const float* __restrict__ T0, int64_t nb_total) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n * n; e += stride) {
+    const int64_t i = e / n, j = e - (e / n) * n;
+    if (j <= i) A[e] = (double)H[e] + (i == j ? lam : 0.0);
+  }
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < nb_total; e += stride)
+    B[e] = __dadd_rn(B[e], __dmul_rn(lam, (double)T0[e]));
+}
+
+// ---------------------------------------------------------- factorisation
+// diagonal block [j0, j0 + jb) of the panel: unblocked right-looking in LDS
+__global__ void __launch_bounds__(256) potrf_diag_kernel(double* __restrict__ A, int64_t n, int j0, int jb) {
+  __shared__ double a[kNB][kNB + 1];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int i = e / kNB, j = e % kNB;
+    a[i][j] = (i < jb && j <= i) ? A[(j0 + i) * n + j0 + j] : 0.0;
+  }
+  __syncthreads();
+  for (int j = 0; j < jb; ++j) {
+    if (tid == 0) a[j][j] = __dsqrt_rn(a[j][j]);
+    __syncthreads();
+    const double d = a[j][j];
+    for (int i = j + 1 + tid; i < jb; i += 256) a[i][j] = __ddiv_rn(a[i][j], d);
+    __syncthreads();
+    // update of the columns right of j: entry (i, q), j < q <= i, term k = j
+    for (int e = tid; e < kNB * kNB; e += 256) {
+      const int i = e / kNB, q = e % kNB;
+      if (q > j && q <= i && i < jb) a[i][q] = __fma_rn(-a[i][j], a[q][j], a[i][q]);
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int i = e / kNB, j = e % kNB;
+    if (i < jb && j <= i) A[(j0 + i) * n + j0 + j] = a[i][j];
+  }
+}
+
+// rows [j0 + jb, n) of the panel: L21 = A21 L11^-T, one row per thread
+__global__ void __launch_bounds__(256) trsm_panel_kernel(double* __restrict__ A, int64_t n, int j0, int jb) {
+  __shared__ double l[kNB][kNB + 1];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int i = e / kNB, j = e % kNB;
+    l[i][j] = (i < jb && j <= i) ? A[(j0 + i) * n + j0 + j] : 0.0;
+  }
+  __syncthreads();
+  const int64_t row = (int64_t)j0 + jb + (int64_t)blockIdx.x * 256 + tid;
+  if (row >= n) return;
+  double* ar = A + row * n + j0;
+  double x[kNB];
+#pragma unroll
+  for (int j = 0; j < kNB; ++j) x[j] = j < jb ? ar[j] : 0.0;
+#pragma unroll
+  for (int j = 0; j < kNB; ++j) {
+    if (j < jb) {
+      x[j] = __ddiv_rn(x[j], l[j][j]);
+#pragma unroll
+      for (int q = j + 1; q < kNB; ++q) x[q] = __fma_rn(-x[j], l[q][j], x[q]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kNB; ++j)
+    if (j < jb) ar[j] = x[j];
+}
+
+// trailing update: A[i][q] -= sum_{k in panel, ascending} L[i][k] L[q][k] for
+// j0 + jb <= q <= i < n; a 32 x 32 tile per workgroup (lower tiles only)
+__global__ void __launch_bounds__(256) syrk_kernel(double* __restrict__ A, int64_t n, int j0, int jb) {
+  __shared__ double li[kNB][kNB + 1];
+  __shared__ double lq[kNB][kNB + 1];
+  const int tid = threadIdx.x;
+  // tile (ti, tq), ti >= tq, from the linear block index
+  int ti = 0;
+  const int b = blockIdx.x;
+  while ((ti + 1) * (ti + 2) / 2 <= b) ++ti;
+  const int tq = b - ti * (ti + 1) / 2;
+  const int64_t s = (int64_t)j0 + jb;
+  const int64_t i0 = s + (int64_t)ti * kNB, q0 = s + (int64_t)tq * kNB;
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int r = e / kNB, k = e % kNB;
+    li[r][k] = (i0 + r < n && k < jb) ? A[(i0 + r) * n + j0 + k] : 0.0;
+    lq[r][k] = (q0 + r < n && k < jb) ? A[(q0 + r) * n + j0 + k] : 0.0;
+  }
+  __syncthreads();
+  const int ty = tid / 16, tx = tid % 16;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int r = ty + 16 * a, q = tx + 16 * c;
+      const int64_t gi = i0 + r, gq = q0 + q;
+      if (gi < n && gq <= gi) {
+        double v = A[gi * n + gq];
+        for (int k = 0; k < jb; ++k) v = __fma_rn(-li[r][k], lq[q][k], v);
+        A[gi * n + gq] = v;
+      }
+    }
+}
+
+// ------------------------------------------------------------------ solves
+// B [n][M] in place.  Forward: z_i = (b_i - sum_{k < i} L[i][k] z_k) / L[i][i],
+// k ascending; backward: t_i = (z_i - sum_{k > i} L[k][i] t_k) / L[i][i], k
+// descending.  Blocks of 32 rows; the diagonal block one column per thread,
+// the update of the other rows as 32 x 64 tiles.
+template <bool FWD>
+__global__ void __launch_bounds__(256) trsv_diag_kernel(const double* __restrict__ A, int64_t n, double* __restrict__ B,
+                                                         int M, int i0, int ib) {
+  __shared__ double l[kNB][kNB + 1];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int i = e / kNB, j = e % kNB;
+    l[i][j] = (i < ib && j <= i) ? A[(i0 + i) * n + i0 + j] : 0.0;
+  }
+  __syncthreads();
+  const int64_t m = (int64_t)blockIdx.x * 256 + tid;
+  if (m >= M) return;
+  double x[kNB];
+#pragma unroll
+  for (int i = 0; i < kNB; ++i) x[i] = i < ib ? B[(i0 + i) * (int64_t)M + m] : 0.0;
+  if (FWD) {
+#pragma unroll
+    for (int i = 0; i < kNB; ++i) {
+      if (i < ib) {
+        x[i] = __ddiv_rn(x[i], l[i][i]);
+#pragma unroll
+        for (int q = i + 1; q < kNB; ++q) x[q] = __fma_rn(-l[q][i], x[i], x[q]);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = kNB - 1; i >= 0; --i) {
+      if (i < ib) {
+        x[i] = __ddiv_rn(x[i], l[i][i]);
+#pragma unroll
+        for (int q = 0; q < i; ++q) x[q] = __fma_rn(-l[i][q], x[i], x[q]);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kNB; ++i)
+    if (i < ib) B[(i0 + i) * (int64_t)M + m] = x[i];
+}
+
+// FWD: rows r >= i0 + ib get the block's terms, k ascending: b_r -= L[r][k] z_k.
+// !FWD: rows r < i0 get them, k descending: b_r -= L[k][r] t_k.
+template <bool FWD>
+__global__ void __launch_bounds__(256) trsv_update_kernel(const double* __restrict__ A, int64_t n, double* __restrict__ B,
+                                                           int M, int i0, int ib) {
+  __shared__ double lr[kNB][kNB + 1];   // lr[r][k]: the coefficient of block row k in row r
+  __shared__ double z[kNB][64];
+  const int tid = threadIdx.x;
+  const int ntm = (M + 63) / 64;
+  const int64_t r0 = FWD ? (int64_t)i0 + ib + (int64_t)(blockIdx.x / ntm) * kNB : (int64_t)(blockIdx.x / ntm) * kNB;
+  const int64_t rend = FWD ? n : i0;
+  const int64_t m0 = (int64_t)(blockIdx.x % ntm) * 64;
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int r = e / kNB, k = e % kNB;
+    const int64_t gr = r0 + r;
+    double v = 0.0;
+    if (gr < rend && k < ib) v = FWD ? A[gr * n + i0 + k] : A[(i0 + k) * n + gr];
+    lr[r][k] = v;
+  }
+  for (int e = tid; e < kNB * 64; e += 256) {
+    const int k = e / 64, c = e % 64;
+    z[k][c] = (k < ib && m0 + c < M) ? B[(i0 + k) * (int64_t)M + m0 + c] : 0.0;
+  }
+  __syncthreads();
+  const int c = tid % 64;
+  const int rr = tid / 64;   // rows rr, rr + 4, ..., 8 per thread
+  if (m0 + c >= M) return;
+#pragma unroll
+  for (int a = 0; a < kNB / 4; ++a) {
+    const int r = rr + 4 * a;
+    const int64_t gr = r0 + r;
+    if (gr >= rend) continue;
+    double v = B[gr * (int64_t)M + m0 + c];
+    if (FWD) {
+      for (int k = 0; k < ib; ++k) v = __fma_rn(-lr[r][k], z[k][c], v);
+    } else {
+      for (int k = ib - 1; k >= 0; --k) v = __fma_rn(-lr[r][k], z[k][c], v);
+    }
+    B[gr * (int64_t)M + m0 + c] = v;
+  }
+}
+
+unsigned grid_1d(int64_t total, int per) {
+  int64_t g = (total + per - 1) / per;
+  if (g < 1) g = 1;
+  if (g > 65536) g = 65536;
+  return (unsigned)g;
+}
+
+}  // namespace
+
+hipError_t launch_gram(const uint8_t* idx, int64_t N, int C, int32_t* H, int cus, hipStream_t stream) {
+  const int64_t n16 = (int64_t)C * kK;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_1d(n16 * n16, 256)), dim3(256), 0, stream, H, n16 * n16);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || N == 0) return e;
+  const int nbc = (C + kGB - 1) / kGB;
+  const int64_t npair = (int64_t)nbc * nbc;
+  // about four workgroups per CU in all, chunks of at least 256 rows
+  int64_t chunks = ((int64_t)4 * cus + npair - 1) / npair;
+  const int64_t max_chunks = (N + 255) / 256;
+  if (chunks > max_chunks) chunks = max_chunks;
+  if (chunks < 1) chunks = 1;
+  const int64_t chunk_rows = (N + chunks - 1) / chunks;
+  chunks = (N + chunk_rows - 1) / chunk_rows;
+  hipLaunchKernelGGL(gram_kernel, dim3((unsigned)(npair * chunks)), dim3(256), 0, stream, idx, N, C, nbc,
+                     chunk_rows, H);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(const uint8_t* idx, int64_t N, int C, const float* Y, int M, double* R,
+                          hipStream_t stream) {
+  const int ntile = (M + 63) / 64;
+  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)(C * ntile)), dim3(64), 0, stream, idx, N, C, Y, M, R);
+  return hipGetLastError();
+}
+
+hipError_t launch_fit_ridge(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* T0,
+                            double lam, double* T, int32_t* H, double* A, int cus, hipStream_t stream) {
+  const int64_t n = (int64_t)C * kK;
+  hipError_t e = launch_gram(idx, N, C, H, cus, stream);
+  if (e != hipSuccess) return e;
+  e = launch_scatter(idx, N, C, Y, M, T, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(assemble_kernel, dim3(grid_1d(n * n, 256)), dim3(256), 0, stream, H, n, lam, A, T, T0,
+                     n * M);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  for (int j0 = 0; j0 < n; j0 += kNB) {
+    const int jb = (int)((n - j0) < kNB ? (n - j0) : kNB);
+    hipLaunchKernelGGL(potrf_diag_kernel, dim3(1), dim3(256), 0, stream, A, n, j0, jb);
+    const int64_t below = n - j0 - jb;
+    if (below > 0) {
+      hipLaunchKernelGGL(trsm_panel_kernel, dim3(grid_1d(below, 256)), dim3(256), 0, stream, A, n, j0, jb);
+      const int64_t tiles = (below + kNB - 1) / kNB;
+      hipLaunchKernelGGL(syrk_kernel, dim3((unsigned)(tiles * (tiles + 1) / 2)), dim3(256), 0, stream, A, n, j0,
+                         jb);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  const int ntm = (M + 63) / 64;
+  for (int i0 = 0; i0 < n; i0 += kNB) {   // forward
+    const int ib = (int)((n - i0) < kNB ? (n - i0) : kNB);
+    hipLaunchKernelGGL(trsv_diag_kernel<true>, dim3(grid_1d(M, 256)), dim3(256), 0, stream, A, n, T, M, i0, ib);
+    const int64_t below = n - i0 - ib;
+    if (below > 0)
+      hipLaunchKernelGGL(trsv_update_kernel<true>, dim3((unsigned)(((below + kNB - 1) / kNB) * ntm)), dim3(256), 0,
+                         stream, A, n, T, M, i0, ib);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  const int64_t last = ((n - 1) / kNB) * kNB;
+  for (int64_t i0 = last; i0 >= 0; i0 -= kNB) {   // backward
+    const int ib = (int)((n - i0) < kNB ? (n - i0) : kNB);
+    hipLaunchKernelGGL(trsv_diag_kernel<false>, dim3(grid_1d(M, 256)), dim3(256), 0, stream, A, n, T, M, (int)i0,
+                       ib);
+    if (i0 > 0)
+      hipLaunchKernelGGL(trsv_update_kernel<false>, dim3((unsigned)(((i0 + kNB - 1) / kNB) * ntm)), dim3(256), 0,
+                         stream, A, n, T, M, (int)i0, ib);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace mdn

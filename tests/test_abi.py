@@ -123,3 +123,32 @@ def test_build_lut_rejects(L):
     assert B(FAKE, FAKE, 4, 64, 10, NULL, FAKE, FAKE, NULL) == 1
     assert B(FAKE, FAKE, 140000, 64, 10, FAKE, FAKE, FAKE, NULL) == 1  # 127 C >= 2^24
     assert L.maddness_build_lut_f32(FAKE, FAKE, 4, 0, 10, FAKE, NULL) == 1
+
+
+def test_fit_entry_points_reject(L):
+    Q = L.maddness_quantize_lut
+    assert Q(FAKE, 0, 10, 0, FAKE, FAKE, FAKE, NULL) == 1
+    assert Q(NULL, 4, 10, 0, FAKE, FAKE, FAKE, NULL) == 1
+    assert Q(ctypes.c_void_p(0x1004), 4, 10, 0, FAKE, FAKE, FAKE, NULL) == 1   # T not 8-byte aligned
+    assert Q(FAKE, 600, 10, 1, FAKE, FAKE, FAKE, NULL) == 3
+    G = L.maddness_encoder_gram
+    assert G(FAKE, -1, 4, FAKE, NULL) == 1
+    assert G(FAKE, 10, 4, NULL, NULL) == 1
+    assert G(FAKE, 10, 300, FAKE, NULL) == 3
+    assert G(FAKE, 1 << 31, 4, FAKE, NULL) == 3
+    S = L.maddness_encoder_scatter
+    assert S(FAKE, 10, 4, FAKE, 0, FAKE, NULL) == 1
+    assert S(FAKE, 10, 4, NULL, 8, FAKE, NULL) == 1
+    assert S(FAKE, 10, 300, FAKE, 8, FAKE, NULL) == 3
+    W = L.maddness_fit_lut_workspace_bytes
+    assert W(0) == -1 and W(257) == -1
+    assert W(4) == 64 * 64 * 4 + 64 * 64 * 8
+    F = L.maddness_fit_lut_ridge
+    ws = W(4)
+    assert F(FAKE, 10, 4, FAKE, 8, FAKE, 0.0, FAKE, FAKE, ws, NULL) == 1            # lambda = 0
+    assert F(FAKE, 10, 4, FAKE, 8, FAKE, float("nan"), FAKE, FAKE, ws, NULL) == 1   # lambda NaN
+    assert F(FAKE, 10, 4, FAKE, 8, FAKE, float("inf"), FAKE, FAKE, ws, NULL) == 1
+    assert F(FAKE, 10, 4, FAKE, 8, FAKE, 1.0, FAKE, FAKE, ws - 1, NULL) == 1        # workspace too small
+    assert F(FAKE, 10, 4, FAKE, 8, FAKE, 1.0, FAKE, ctypes.c_void_p(0x1010), ws, NULL) == 1   # not 256-aligned
+    assert F(FAKE, 10, 4, FAKE, 8, NULL, 1.0, FAKE, FAKE, ws, NULL) == 1            # NULL T0
+    assert F(FAKE, 10, 300, FAKE, 8, FAKE, 1.0, FAKE, FAKE, 1 << 40, NULL) == 3
