@@ -255,13 +255,13 @@ int maddness_quantize_lut(const double* T, int32_t C, int32_t M, int32_t shared,
  * a Cholesky factorisation and forward / backward substitution whose every
  * multiply-subtract is one fused multiply-add, terms of an entry taken k
  * ascending (factor, forward pass) or descending (backward pass).
- * workspace: device memory of at least maddness_fit_lut_workspace_bytes(C)
+ * workspace: device memory of at least maddness_fit_lut_workspace_bytes(N, C)
  * bytes, 256-byte aligned, caller-owned, contents undefined on return.
  * lambda must be positive and finite (EINVAL).  C > 256 or N >= 2^31 gives
  * EUNSUPPORTED.  Quantize the result with maddness_quantize_lut, or round it
  * to fp32 for the unquantized mode.
  */
-int64_t maddness_fit_lut_workspace_bytes(int32_t C);   /* -1 if C is out of range */
+int64_t maddness_fit_lut_workspace_bytes(int64_t N, int32_t C);   /* -1 if out of range */
 int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
                            const float* Y, int32_t M, const float* T0,
                            double lambda, double* T_out, void* workspace,
@@ -273,13 +273,17 @@ int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
  *   (H[16c + k][16c' + k'] = number of rows with idx[n][c] = k and
  *   idx[n][c'] = k'); exact.
  * maddness_encoder_scatter: R = G^T Y [16C][M] in double, each entry the sum
- *   of its rows in ascending row order.
- * C > 256 (or N >= 2^31 for the counts) gives EUNSUPPORTED.
+ *   of its rows in ascending row order; workspace (device, 256-byte aligned,
+ *   at least maddness_encoder_scatter_workspace_bytes(N, C) bytes) holds the
+ *   rows listed bucket by bucket.
+ * C > 256 or N >= 2^31 gives EUNSUPPORTED.
  */
 int maddness_encoder_gram(const uint8_t* idx, int64_t N, int32_t C,
                           int32_t* gram_out, void* stream);
+int64_t maddness_encoder_scatter_workspace_bytes(int64_t N, int32_t C);   /* -1 if out of range */
 int maddness_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C,
                              const float* Y, int32_t M, double* out,
+                             void* workspace, int64_t workspace_bytes,
                              void* stream);
 
 #ifdef __cplusplus

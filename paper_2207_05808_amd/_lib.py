@@ -55,8 +55,10 @@ def lib() -> ctypes.CDLL:
         L.maddness_build_lut_f32.argtypes = [vp, vp, i32, i32, i32, vp, vp]
         L.maddness_quantize_lut.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp]
         L.maddness_encoder_gram.argtypes = [vp, i64, i32, vp, vp]
-        L.maddness_encoder_scatter.argtypes = [vp, i64, i32, vp, i32, vp, vp]
-        L.maddness_fit_lut_workspace_bytes.argtypes = [i32]
+        L.maddness_encoder_scatter.argtypes = [vp, i64, i32, vp, i32, vp, vp, i64, vp]
+        L.maddness_encoder_scatter_workspace_bytes.argtypes = [i64, i32]
+        L.maddness_encoder_scatter_workspace_bytes.restype = i64
+        L.maddness_fit_lut_workspace_bytes.argtypes = [i64, i32]
         L.maddness_fit_lut_workspace_bytes.restype = i64
         L.maddness_fit_lut_ridge.argtypes = [vp, i64, i32, vp, i32, vp, ctypes.c_double, vp, vp, i64, vp]
         for f in ("maddness_version", "maddness_encode", "maddness_lut_accumulate",

@@ -462,11 +462,28 @@ def encoder_gram(idx, stream=None):
     return H
 
 
-def encoder_scatter(idx, Y, stream=None):
+def _workspace(workspace, need, device, stream):
+    """A 256-byte aligned pointer into ``workspace`` (allocated when None)."""
+    if workspace is None:
+        workspace = torch.empty((need + 256,), dtype=torch.uint8, device=device)
+        if stream is not None:
+            workspace.record_stream(stream)   # freed only after the work queued on `stream`
+    base = workspace.data_ptr()
+    off = (-base) % 256
+    if workspace.numel() - off < need:
+        raise ValueError(f"workspace must hold {need} bytes at a 256-byte aligned address")
+    return workspace, ctypes.c_void_p(base + off)
+
+
+def encoder_scatter(idx, Y, workspace=None, stream=None):
     """R = G^T Y: float64 [16C, M], each entry summed over its rows in order."""
     N, C, M = _fit_inputs(idx, Y)
+    need = int(_lib.lib().maddness_encoder_scatter_workspace_bytes(N, C))
+    if need < 0:
+        _lib.check("maddness_encoder_scatter", _lib.EUNSUPPORTED)
+    workspace, wp = _workspace(workspace, need, idx.device, stream)
     R = torch.empty((C * K, M), dtype=torch.float64, device=idx.device)
-    st = _lib.lib().maddness_encoder_scatter(_ptr(idx), N, C, _ptr(Y), M, _ptr(R), _stream(stream))
+    st = _lib.lib().maddness_encoder_scatter(_ptr(idx), N, C, _ptr(Y), M, _ptr(R), wp, need, _stream(stream))
     _lib.check("maddness_encoder_scatter", st)
     return R
 
@@ -475,25 +492,26 @@ def fit_lut_ridge(idx, Y, T0, lam, workspace=None, stream=None):
     """Model-aware table fit (Eq. 3, affine output): the float64 table
     [C,16,M] minimising ||Y - G T||^2 + lam ||T - T0||^2.  ``workspace``: an
     optional preallocated uint8 device tensor of at least
-    fit_lut_workspace_bytes(C) bytes."""
+    fit_lut_workspace_bytes(N, C) bytes (+ up to 255 for alignment)."""
     N, C, M = _fit_inputs(idx, Y)
     _need(T0, "T0", torch.float32, 3)
     _dense(T0, "T0")
     if tuple(T0.shape) != (C, K, M):
         raise ValueError("T0 must be [C,16,M]")
-    need = int(_lib.lib().maddness_fit_lut_workspace_bytes(C))
+    need = int(_lib.lib().maddness_fit_lut_workspace_bytes(N, C))
     if need < 0:
         _lib.check("maddness_fit_lut_ridge", _lib.EUNSUPPORTED)
-    if workspace is None:
-        workspace = torch.empty((need + 256,), dtype=torch.uint8, device=idx.device)
-        if stream is not None:
-            workspace.record_stream(stream)   # freed only after the work queued on `stream`
-    base = workspace.data_ptr()
-    off = (-base) % 256
-    if workspace.numel() - off < need:
-        raise ValueError(f"workspace must hold {need} bytes at a 256-byte aligned address")
+    workspace, wp = _workspace(workspace, need, idx.device, stream)
     T = torch.empty((C, K, M), dtype=torch.float64, device=idx.device)
     st = _lib.lib().maddness_fit_lut_ridge(_ptr(idx), N, C, _ptr(Y), M, _ptr(T0), float(lam), _ptr(T),
-                                           ctypes.c_void_p(base + off), need, _stream(stream))
+                                           wp, need, _stream(stream))
     _lib.check("maddness_fit_lut_ridge", st)
     return T
+
+
+def fit_lut_workspace_bytes(N: int, C: int) -> int:
+    """Device bytes fit_lut_ridge needs as workspace for N training rows and C codebooks."""
+    n = int(_lib.lib().maddness_fit_lut_workspace_bytes(N, C))
+    if n < 0:
+        _lib.check("maddness_fit_lut_workspace_bytes", _lib.EUNSUPPORTED)
+    return n

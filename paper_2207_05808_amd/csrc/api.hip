@@ -628,18 +628,27 @@ int maddness_encoder_gram(const uint8_t* idx, int64_t N, int32_t C, int32_t* gra
   return status_from(launch_gram(idx, N, C, gram_out, device_cus(), static_cast<hipStream_t>(stream)));
 }
 
-int maddness_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M, double* out,
-                             void* stream) {
-  if (N < 0 || C <= 0 || M <= 0 || !out || (N > 0 && (!idx || !Y))) return MADDNESS_EINVAL;
-  if (!aligned(out, 8) || (N > 0 && !aligned(Y, 4))) return MADDNESS_EINVAL;
-  if (C > kMaxFitC) return MADDNESS_EUNSUPPORTED;
-  return status_from(launch_scatter(idx, N, C, Y, M, out, static_cast<hipStream_t>(stream)));
+int64_t maddness_encoder_scatter_workspace_bytes(int64_t N, int32_t C) {
+  if (N < 0 || N >= (1ll << 31) || C <= 0 || C > kMaxFitC) return -1;
+  return round_up64((int64_t)C * (N + 128) * 4, 256) + (int64_t)C * (kK + 1) * 4;   // row lists + 128 padding each
 }
 
-int64_t maddness_fit_lut_workspace_bytes(int32_t C) {
-  if (C <= 0 || C > kMaxFitC) return -1;
+int maddness_encoder_scatter(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M, double* out,
+                             void* workspace, int64_t workspace_bytes, void* stream) {
+  if (N < 0 || C <= 0 || M <= 0 || !out || !workspace || (N > 0 && (!idx || !Y))) return MADDNESS_EINVAL;
+  if (!aligned(out, 8) || !aligned(workspace, 256) || (N > 0 && !aligned(Y, 4))) return MADDNESS_EINVAL;
+  if (C > kMaxFitC || N >= (1ll << 31)) return MADDNESS_EUNSUPPORTED;
+  if (workspace_bytes < maddness_encoder_scatter_workspace_bytes(N, C)) return MADDNESS_EINVAL;
+  int32_t* perm = static_cast<int32_t*>(workspace);
+  int32_t* start = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + round_up64((int64_t)C * (N + 128) * 4, 256));
+  return status_from(launch_scatter(idx, N, C, Y, M, out, perm, start, static_cast<hipStream_t>(stream)));
+}
+
+int64_t maddness_fit_lut_workspace_bytes(int64_t N, int32_t C) {
+  const int64_t ws = maddness_encoder_scatter_workspace_bytes(N, C);
+  if (ws < 0) return -1;
   const int64_t n = (int64_t)C * kK;
-  return round_up64(n * n * 4, 256) + n * n * 8;
+  return round_up64(n * n * 4, 256) + round_up64(n * n * 8, 256) + ws;
 }
 
 int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M, const float* T0,
@@ -650,12 +659,17 @@ int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C, const float
   if (!aligned(T_out, 8) || !aligned(T0, 4) || !aligned(workspace, 256) || (N > 0 && !aligned(Y, 4)))
     return MADDNESS_EINVAL;
   if (C > kMaxFitC || N >= (1ll << 31)) return MADDNESS_EUNSUPPORTED;
-  const int64_t need = maddness_fit_lut_workspace_bytes(C);
+  const int64_t need = maddness_fit_lut_workspace_bytes(N, C);
   if (workspace_bytes < need) return MADDNESS_EINVAL;
   const int64_t n = (int64_t)C * kK;
-  int32_t* H = static_cast<int32_t*>(workspace);
-  double* A = reinterpret_cast<double*>(static_cast<char*>(workspace) + round_up64(n * n * 4, 256));
-  return status_from(launch_fit_ridge(idx, N, C, Y, M, T0, lambda, T_out, H, A, device_cus(),
+  char* w = static_cast<char*>(workspace);
+  int32_t* H = reinterpret_cast<int32_t*>(w);
+  w += round_up64(n * n * 4, 256);
+  double* A = reinterpret_cast<double*>(w);
+  w += round_up64(n * n * 8, 256);
+  int32_t* perm = reinterpret_cast<int32_t*>(w);
+  int32_t* start = reinterpret_cast<int32_t*>(w + round_up64((int64_t)C * (N + 128) * 4, 256));
+  return status_from(launch_fit_ridge(idx, N, C, Y, M, T0, lambda, T_out, H, A, perm, start, device_cus(),
                                       static_cast<hipStream_t>(stream)));
 }
 

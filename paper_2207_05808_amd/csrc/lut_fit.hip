@@ -12,9 +12,11 @@
 //           Workgroups own an 8 x 8 block of codebook pairs and a row chunk,
 //           count in LDS, then add their nonzero counts to H (integer
 //           atomics: the result does not depend on their order).
-//   scatter R = G^T Y in double, one wavefront per (codebook, 64 columns),
-//           lane = column, rows in ascending order: every entry is the sum
-//           of its rows in the order they come.
+//   scatter R = G^T Y in double: a stable counting sort lists each
+//           codebook's rows bucket by bucket (ascending within a bucket),
+//           then one wavefront per (codebook, 64 columns), lane = column,
+//           sums each bucket's rows in that order: every entry is the sum of
+//           its rows in ascending row order.
 //   solve   A = H + lambda I (double), B = R + lambda T0; A = L L^T by a
 //           blocked right-looking Cholesky factorisation (panels of 32:
 //           diagonal block in one workgroup, the rows below it, then the
@@ -79,46 +81,115 @@ gram_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, int nbc, int64_t 
 
 // --------------------------------------------------------------- scatter
 // R[16c + k][m] = sum over rows n (ascending) with idx[n][c] = k of Y[n][m].
-// One wavefront per (codebook, 64-column tile); the row's index is uniform
-// across the wavefront, so the sum it feeds is chosen by a scalar branch.
-constexpr int kSR = 8;   // rows loaded ahead
+//
+// partition: one wavefront per codebook lists the rows bucket by bucket,
+// ascending within each bucket (a stable counting sort: per 64-row batch, one
+// ballot per bucket gives each row its rank among the batch's rows of its
+// bucket), perm[c][start_k ..] = rows of bucket k, start[c][k] the bucket
+// starts (start[c][16] = N).  Each codebook's list is followed by 2 x 64
+// entries of row 0, read (and ignored) by the last batches of the scatter.
+constexpr int kPermPad = 128;
 
 __global__ void __launch_bounds__(64)
-scatter_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, const float* __restrict__ Y, int M,
-               double* __restrict__ R) {
+partition_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, int32_t* __restrict__ perm,
+                 int32_t* __restrict__ start) {
+  const int lane = threadIdx.x;
+  const int c = blockIdx.x;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));   // lanes below this one
+  int64_t cnt[kK];
+#pragma unroll
+  for (int k = 0; k < kK; ++k) cnt[k] = 0;
+  for (int64_t n0 = 0; n0 < N; n0 += 64) {
+    const int key = (n0 + lane < N) ? (int)(idx[(n0 + lane) * C + c] & 15) : kK;
+#pragma unroll
+    for (int k = 0; k < kK; ++k) cnt[k] += __popcll(__ballot(key == k));
+  }
+  int64_t pos[kK];
+  int64_t run = 0;
+#pragma unroll
+  for (int k = 0; k < kK; ++k) {
+    pos[k] = run;
+    if (lane == 0) start[c * (kK + 1) + k] = (int32_t)run;
+    run += cnt[k];
+  }
+  if (lane == 0) start[c * (kK + 1) + kK] = (int32_t)N;
+  int32_t* pc = perm + (int64_t)c * (N + kPermPad);
+  pc[N + lane] = 0;
+  pc[N + 64 + lane] = 0;
+  for (int64_t n0 = 0; n0 < N; n0 += 64) {
+    const int key = (n0 + lane < N) ? (int)(idx[(n0 + lane) * C + c] & 15) : kK;
+#pragma unroll
+    for (int k = 0; k < kK; ++k) {
+      const uint64_t mask = __ballot(key == k);
+      if (key == k) pc[pos[k] + __popcll(mask & lt)] = (int32_t)(n0 + lane);
+      pos[k] += __popcll(mask);
+    }
+  }
+}
+
+// scatter: one wavefront per (codebook, 64-column tile), lane = column.  The
+// codebook's row list is walked in batches of 64 positions (the next batch's
+// 64 row loads in flight while the current one is added); a running double
+// sum takes the rows in list order and is stored and restarted at each
+// bucket end, so every entry is its bucket's rows summed in ascending order.
+constexpr int kSR = 64;   // positions per batch
+
+__global__ void __launch_bounds__(64)
+scatter_kernel(const int32_t* __restrict__ perm, const int32_t* __restrict__ start, int64_t N, int C,
+               const float* __restrict__ Y, int M, double* __restrict__ R) {
+  __shared__ float s_v[kSR][64];
   const int lane = threadIdx.x;
   const int ntile = (M + 63) / 64;
   const int c = blockIdx.x / ntile;
   const int m = (blockIdx.x % ntile) * 64 + lane;
   const bool ok = m < M;
-  double acc[kK];
-#pragma unroll
-  for (int k = 0; k < kK; ++k) acc[k] = 0.0;
-  for (int64_t n0 = 0; n0 < N; n0 += kSR) {
-    int kr[kSR];
-    double v[kSR];
-#pragma unroll
-    for (int j = 0; j < kSR; ++j) {
-      const int64_t n = n0 + j;
-      kr[j] = n < N ? (int)idx[n * C + c] : -1;
-      v[j] = (n < N && ok) ? (double)Y[n * M + m] : 0.0;
+  const float* yc = Y + min(m, M - 1);
+  const int32_t* pc = perm + (int64_t)c * (N + kPermPad);
+  const int32_t* sc = start + c * (kK + 1);
+  double* rc = R + (int64_t)c * kK * M + m;
+  int k = 0;
+  int64_t end = sc[1];   // end of bucket k
+  double acc = 0.0;
+  // store and restart the sums of every bucket that ends at position p
+  auto close_buckets = [&](int64_t p) {
+    while (k < kK && end == p) {
+      if (ok) rc[(int64_t)k * M] = acc;
+      acc = 0.0;
+      ++k;
+      end = (k < kK) ? sc[k + 1] : -1;
     }
+  };
+  // positions past N read the padding (row 0) and columns past M column
+  // M - 1: every load is valid, unused values are ignored; the row numbers
+  // are uniform (scalar loads)
+  float v[kSR], vn[kSR];
+  if (N > 0) {
 #pragma unroll
-    for (int j = 0; j < kSR; ++j) {
-      switch (__builtin_amdgcn_readfirstlane(kr[j])) {   // every lane holds the same value
-#define MDN_SCATTER_CASE(q) case q: acc[q] = __dadd_rn(acc[q], v[j]); break;
-        MDN_SCATTER_CASE(0) MDN_SCATTER_CASE(1) MDN_SCATTER_CASE(2) MDN_SCATTER_CASE(3)
-        MDN_SCATTER_CASE(4) MDN_SCATTER_CASE(5) MDN_SCATTER_CASE(6) MDN_SCATTER_CASE(7)
-        MDN_SCATTER_CASE(8) MDN_SCATTER_CASE(9) MDN_SCATTER_CASE(10) MDN_SCATTER_CASE(11)
-        MDN_SCATTER_CASE(12) MDN_SCATTER_CASE(13) MDN_SCATTER_CASE(14) MDN_SCATTER_CASE(15)
-#undef MDN_SCATTER_CASE
-        default: break;   // rows past N
+    for (int j = 0; j < kSR; ++j) v[j] = yc[(int64_t)pc[j] * M];
+  }
+  for (int64_t p0 = 0; p0 < N; p0 += kSR) {
+    const int32_t* pn = pc + p0 + kSR;
+#pragma unroll
+    for (int j = 0; j < kSR; ++j) vn[j] = yc[(int64_t)pn[j] * M];
+    if (end >= p0 + kSR) {
+      // the whole batch lies in bucket k
+#pragma unroll
+      for (int j = 0; j < kSR; ++j) acc = __dadd_rn(acc, (double)v[j]);
+    } else {
+      // a bucket ends inside the batch (at most 16 + 1 batches): position by
+      // position, the values parked in LDS (this lane's own column)
+#pragma unroll
+      for (int j = 0; j < kSR; ++j) s_v[j][lane] = v[j];
+#pragma unroll 1
+      for (int j = 0; j < kSR; ++j) {
+        close_buckets(p0 + j);
+        if (p0 + j < N) acc = __dadd_rn(acc, (double)s_v[j][lane]);
       }
     }
-  }
-  if (ok)
 #pragma unroll
-    for (int k = 0; k < kK; ++k) R[((int64_t)c * kK + k) * M + m] = acc[k];
+    for (int j = 0; j < kSR; ++j) v[j] = vn[j];
+  }
+  close_buckets(N);
 }
 
 // -------------------------------------------------------------- assemble
@@ -342,18 +413,22 @@ hipError_t launch_gram(const uint8_t* idx, int64_t N, int C, int32_t* H, int cus
 }
 
 hipError_t launch_scatter(const uint8_t* idx, int64_t N, int C, const float* Y, int M, double* R,
-                          hipStream_t stream) {
+                          int32_t* perm, int32_t* start, hipStream_t stream) {
+  hipLaunchKernelGGL(partition_kernel, dim3((unsigned)C), dim3(64), 0, stream, idx, N, C, perm, start);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int ntile = (M + 63) / 64;
-  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)(C * ntile)), dim3(64), 0, stream, idx, N, C, Y, M, R);
+  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)(C * ntile)), dim3(64), 0, stream, perm, start, N, C, Y, M, R);
   return hipGetLastError();
 }
 
 hipError_t launch_fit_ridge(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* T0,
-                            double lam, double* T, int32_t* H, double* A, int cus, hipStream_t stream) {
+                            double lam, double* T, int32_t* H, double* A, int32_t* perm, int32_t* start,
+                            int cus, hipStream_t stream) {
   const int64_t n = (int64_t)C * kK;
   hipError_t e = launch_gram(idx, N, C, H, cus, stream);
   if (e != hipSuccess) return e;
-  e = launch_scatter(idx, N, C, Y, M, T, stream);
+  e = launch_scatter(idx, N, C, Y, M, T, perm, start, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(assemble_kernel, dim3(grid_1d(n * n, 256)), dim3(256), 0, stream, H, n, lam, A, T, T0,
                      n * M);

@@ -137,14 +137,20 @@ def test_fit_entry_points_reject(L):
     assert G(FAKE, 10, 300, FAKE, NULL) == 3
     assert G(FAKE, 1 << 31, 4, FAKE, NULL) == 3
     S = L.maddness_encoder_scatter
-    assert S(FAKE, 10, 4, FAKE, 0, FAKE, NULL) == 1
-    assert S(FAKE, 10, 4, NULL, 8, FAKE, NULL) == 1
-    assert S(FAKE, 10, 300, FAKE, 8, FAKE, NULL) == 3
+    SW = L.maddness_encoder_scatter_workspace_bytes
+    assert SW(10, 0) == -1 and SW(-1, 4) == -1 and SW(1 << 31, 4) == -1
+    assert SW(10, 4) == 2304 + 4 * 17 * 4   # 4 lists of 10 + 128 rows (2208 bytes, rounded to 256), bucket starts
+    sw = SW(10, 4)
+    assert S(FAKE, 10, 4, FAKE, 0, FAKE, FAKE, sw, NULL) == 1
+    assert S(FAKE, 10, 4, NULL, 8, FAKE, FAKE, sw, NULL) == 1
+    assert S(FAKE, 10, 4, FAKE, 8, FAKE, FAKE, sw - 1, NULL) == 1   # workspace too small
+    assert S(FAKE, 10, 4, FAKE, 8, FAKE, NULL, sw, NULL) == 1
+    assert S(FAKE, 10, 300, FAKE, 8, FAKE, FAKE, 1 << 40, NULL) == 3
     W = L.maddness_fit_lut_workspace_bytes
-    assert W(0) == -1 and W(257) == -1
-    assert W(4) == 64 * 64 * 4 + 64 * 64 * 8
+    assert W(10, 0) == -1 and W(10, 257) == -1
+    assert W(10, 4) == 64 * 64 * 4 + 64 * 64 * 8 + SW(10, 4)
     F = L.maddness_fit_lut_ridge
-    ws = W(4)
+    ws = W(10, 4)
     assert F(FAKE, 10, 4, FAKE, 8, FAKE, 0.0, FAKE, FAKE, ws, NULL) == 1            # lambda = 0
     assert F(FAKE, 10, 4, FAKE, 8, FAKE, float("nan"), FAKE, FAKE, ws, NULL) == 1   # lambda NaN
     assert F(FAKE, 10, 4, FAKE, 8, FAKE, float("inf"), FAKE, FAKE, ws, NULL) == 1
