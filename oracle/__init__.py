@@ -20,6 +20,8 @@ Functions and the passages they follow (the paper: McCarter & Dronen,
   8-bit summation over codebooks, one shared block exponent), reading R20.
 * :func:`encoder_gram`, :func:`encoder_scatter`, :func:`fit_lut_ridge` --
   §2.2, Eq. 3 (model-aware table fit) with sigma affine, reading R21.
+* :func:`fit_lut_gd` -- Eq. 3 with sigma = ReLU (squared error) or softmax
+  (KL divergence, the objective of §3.1), gradient descent, reading R22.
 """
 from __future__ import annotations
 
@@ -81,6 +83,8 @@ class Oracle:
         lib.oracle_encoder_gram.argtypes = [vp, i64, i32, vp]
         lib.oracle_encoder_scatter.argtypes = [vp, i64, i32, vp, i32, vp]
         lib.oracle_fit_lut_ridge.argtypes = [vp, i64, i32, vp, i32, vp, ctypes.c_double, vp]
+        lib.oracle_fit_lut_gd.argtypes = [vp, i64, i32, vp, i32, vp, i32, vp, ctypes.c_double, ctypes.c_double,
+                                          i32, vp]
         self.lib = lib
 
     @staticmethod
@@ -265,6 +269,26 @@ class Oracle:
         rc = self.lib.oracle_fit_lut_ridge(idx.ctypes.data, N, C, Y.ctypes.data, M, T0.ctypes.data,
                                            ctypes.c_double(lam), T.ctypes.data)
         self._check(rc, "oracle_fit_lut_ridge")
+        return T
+
+    def fit_lut_gd(self, idx, Y, T0, act, lam, eta, iters, bias=None):
+        """Eq. 3 with a nonlinear sigma (R22): act 2 = ReLU + squared error,
+        3 = softmax + KL divergence; gradient descent from T0.  float64 [C, 16, M]."""
+        idx = np.ascontiguousarray(idx, dtype=np.uint8)
+        Y = np.ascontiguousarray(Y, dtype=np.float32)
+        T0 = np.ascontiguousarray(T0, dtype=np.float32)
+        N, C = idx.shape
+        M = Y.shape[1]
+        assert Y.shape[0] == N and T0.shape == (C, K, M)
+        bp = None
+        if bias is not None:
+            bias = np.ascontiguousarray(bias, dtype=np.float32)
+            assert bias.shape == (M,)
+            bp = bias.ctypes.data
+        T = np.zeros((C, K, M), dtype=np.float64)
+        rc = self.lib.oracle_fit_lut_gd(idx.ctypes.data, N, C, Y.ctypes.data, M, bp, int(act), T0.ctypes.data,
+                                        ctypes.c_double(lam), ctypes.c_double(eta), int(iters), T.ctypes.data)
+        self._check(rc, "oracle_fit_lut_gd")
         return T
 
     # convenience compositions (no arithmetic of their own)

@@ -41,6 +41,14 @@
  *       substitution, every multiply-subtract one fused multiply-add, the
  *       terms of an entry taken k ascending (factor, forward pass) or k
  *       descending (backward pass).
+ *   R22 Eq. 3 with a nonlinear sigma, by full-batch gradient descent from
+ *       T = T0 with a given step eta and iteration count (the paper names
+ *       the objectives, not the optimiser).  z_n = (sum_c T[c][idx][.], c
+ *       ascending, in double) + b.  ReLU: objective sum_n ||relu(y_n + b) -
+ *       relu(z_n)||^2, residual r = 2 (relu(z) - relu(y + b)) [z > 0].
+ *       Softmax: objective sum_n KL(softmax(y_n + b) || softmax(z_n)),
+ *       residual r = softmax(z) - softmax(y + b).  Step: R = G^T r (rows
+ *       ascending from 0), g = R + 2 lambda (T - T0), T = T - eta g.
  *   R19 layer output sigma: z = fl32(y + bias_m); ReLU keeps z when z > 0 and
  *       gives +0 otherwise; softmax is taken over the M outputs of a row.
  *   R20 rounded 8-bit summation: one shared block exponent; biased codes
@@ -521,4 +529,75 @@ int oracle_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
     }
     free(H); free(L); free(R); free(z);
     return rc;
+}
+
+/* row softmax in double: maximum subtracted, exp, sum over m ascending */
+static void softmax_row(const double* z, int32_t M, double* q)
+{
+    double mx = z[0];
+    for (int32_t m = 1; m < M; ++m) if (z[m] > mx) mx = z[m];
+    double sum = 0.0;
+    for (int32_t m = 0; m < M; ++m) { q[m] = exp(z[m] - mx); sum += q[m]; }
+    for (int32_t m = 0; m < M; ++m) q[m] = q[m] / sum;
+}
+
+/*
+ * Model-aware table fit, Eq. 3 with a nonlinear layer output (reading R22):
+ * act 2 = bias + ReLU with the squared-error objective, act 3 = bias + row
+ * softmax with the KL-divergence objective, both plus lambda ||T - T0||^2.
+ * Full-batch gradient descent from T = T0: `iters` steps of size eta.  The
+ * bias is optional (NULL = zeros).  T is [C][16][M] double.  Returns -1 on
+ * bad sizes, -2 on a bad act, lambda, eta or iteration count.
+ */
+int oracle_fit_lut_gd(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M,
+                      const float* bias, int32_t act, const float* T0, double lambda, double eta,
+                      int32_t iters, double* T)
+{
+    if (N < 0 || C <= 0 || M <= 0 || !T0 || !T || (N > 0 && (!idx || !Y))) return -1;
+    if ((act != 2 && act != 3) || !(lambda >= 0.0) || !isfinite(lambda) || !(eta > 0.0) ||
+        !isfinite(eta) || iters < 0)
+        return -2;
+    const int64_t n16 = (int64_t)C * ORACLE_K;
+    double* P = (double*)malloc(sizeof(double) * (N > 0 ? N : 1) * M);   /* sigma of the targets */
+    double* R = (double*)malloc(sizeof(double) * n16 * M);
+    double* z = (double*)malloc(sizeof(double) * M);
+    double* q = (double*)malloc(sizeof(double) * M);
+    if (!P || !R || !z || !q) { free(P); free(R); free(z); free(q); return -1; }
+    for (int64_t n = 0; n < N; ++n) {
+        for (int32_t m = 0; m < M; ++m) z[m] = (double)Y[n * M + m] + (bias ? (double)bias[m] : 0.0);
+        if (act == 2) {
+            for (int32_t m = 0; m < M; ++m) P[n * M + m] = z[m] > 0.0 ? z[m] : 0.0;
+        } else {
+            softmax_row(z, M, &P[n * M]);
+        }
+    }
+    for (int64_t j = 0; j < n16 * M; ++j) T[j] = (double)T0[j];
+    for (int32_t it = 0; it < iters; ++it) {
+        for (int64_t j = 0; j < n16 * M; ++j) R[j] = 0.0;
+        for (int64_t n = 0; n < N; ++n) {
+            for (int32_t m = 0; m < M; ++m) {
+                double sacc = 0.0;
+                for (int32_t c = 0; c < C; ++c)
+                    sacc += T[((int64_t)c * ORACLE_K + idx[n * C + c]) * M + m];
+                z[m] = sacc + (bias ? (double)bias[m] : 0.0);
+            }
+            if (act == 2) {
+                for (int32_t m = 0; m < M; ++m)
+                    q[m] = z[m] > 0.0 ? 2.0 * (z[m] - P[n * M + m]) : 0.0;
+            } else {
+                softmax_row(z, M, q);
+                for (int32_t m = 0; m < M; ++m) q[m] = q[m] - P[n * M + m];
+            }
+            for (int32_t c = 0; c < C; ++c) {
+                const int64_t r = (int64_t)c * ORACLE_K + idx[n * C + c];
+                for (int32_t m = 0; m < M; ++m) R[r * M + m] += q[m];
+            }
+        }
+        for (int64_t j = 0; j < n16 * M; ++j) {
+            const double g = R[j] + 2.0 * lambda * (T[j] - (double)T0[j]);
+            T[j] = T[j] - eta * g;
+        }
+    }
+    free(P); free(R); free(z); free(q);
+    return 0;
 }

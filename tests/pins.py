@@ -698,6 +698,86 @@ def check_fit_optimality(orc, seed=19):
     assert np.abs(res.x.reshape(2, K, 1) - T).max() <= 1e-5
 
 
+# ------------------------------------------- table fit, nonlinear sigma (R22)
+def _gd_objective(idx, Y, T, T0, lam, act, bias):
+    """Eq. 3 evaluated directly: act 2 = squared error after bias + ReLU, act 3
+    = KL divergence between the row softmaxes (scipy), plus lam ||T - T0||^2."""
+    from scipy.special import rel_entr, softmax
+    b = np.zeros(Y.shape[1]) if bias is None else bias.astype(np.float64)
+    z = _gather(idx, T) + b
+    t = Y.astype(np.float64) + b
+    if act == 2:
+        r = np.maximum(t, 0.0) - np.maximum(z, 0.0)
+        f = float((r * r).sum())
+    else:
+        f = float(rel_entr(softmax(t, axis=1), softmax(z, axis=1)).sum())
+    d = np.asarray(T, np.float64) - np.asarray(T0, np.float64)
+    return f + lam * float((d * d).sum())
+
+
+def check_fit_gd_gradient(orc, seed=20):
+    """One gradient step moves T by -eta times the gradient of Eq. 3's
+    objective: (T_k - T_{k+1}) / eta matches central finite differences of the
+    objective (evaluated directly), at T0 and after a first step (where the
+    penalty contributes), for ReLU and softmax, with and without a bias."""
+    rng = np.random.default_rng(seed)
+    idx, Y, T0 = _fit_problem(30, 2, 4, seed)
+    for act in (2, 3):
+        for bias in (None, rng.standard_normal(4).astype(np.float32)):
+            lam, eta = 0.3, 1e-3
+            T1 = orc.fit_lut_gd(idx, Y, T0, act, lam, eta, 1, bias)
+            T2 = orc.fit_lut_gd(idx, Y, T0, act, lam, eta, 2, bias)
+            for Ta, Tb in ((T0.astype(np.float64), T1), (T1, T2)):
+                g = (Ta - Tb) / eta
+                h = 1e-6
+                for _ in range(12):
+                    e = tuple(int(rng.integers(0, d)) for d in T0.shape)
+                    Tp, Tm = Ta.copy(), Ta.copy()
+                    Tp[e] += h
+                    Tm[e] -= h
+                    fd = (_gd_objective(idx, Y, Tp, T0, lam, act, bias) -
+                          _gd_objective(idx, Y, Tm, T0, lam, act, bias)) / (2 * h)
+                    assert abs(fd - g[e]) <= 1e-5 * (1 + abs(fd)), (act, e, fd, g[e])
+
+
+def check_fit_gd_fixed_point(orc, seed=21):
+    """Targets the prototype table already reproduces: for ReLU, Y = G T0
+    exactly (integer table) leaves T0 unchanged bit for bit; for softmax, any
+    per-row shift of G T0 gives the same row distributions (softmax is shift
+    invariant), so the gradient vanishes and T stays at T0 to rounding."""
+    rng = np.random.default_rng(seed)
+    C, M, N = 3, 5, 60
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    T0 = rng.integers(-6, 7, size=(C, K, M)).astype(np.float32)
+    bias = rng.integers(-3, 4, size=M).astype(np.float32)
+    Y = _gather(idx, T0).astype(np.float32)
+    T = orc.fit_lut_gd(idx, Y, T0, 2, 0.5, 0.01, 25, bias)
+    assert np.array_equal(T, T0.astype(np.float64))
+    shift = rng.integers(-4, 5, size=(N, 1)).astype(np.float64)
+    Ys = (_gather(idx, T0) + shift).astype(np.float32)
+    T = orc.fit_lut_gd(idx, Ys, T0, 3, 0.5, 0.01, 25, bias)
+    assert np.abs(T - T0).max() <= 1e-12
+
+
+def check_fit_gd_descent_and_limit(orc, seed=22):
+    """Small steps never raise the objective (softmax: convex; ReLU from a
+    generic start), and many steps reach the minimiser a generic method
+    (scipy BFGS on the directly evaluated objective) finds on a tiny case."""
+    from scipy.optimize import minimize
+    idx, Y, T0 = _fit_problem(40, 2, 3, seed)
+    bias = np.array([0.2, -0.1, 0.4], np.float32)
+    for act in (2, 3):
+        fs = [_gd_objective(idx, Y, orc.fit_lut_gd(idx, Y, T0, act, 0.2, 5e-3, k, bias), T0, 0.2, act, bias)
+              for k in range(0, 6)]
+        assert all(b <= a + 1e-12 for a, b in zip(fs, fs[1:])) and fs[-1] < fs[0]
+    idx, Y, T0 = _fit_problem(16, 1, 2, seed + 1)
+    lam = 0.5
+    T = orc.fit_lut_gd(idx, Y, T0, 3, lam, 0.2, 4000)
+    res = minimize(lambda v: _gd_objective(idx, Y, v.reshape(1, K, 2), T0, lam, 3, None),
+                   T0.astype(np.float64).ravel(), method="BFGS", options={"gtol": 1e-12})
+    assert np.abs(res.x.reshape(1, K, 2) - T).max() <= 1e-5
+
+
 ALL_CHECKS = [
     check_encode_brute_force, check_encode_search_tree, check_encode_nan, check_encode_permutation,
     check_encode_golden, check_one_hot_identity, check_decoder_table, check_output_rounding,
@@ -705,5 +785,5 @@ ALL_CHECKS = [
     check_f32_reconstruction, check_quantized_reconstruction, check_rejects_bad_inputs,
     check_sigma_bias_relu, check_sigma_softmax, check_avg_closed_forms, check_avg_bounds,
     check_shared_quantizer, check_encoder_gram, check_encoder_scatter, check_fit_closed_forms,
-    check_fit_optimality,
+    check_fit_optimality, check_fit_gd_gradient, check_fit_gd_fixed_point, check_fit_gd_descent_and_limit,
 ]

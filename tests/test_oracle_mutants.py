@@ -56,6 +56,16 @@ MUTANTS = [
     ("back substitution with the unfactored upper triangle", "v = fma(-L[k * n16 + i], z[k], v);",
      "v = fma(-L[i * n16 + k], z[k], v);"),
     ("ridge weight doubled in the matrix", "(i == j ? lambda : 0.0)", "(i == j ? 2.0 * lambda : 0.0)"),
+    ("softmax residual of the wrong sign", "q[m] = q[m] - P[n * M + m];", "q[m] = P[n * M + m] - q[m];"),
+    ("ReLU residual without the derivative",
+     "q[m] = z[m] > 0.0 ? 2.0 * (z[m] - P[n * M + m]) : 0.0;",
+     "q[m] = 2.0 * ((z[m] > 0.0 ? z[m] : 0.0) - P[n * M + m]);"),
+    ("bias left out of the fitted outputs", "z[m] = sacc + (bias ? (double)bias[m] : 0.0);", "z[m] = sacc;"),
+    ("penalty gradient without its factor 2", "const double g = R[j] + 2.0 * lambda * (T[j] - (double)T0[j]);",
+     "const double g = R[j] + lambda * (T[j] - (double)T0[j]);"),
+    ("step up the gradient", "T[j] = T[j] - eta * g;", "T[j] = T[j] + eta * g;"),
+    ("softmax sum over half the row", "for (int32_t m = 0; m < M; ++m) { q[m] = exp(z[m] - mx); sum += q[m]; }",
+     "for (int32_t m = 0; m < M; ++m) { q[m] = exp(z[m] - mx); if (m < M / 2 + 1) sum += q[m]; }"),
 ]
 
 
