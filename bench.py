@@ -123,6 +123,7 @@ def cpu_baseline(p, budget_s: float):
 FIT_TRAIN_ROWS = 16384    # training rows for the table fit (the paper's layers use 10,000)
 FIT_HELDOUT_ROWS = 8192
 FIT_LAMBDA = 1.0
+FIT_GD_STEPS = 10
 
 
 def main():
@@ -321,6 +322,19 @@ def main():
             torch.cuda.synchronize()
             return float((yh.double() - Y_ho.double()).norm() / Y_ho.double().norm())
 
+        # the nonlinear objectives (ReLU + squared error, softmax + KL
+        # divergence) by gradient descent: time per step over 10 steps, step
+        # 1 / (2 C Nb + 2 lambda) (Nb the largest bucket: Gershgorin bound on
+        # the curvature)
+        nb_max = max(int(torch.bincount(idx_tr[:, c].long(), minlength=16).max()) for c in range(spec.C))
+        eta = 1.0 / (2.0 * spec.C * nb_max + 2.0 * FIT_LAMBDA)
+        ws_gd = torch.empty((mdn.fit_lut_gd_workspace_bytes(n_tr, spec.C, spec.M) + 256,), dtype=torch.uint8,
+                            device=dev)
+        for act in ("relu", "softmax"):
+            us = region_us(lambda i, a=act: mdn.fit_lut_gd(idx_tr, Y_tr, T0, a, FIT_LAMBDA, eta, FIT_GD_STEPS,
+                                                            workspace=ws_gd), reps=2)
+            result["context"][f"fit_gd_{act}_ms_per_step"] = round(us / 1e3 / FIT_GD_STEPS, 3)
+        del ws_gd
         result["context"].update({"fit_lut_ridge_ms": round(fit_us / 1e3, 3), "fit_train_rows": n_tr,
                                   "fit_lambda": FIT_LAMBDA,
                                   "heldout_rel_err_prototype_table": float(f"{rel_err(T0):.4g}"),

@@ -268,6 +268,30 @@ int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
                            int64_t workspace_bytes, void* stream);
 
 /*
+ * Model-aware table fit (§2.2, Eq. 3) with a nonlinear layer output, by
+ * full-batch gradient descent from T = T0 (the paper names the objectives,
+ * not an optimiser; eta and iters are the caller's).  With
+ * z_n = (sum_c T[c][idx[n][c]][.], c ascending, double) + col_bias:
+ *   act = MADDNESS_ACT_RELU:    objective sum_n ||relu(Y[n] + b) - relu(z_n)||^2,
+ *                               residual 2 (relu(z) - relu(y + b)) [z > 0];
+ *   act = MADDNESS_ACT_SOFTMAX: objective sum_n KL(softmax(Y[n] + b) || softmax(z_n)),
+ *                               residual softmax(z) - softmax(y + b);
+ * each plus lambda ||T - T0||^2.  A step: R = G^T residual (rows ascending),
+ * g = R + 2 lambda (T - T0), T = T - eta g, all in double.  ReLU steps are
+ * exactly reproducible; softmax steps differ from another implementation only
+ * through exp and the order of the row sums.  col_bias [M] fp32 or NULL
+ * (zeros).  workspace: at least maddness_fit_lut_gd_workspace_bytes(N, C, M)
+ * device bytes, 256-byte aligned.  EINVAL: another act, lambda < 0, eta <= 0,
+ * non-finite values, iters < 0; EUNSUPPORTED: C > 256 or N >= 2^31.
+ */
+int64_t maddness_fit_lut_gd_workspace_bytes(int64_t N, int32_t C, int32_t M);   /* -1 if out of range */
+int maddness_fit_lut_gd(const uint8_t* idx, int64_t N, int32_t C,
+                        const float* Y, int32_t M, const float* col_bias,
+                        int32_t act, const float* T0, double lambda,
+                        double eta, int32_t iters, double* T_out,
+                        void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
  * The two sums the normal equations of Eq. 3 are built from:
  * maddness_encoder_gram: H = G^T G [16C][16C] as int32 counts
  *   (H[16c + k][16c' + k'] = number of rows with idx[n][c] = k and

@@ -61,12 +61,16 @@ def lib() -> ctypes.CDLL:
         L.maddness_fit_lut_workspace_bytes.argtypes = [i64, i32]
         L.maddness_fit_lut_workspace_bytes.restype = i64
         L.maddness_fit_lut_ridge.argtypes = [vp, i64, i32, vp, i32, vp, ctypes.c_double, vp, vp, i64, vp]
+        L.maddness_fit_lut_gd_workspace_bytes.argtypes = [i64, i32, i32]
+        L.maddness_fit_lut_gd_workspace_bytes.restype = i64
+        L.maddness_fit_lut_gd.argtypes = [vp, i64, i32, vp, i32, vp, i32, vp, ctypes.c_double, ctypes.c_double, i32,
+                                          vp, vp, i64, vp]
         for f in ("maddness_version", "maddness_encode", "maddness_lut_accumulate",
                   "maddness_lut_accumulate_f32", "maddness_matmul", "maddness_matmul_f32",
                   "maddness_matmul_act", "maddness_matmul_act_f32", "maddness_build_lut",
                   "maddness_build_lut_f32", "maddness_lut_accumulate_avg", "maddness_build_lut_shared",
                   "maddness_quantize_lut", "maddness_encoder_gram", "maddness_encoder_scatter",
-                  "maddness_fit_lut_ridge"):
+                  "maddness_fit_lut_ridge", "maddness_fit_lut_gd"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib

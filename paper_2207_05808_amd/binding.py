@@ -515,3 +515,37 @@ def fit_lut_workspace_bytes(N: int, C: int) -> int:
     if n < 0:
         _lib.check("maddness_fit_lut_workspace_bytes", _lib.EUNSUPPORTED)
     return n
+
+
+def fit_lut_gd(idx, Y, T0, act, lam, eta, iters, col_bias=None, workspace=None, stream=None):
+    """Model-aware table fit (Eq. 3) with a nonlinear output by gradient
+    descent from T0: act "relu" (squared error after bias + ReLU) or
+    "softmax" (KL divergence between row softmaxes); float64 [C,16,M]."""
+    N, C, M = _fit_inputs(idx, Y)
+    _need(T0, "T0", torch.float32, 3)
+    _dense(T0, "T0")
+    if tuple(T0.shape) != (C, K, M):
+        raise ValueError("T0 must be [C,16,M]")
+    code = ACT[act] if isinstance(act, str) else int(act)
+    if col_bias is not None:
+        _need(col_bias, "col_bias", torch.float32, 1)
+        _dense(col_bias, "col_bias")
+        if col_bias.shape[0] != M:
+            raise ValueError("col_bias must be [M]")
+    need = int(_lib.lib().maddness_fit_lut_gd_workspace_bytes(N, C, M))
+    if need < 0:
+        _lib.check("maddness_fit_lut_gd", _lib.EUNSUPPORTED)
+    workspace, wp = _workspace(workspace, need, idx.device, stream)
+    T = torch.empty((C, K, M), dtype=torch.float64, device=idx.device)
+    st = _lib.lib().maddness_fit_lut_gd(_ptr(idx), N, C, _ptr(Y), M, _ptr(col_bias), int(code), _ptr(T0), float(lam),
+                                        float(eta), int(iters), _ptr(T), wp, need, _stream(stream))
+    _lib.check("maddness_fit_lut_gd", st)
+    return T
+
+
+def fit_lut_gd_workspace_bytes(N: int, C: int, M: int) -> int:
+    """Device bytes fit_lut_gd needs as workspace."""
+    n = int(_lib.lib().maddness_fit_lut_gd_workspace_bytes(N, C, M))
+    if n < 0:
+        _lib.check("maddness_fit_lut_gd_workspace_bytes", _lib.EUNSUPPORTED)
+    return n

@@ -673,6 +673,38 @@ int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C, const float
                                       static_cast<hipStream_t>(stream)));
 }
 
+int64_t maddness_fit_lut_gd_workspace_bytes(int64_t N, int32_t C, int32_t M) {
+  const int64_t ws = maddness_encoder_scatter_workspace_bytes(N, C);
+  if (ws < 0 || M <= 0) return -1;
+  return 2 * round_up64(N * M * 8, 256) + round_up64((int64_t)C * kK * M * 8, 256) + ws;
+}
+
+int maddness_fit_lut_gd(const uint8_t* idx, int64_t N, int32_t C, const float* Y, int32_t M, const float* col_bias,
+                        int32_t act, const float* T0, double lambda, double eta, int32_t iters, double* T_out,
+                        void* workspace, int64_t workspace_bytes, void* stream) {
+  if (N < 0 || C <= 0 || M <= 0 || !T0 || !T_out || !workspace || (N > 0 && (!idx || !Y)))
+    return MADDNESS_EINVAL;
+  if (act != MADDNESS_ACT_RELU && act != MADDNESS_ACT_SOFTMAX) return MADDNESS_EINVAL;
+  if (!(lambda >= 0.0) || !std::isfinite(lambda) || !(eta > 0.0) || !std::isfinite(eta) || iters < 0)
+    return MADDNESS_EINVAL;
+  if (!aligned(T_out, 8) || !aligned(T0, 4) || !aligned(workspace, 256) || (N > 0 && !aligned(Y, 4)) ||
+      (col_bias && !aligned(col_bias, 4)))
+    return MADDNESS_EINVAL;
+  if (C > kMaxFitC || N >= (1ll << 31)) return MADDNESS_EUNSUPPORTED;
+  if (workspace_bytes < maddness_fit_lut_gd_workspace_bytes(N, C, M)) return MADDNESS_EINVAL;
+  char* w = static_cast<char*>(workspace);
+  double* P = reinterpret_cast<double*>(w);
+  w += round_up64(N * M * 8, 256);
+  double* D = reinterpret_cast<double*>(w);
+  w += round_up64(N * M * 8, 256);
+  double* R = reinterpret_cast<double*>(w);
+  w += round_up64((int64_t)C * kK * M * 8, 256);
+  int32_t* perm = reinterpret_cast<int32_t*>(w);
+  int32_t* start = reinterpret_cast<int32_t*>(w + round_up64((int64_t)C * (N + 128) * 4, 256));
+  return status_from(launch_fit_gd(idx, N, C, Y, M, col_bias, act, T0, lambda, eta, iters, T_out, P, D, R, perm,
+                                   start, static_cast<hipStream_t>(stream)));
+}
+
 int maddness_build_lut_f32(const float* P, const float* B, int32_t C, int32_t D, int32_t M, float* lut_out,
                            void* stream) {
   if (C <= 0 || D <= 0 || M <= 0 || !P || !B || !lut_out) return MADDNESS_EINVAL;

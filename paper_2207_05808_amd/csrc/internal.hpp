@@ -147,6 +147,9 @@ hipError_t launch_quantize_lut(const double* T, int C, int M, int8_t* lut, float
 hipError_t launch_gram(const uint8_t* idx, int64_t N, int C, int32_t* H, int cus, hipStream_t stream);
 hipError_t launch_scatter(const uint8_t* idx, int64_t N, int C, const float* Y, int M, double* R,
                           int32_t* perm, int32_t* start, hipStream_t stream);
+hipError_t launch_fit_gd(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* bias, int act,
+                         const float* T0, double lam, double eta, int iters, double* T, double* P, double* D,
+                         double* R, int32_t* perm, int32_t* start, hipStream_t stream);
 hipError_t launch_fit_ridge(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* T0,
                             double lam, double* T, int32_t* H, double* A, int32_t* perm, int32_t* start,
                             int cus, hipStream_t stream);

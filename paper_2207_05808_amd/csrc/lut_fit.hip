@@ -132,18 +132,18 @@ partition_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, int32_t* __r
 // 64 row loads in flight while the current one is added); a running double
 // sum takes the rows in list order and is stored and restarted at each
 // bucket end, so every entry is its bucket's rows summed in ascending order.
-constexpr int kSR = 64;   // positions per batch
-
+// V: float (targets Y) or double (gradient residuals); kSR positions per batch
+template <class V, int kSR>
 __global__ void __launch_bounds__(64)
 scatter_kernel(const int32_t* __restrict__ perm, const int32_t* __restrict__ start, int64_t N, int C,
-               const float* __restrict__ Y, int M, double* __restrict__ R) {
-  __shared__ float s_v[kSR][64];
+               const V* __restrict__ Y, int M, double* __restrict__ R) {
+  __shared__ V s_v[kSR][64];
   const int lane = threadIdx.x;
   const int ntile = (M + 63) / 64;
   const int c = blockIdx.x / ntile;
   const int m = (blockIdx.x % ntile) * 64 + lane;
   const bool ok = m < M;
-  const float* yc = Y + min(m, M - 1);
+  const V* yc = Y + min(m, M - 1);
   const int32_t* pc = perm + (int64_t)c * (N + kPermPad);
   const int32_t* sc = start + c * (kK + 1);
   double* rc = R + (int64_t)c * kK * M + m;
@@ -162,7 +162,7 @@ scatter_kernel(const int32_t* __restrict__ perm, const int32_t* __restrict__ sta
   // positions past N read the padding (row 0) and columns past M column
   // M - 1: every load is valid, unused values are ignored; the row numbers
   // are uniform (scalar loads)
-  float v[kSR], vn[kSR];
+  V v[kSR], vn[kSR];
   if (N > 0) {
 #pragma unroll
     for (int j = 0; j < kSR; ++j) v[j] = yc[(int64_t)pc[j] * M];
@@ -384,6 +384,88 @@ __global__ void __launch_bounds__(256) trsv_update_kernel(const double* __restri
   }
 }
 
+// ------------------------------------------- nonlinear output: gradient descent
+// z_n = (sum_c T[c][idx[n][c]][.], c ascending) + b.  One wavefront per row,
+// lanes over columns; the row's indices are uniform (scalar loads).
+__device__ __forceinline__ double wave_max(double v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+  for (int o = 32; o > 0; o >>= 1) v = __dadd_rn(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Softmax of the row held in out[0..M) (in place): maximum subtracted, exp,
+// sum, division.
+__device__ void softmax_row_inplace(double* __restrict__ out, int M, int lane) {
+  double mx = -__builtin_inf();
+  for (int m = lane; m < M; m += 64) mx = fmax(mx, out[m]);
+  mx = wave_max(mx);
+  double sum = 0.0;
+  for (int m = lane; m < M; m += 64) {
+    const double e = exp(__dsub_rn(out[m], mx));
+    out[m] = e;
+    sum = __dadd_rn(sum, e);
+  }
+  sum = wave_sum(sum);
+  for (int m = lane; m < M; m += 64) out[m] = __ddiv_rn(out[m], sum);
+}
+
+// P = sigma(Y + b): ReLU (act 2) or row softmax (act 3), in double
+__global__ void __launch_bounds__(256)
+target_kernel(const float* __restrict__ Y, int64_t N, int M, const float* __restrict__ bias, int act,
+              double* __restrict__ P) {
+  const int lane = threadIdx.x & 63;
+  for (int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); n < N; n += (int64_t)gridDim.x * 4) {
+    double* pr = P + n * M;
+    for (int m = lane; m < M; m += 64) {
+      const double z = __dadd_rn((double)Y[n * M + m], bias ? (double)bias[m] : 0.0);
+      pr[m] = (act == 2) ? (z > 0.0 ? z : 0.0) : z;
+    }
+    if (act == 3) softmax_row_inplace(pr, M, lane);
+  }
+}
+
+// D = dObjective / dz per row: ReLU 2 (relu(z) - P) [z > 0]; softmax softmax(z) - P
+__global__ void __launch_bounds__(256)
+resid_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, const double* __restrict__ T, int M,
+             const float* __restrict__ bias, int act, const double* __restrict__ P, double* __restrict__ D) {
+  const int lane = threadIdx.x & 63;
+  for (int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); n < N; n += (int64_t)gridDim.x * 4) {
+    const uint8_t* ir = idx + n * C;
+    double* dr = D + n * M;
+    const double* pr = P + n * M;
+    for (int m = lane; m < M; m += 64) {
+      double s = 0.0;
+      for (int c = 0; c < C; ++c) s = __dadd_rn(s, T[((int64_t)c * kK + (ir[c] & 15)) * M + m]);
+      const double z = __dadd_rn(s, bias ? (double)bias[m] : 0.0);
+      dr[m] = (act == 2) ? (z > 0.0 ? __dmul_rn(2.0, __dsub_rn(z, pr[m])) : 0.0) : z;
+    }
+    if (act == 3) {
+      softmax_row_inplace(dr, M, lane);
+      for (int m = lane; m < M; m += 64) dr[m] = __dsub_rn(dr[m], pr[m]);
+    }
+  }
+}
+
+// T = T - eta (R + 2 lambda (T - T0))
+__global__ void __launch_bounds__(256)
+gd_update_kernel(double* __restrict__ T, const float* __restrict__ T0, const double* __restrict__ R, double lam,
+                 double eta, int64_t total) {
+  const double two_lam = __dmul_rn(2.0, lam);
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const double g = __dadd_rn(R[e], __dmul_rn(two_lam, __dsub_rn(T[e], (double)T0[e])));
+    T[e] = __dsub_rn(T[e], __dmul_rn(eta, g));
+  }
+}
+
+__global__ void __launch_bounds__(256) copy_f32_f64_kernel(const float* __restrict__ a, double* __restrict__ b,
+                                                           int64_t total) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256)
+    b[e] = (double)a[e];
+}
+
 unsigned grid_1d(int64_t total, int per) {
   int64_t g = (total + per - 1) / per;
   if (g < 1) g = 1;
@@ -412,14 +494,26 @@ hipError_t launch_gram(const uint8_t* idx, int64_t N, int C, int32_t* H, int cus
   return hipGetLastError();
 }
 
+hipError_t launch_partition(const uint8_t* idx, int64_t N, int C, int32_t* perm, int32_t* start,
+                            hipStream_t stream) {
+  hipLaunchKernelGGL(partition_kernel, dim3((unsigned)C), dim3(64), 0, stream, idx, N, C, perm, start);
+  return hipGetLastError();
+}
+
+template <class V, int kSR>
+hipError_t launch_scatter_sorted(const int32_t* perm, const int32_t* start, int64_t N, int C, const V* Y, int M,
+                                 double* R, hipStream_t stream) {
+  const int ntile = (M + 63) / 64;
+  hipLaunchKernelGGL((scatter_kernel<V, kSR>), dim3((unsigned)(C * ntile)), dim3(64), 0, stream, perm, start, N, C,
+                     Y, M, R);
+  return hipGetLastError();
+}
+
 hipError_t launch_scatter(const uint8_t* idx, int64_t N, int C, const float* Y, int M, double* R,
                           int32_t* perm, int32_t* start, hipStream_t stream) {
-  hipLaunchKernelGGL(partition_kernel, dim3((unsigned)C), dim3(64), 0, stream, idx, N, C, perm, start);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_partition(idx, N, C, perm, start, stream);
   if (e != hipSuccess) return e;
-  const int ntile = (M + 63) / 64;
-  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)(C * ntile)), dim3(64), 0, stream, perm, start, N, C, Y, M, R);
-  return hipGetLastError();
+  return launch_scatter_sorted<float, 64>(perm, start, N, C, Y, M, R, stream);
 }
 
 hipError_t launch_fit_ridge(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* T0,
@@ -463,6 +557,31 @@ hipError_t launch_fit_ridge(const uint8_t* idx, int64_t N, int C, const float* Y
     if (i0 > 0)
       hipLaunchKernelGGL(trsv_update_kernel<false>, dim3((unsigned)(((i0 + kNB - 1) / kNB) * ntm)), dim3(256), 0,
                          stream, A, n, T, M, (int)i0, ib);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_fit_gd(const uint8_t* idx, int64_t N, int C, const float* Y, int M, const float* bias, int act,
+                         const float* T0, double lam, double eta, int iters, double* T, double* P, double* D,
+                         double* R, int32_t* perm, int32_t* start, hipStream_t stream) {
+  const int64_t total = (int64_t)C * kK * M;
+  hipLaunchKernelGGL(copy_f32_f64_kernel, dim3(grid_1d(total, 256)), dim3(256), 0, stream, T0, T, total);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || iters == 0) return e;
+  if ((e = launch_partition(idx, N, C, perm, start, stream)) != hipSuccess) return e;
+  const unsigned rows = grid_1d((N + 3) / 4, 1);   // 4 rows per workgroup, rows looped past 65536 groups
+  if (N > 0) {
+    hipLaunchKernelGGL(target_kernel, dim3(rows), dim3(256), 0, stream, Y, N, M, bias, act, P);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  for (int it = 0; it < iters; ++it) {
+    if (N > 0) {
+      hipLaunchKernelGGL(resid_kernel, dim3(rows), dim3(256), 0, stream, idx, N, C, T, M, bias, act, P, D);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if ((e = launch_scatter_sorted<double, 32>(perm, start, N, C, D, M, R, stream)) != hipSuccess) return e;
+    hipLaunchKernelGGL(gd_update_kernel, dim3(grid_1d(total, 256)), dim3(256), 0, stream, T, T0, R, lam, eta, total);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;

@@ -158,3 +158,18 @@ def test_fit_entry_points_reject(L):
     assert F(FAKE, 10, 4, FAKE, 8, FAKE, 1.0, FAKE, ctypes.c_void_p(0x1010), ws, NULL) == 1   # not 256-aligned
     assert F(FAKE, 10, 4, FAKE, 8, NULL, 1.0, FAKE, FAKE, ws, NULL) == 1            # NULL T0
     assert F(FAKE, 10, 300, FAKE, 8, FAKE, 1.0, FAKE, FAKE, 1 << 40, NULL) == 3
+
+
+def test_fit_gd_rejects(L):
+    W = L.maddness_fit_lut_gd_workspace_bytes
+    assert W(10, 0, 5) == -1 and W(10, 4, 0) == -1 and W(10, 300, 5) == -1
+    ws = W(10, 4, 5)
+    assert ws > 0
+    G = L.maddness_fit_lut_gd
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 1, FAKE, 0.1, 0.01, 3, FAKE, FAKE, ws, NULL) == 1   # act 1
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 3, FAKE, -0.1, 0.01, 3, FAKE, FAKE, ws, NULL) == 1  # lambda < 0
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 3, FAKE, 0.1, 0.0, 3, FAKE, FAKE, ws, NULL) == 1    # eta = 0
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 2, FAKE, 0.1, 0.01, -1, FAKE, FAKE, ws, NULL) == 1  # iters < 0
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 2, FAKE, 0.1, float("inf"), 3, FAKE, FAKE, ws, NULL) == 1
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 2, FAKE, 0.1, 0.01, 3, FAKE, FAKE, ws - 1, NULL) == 1
+    assert G(FAKE, 10, 300, FAKE, 5, NULL, 2, FAKE, 0.1, 0.01, 3, FAKE, FAKE, 1 << 40, NULL) == 3

@@ -1,7 +1,8 @@
-"""Parity of the model-aware table fit (Eq. 3, affine output, reading R21)
-and its pieces with the oracle, through the C ABI.
+"""Parity of the model-aware table fit (Eq. 3: affine output, reading R21;
+ReLU and softmax outputs by gradient descent, reading R22) and its pieces with
+the oracle, through the C ABI.
 
-Bar: bit-exact everywhere.  The Gram counts are integers; the scatter sums
+Bar: bit-exact everywhere except the softmax fit (bound derived below).  The Gram counts are integers; the scatter sums
 each entry's rows in ascending order in double on both sides; the solve
 takes the same correctly rounded operations (fma, division, square root) in
 the same order per entry on both sides (blocked on the GPU, unblocked in the
@@ -118,3 +119,93 @@ def test_fit_on_workload_training_rows(orc, name):
         return float((r * r).sum() + lam * ((np.asarray(Tx, np.float64) - T0) ** 2).sum())
 
     assert objective(T) < objective(T0)
+
+
+# ------------------------------------------------ nonlinear output (R22)
+# (N, C, M, lambda, step as a fraction of 1 / L, steps, bias)
+GD_CASES = [(200, 2, 5, 0.2, 1.0, 10, False),
+            (700, 8, 64, 0.0, 0.5, 6, True),
+            (1500, 17, 100, 1.0, 1.0, 5, True),
+            (999, 32, 10, 0.5, 1.5, 8, False)]
+
+
+def lipschitz(orc, idx, lam):
+    """L = lambda_max(G^T G) / 2 + 2 lambda bounds the curvature of the
+    softmax objective (the Hessian of log-sum-exp has norm <= 1/2); a step
+    eta <= 2 / L makes the exact gradient step non-expansive."""
+    H = orc.encoder_gram(idx).astype(np.float64)
+    return 0.5 * float(np.linalg.eigvalsh(H)[-1]) + 2.0 * lam
+
+
+@pytest.mark.parametrize("N,C,M,lam,frac,iters,with_bias", GD_CASES)
+def test_fit_gd_relu_matches_oracle(orc, N, C, M, lam, frac, iters, with_bias):
+    """ReLU + squared error: every operation is correctly rounded and in the
+    same order on both sides, so the tables agree to the bit."""
+    idx, Y, T0 = problem(N, C, M, seed=N + C + M + iters)
+    bias = np.random.default_rng(N).standard_normal(M).astype(np.float32) if with_bias else None
+    eta = frac / (2.0 * lipschitz(orc, idx, lam))
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "relu", lam, eta, iters,
+                            col_bias=dev(bias) if with_bias else None))
+    ref = orc.fit_lut_gd(idx, Y, T0, 2, lam, eta, iters, bias)
+    assert np.array_equal(T, ref), f"max |diff| {np.abs(T - ref).max():.3g}"
+
+
+def softmax_tolerance(idx, C, M, eta, iters, tmax):
+    """Bound on max |T_gpu - T_oracle| after K softmax steps with eta <= 2 / L.
+    Against the exact step, each side's computed step errs only by rounding:
+    a probability (exp within 1 ulp, an M-term sum, a division) by at most
+    (2M + 4) u, so a residual entry (two of them) by (4M + 8) u; a gradient
+    entry, a sum over its bucket's Nb rows, by Nb (4M + 8) u plus its own
+    rounding, at most Nb^2 u; the update by 4 u |T|.  The exact step is
+    non-expansive, so the two sides drift apart by at most the sum of both
+    sides' errors per step: in the 2-norm over the 16 C M entries,
+    K (eta (Nb (4M + 8) + Nb^2) + 4 tmax) u sqrt(16 C M) x 2."""
+    u = 2.0 ** -53
+    Nb = max(int(np.bincount(idx[:, c], minlength=16).max()) for c in range(C))
+    return 2 * iters * (eta * (Nb * (4 * M + 8) + Nb * Nb) + 4 * tmax) * u * np.sqrt(16 * C * M)
+
+
+@pytest.mark.parametrize("N,C,M,lam,frac,iters,with_bias", GD_CASES)
+def test_fit_gd_softmax_matches_oracle(orc, N, C, M, lam, frac, iters, with_bias):
+    idx, Y, T0 = problem(N, C, M, seed=N + 2 * C + M)
+    bias = np.random.default_rng(N + 1).standard_normal(M).astype(np.float32) if with_bias else None
+    eta = frac / lipschitz(orc, idx, lam)
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "softmax", lam, eta, iters,
+                            col_bias=dev(bias) if with_bias else None))
+    ref = orc.fit_lut_gd(idx, Y, T0, 3, lam, eta, iters, bias)
+    tol = softmax_tolerance(idx, C, M, eta, iters, float(np.abs(ref).max()))
+    err = float(np.abs(T - ref).max())
+    assert err <= tol, f"max |diff| {err:.3g} > bound {tol:.3g}"
+
+
+def test_fit_gd_zero_steps_and_rejects(orc):
+    idx, Y, T0 = problem(100, 3, 7, seed=9)
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "softmax", 0.1, 0.01, 0))
+    assert np.array_equal(T, T0.astype(np.float64))
+    for act, lam, eta, iters in (("bias", 0.1, 0.01, 2), ("relu", -1.0, 0.01, 2), ("relu", 0.1, 0.0, 2),
+                                 ("softmax", 0.1, 0.01, -1)):
+        with pytest.raises(mdn.MaddnessError):
+            mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), act, lam, eta, iters)
+
+
+def test_fit_gd_softmax_classifier(orc):
+    """The paper's softmax-classifier setting on the classifier workload
+    (C = 4, M = 10): the KL-divergence fit on 512 training rows (step 1 / L)
+    matches the oracle within the bound and lowers the training objective
+    below the prototype table's."""
+    p = W.make("classifier_tiny")
+    idx = orc.encode(p.A[:512], p.split, p.thr)
+    Y = (p.A[:512].astype(np.float64) @ p.B.astype(np.float64)).astype(np.float32)
+    T0 = orc.build_lut_f32(p.P, p.B)
+    lam, iters = 0.1, 40
+    eta = 1.0 / lipschitz(orc, idx, lam)
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "softmax", lam, eta, iters))
+    ref = orc.fit_lut_gd(idx, Y, T0, 3, lam, eta, iters)
+    assert np.abs(T - ref).max() <= softmax_tolerance(idx, 4, 10, eta, iters, float(np.abs(ref).max()))
+    from scipy.special import rel_entr, softmax
+
+    def kl(Tx):
+        z = sum(np.asarray(Tx, np.float64)[c][idx[:, c]] for c in range(4))
+        return float(rel_entr(softmax(Y.astype(np.float64), axis=1), softmax(z, axis=1)).sum())
+
+    assert kl(T) < kl(T0)
