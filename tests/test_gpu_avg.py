@@ -85,3 +85,25 @@ def test_avg_workloads_with_shared_tables(orc, name):
     assert np.array_equal(host(lut), rl) and np.array_equal(host(scale), rs) and np.array_equal(host(offset), ro)
     idx = orc.encode(p.A, p.split, p.thr)
     run_avg(orc, idx, rl, rs, ro)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["conv3x3_im2col", "dense_hidden", "wide_layer"])
+def test_avg_full_size_sampled(orc, name):
+    """Full-size workload in the launch configuration the benchmark's context
+    times (GPU encoder, GPU shared-exponent table, averaging accumulate over
+    every row); the oracle encodes and sums a sample of rows itself."""
+    from test_gpu_parity import sample_rows
+    p = W.make(name)
+    rows = sample_rows(p.N)
+    idx = mdn.encode(dev(p.A), dev(p.split), dev(p.thr))
+    lut, scale, offset = mdn.build_lut_shared(dev(p.P), dev(p.B))
+    rl, rs, ro = orc.build_shared_lut(p.P, p.B)
+    assert np.array_equal(host(lut), rl) and np.array_equal(host(scale), rs)
+    acc, y = mdn.lut_accumulate_avg(idx, lut, scale, offset, want_acc=True)
+    racc, ry = orc.lut_accumulate_avg(orc.encode(p.A[rows], p.split, p.thr), rl, rs, ro)
+    r = torch.from_numpy(rows).to(DEV)
+    assert np.array_equal(host(acc[r]), racc)
+    assert np.array_equal(host(y[r]), ry)
+    del acc, y, idx
+    torch.cuda.empty_cache()

@@ -209,3 +209,20 @@ def test_fit_gd_softmax_classifier(orc):
         return float(rel_entr(softmax(Y.astype(np.float64), axis=1), softmax(z, axis=1)).sum())
 
     assert kl(T) < kl(T0)
+
+
+@pytest.mark.slow
+def test_fits_at_benchmark_size(orc):
+    """The benchmark's fit configuration on dense_hidden: 16384 training rows,
+    C = 64, M = 512 (1024 unknowns per column), lambda = 1; the closed-form
+    fit and three ReLU gradient steps equal the oracle's bit for bit."""
+    p = W.make("dense_hidden", N=16384)
+    idx = orc.encode(p.A, p.split, p.thr)
+    Y = (p.A.astype(np.float64) @ p.B.astype(np.float64)).astype(np.float32)
+    T0 = orc.build_lut_f32(p.P, p.B)
+    T = host(mdn.fit_lut_ridge(dev(idx), dev(Y), dev(T0), 1.0))
+    assert np.array_equal(T, orc.fit_lut_ridge(idx, Y, T0, 1.0))
+    nb = max(int(np.bincount(idx[:, c], minlength=16).max()) for c in range(64))
+    eta = 1.0 / (2.0 * 64 * nb + 2.0)
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "relu", 1.0, eta, 3))
+    assert np.array_equal(T, orc.fit_lut_gd(idx, Y, T0, 2, 1.0, eta, 3))
