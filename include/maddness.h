@@ -259,8 +259,9 @@ int maddness_quantize_lut(const double* T, int32_t C, int32_t M, int32_t shared,
  * bytes, 256-byte aligned, caller-owned, contents undefined on return.
  * lambda must be positive and finite (EINVAL); with a rank-deficient G^T G
  * (every row picks one bucket per codebook, so it always is for C > 1) a
- * lambda far below 1 can leave the factorisation without a positive pivot
- * in double, and the result is then NaN.  C > 256 or N >= 2^31 gives
+ * lambda near the rounding level of G^T G's entries (about N x 1e-16) can
+ * leave the factorisation without a positive pivot in double, and the
+ * result is then NaN.  C > 256 or N >= 2^31 gives
  * EUNSUPPORTED.  Quantize the result with maddness_quantize_lut, or round it
  * to fp32 for the unquantized mode.
  */
