@@ -28,8 +28,6 @@
 // does not depend on the blocking.
 #include "internal.hpp"
 
-#include <climits>
-
 namespace mdn {
 
 namespace {
@@ -86,8 +84,8 @@ gram_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, int nbc, int64_t 
 // ascending within each bucket (a stable counting sort: per 64-row batch, one
 // ballot per bucket gives each row its rank among the batch's rows of its
 // bucket), perm[c][start_k ..] = rows of bucket k, start[c][k] the bucket
-// starts (start[c][16] = N).  Each codebook's list is followed by 2 x 64
-// entries of row 0, read (and ignored) by the last batches of the scatter.
+// starts (start[c][16] = N).  Each codebook's list is followed by 128 entries
+// of row 0, read (and ignored) by the last two batches of the scatter.
 constexpr int kPermPad = 128;
 
 __global__ void __launch_bounds__(64)
@@ -128,8 +126,9 @@ partition_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, int32_t* __r
 }
 
 // scatter: one wavefront per (codebook, 64-column tile), lane = column.  The
-// codebook's row list is walked in batches of 64 positions (the next batch's
-// 64 row loads in flight while the current one is added); a running double
+// codebook's row list is walked in batches of kSR positions (64 for float
+// inputs, 32 for double; the next batch's loads in flight while the current
+// one is added); a running double
 // sum takes the rows in list order and is stored and restarted at each
 // bucket end, so every entry is its bucket's rows summed in ascending order.
 // V: float (targets Y) or double (gradient residuals); kSR positions per batch
