@@ -304,6 +304,14 @@ def main():
                                   "fused_speedup_vs_gemm": round(gms / 1e3 / avg_kern_s, 3)})
         del out
 
+        # offline table construction on the GPU: T = P B in double, then the
+        # 8-bit block floating point quantizer (or the fp32 rounding)
+        if spec.quantized:
+            build_us = region_us(lambda i: mdn.build_lut(Pd, Bd), reps=3)
+        else:
+            build_us = region_us(lambda i: mdn.build_lut_f32(Pd, Bd), reps=3)
+        result["context"]["build_lut_ms"] = round(build_us / 1e3, 3)
+
         # model-aware table fit (Eq. 3, affine output) on 16384 training rows
         # of the same layer (targets Y = AB, prototype table T0 = P B), and
         # its effect on 8192 held-out rows through the fp32-table accumulate

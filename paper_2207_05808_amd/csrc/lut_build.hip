@@ -18,6 +18,11 @@
 namespace mdn {
 
 constexpr int kBuildThreads = 256;
+// the statistics pass: one workgroup of kStatsThreads per codebook, kStatsILP
+// entries of a thread evaluated together (their sums are independent chains,
+// each in its own order)
+constexpr int kStatsThreads = 1024;
+constexpr int kStatsILP = 4;
 
 __device__ __forceinline__ double table_entry(const float* __restrict__ P, const float* __restrict__ B,
                                               int D, int M, int64_t row, int m) {
@@ -34,18 +39,45 @@ struct SrcPB {
   const float* B;
   int D, M;
   __device__ double at(int64_t row, int m) const { return table_entry(P, B, D, M, row, m); }
+  // entries e0 + q stride (q < kStatsILP) of codebook c's 16 x M block: the
+  // sums run side by side, each over d ascending; entries past `per` read a
+  // valid entry and are ignored
+  __device__ void at_many(int c, int e0, int stride, int per, double* t) const {
+    const float* p[kStatsILP];
+    const float* b[kStatsILP];
+#pragma unroll
+    for (int q = 0; q < kStatsILP; ++q) {
+      const int e = min(e0 + q * stride, per - 1);
+      const int k = e / M, m = e - k * M;
+      p[q] = P + ((int64_t)c * kK + k) * D;
+      b[q] = B + m;
+      t[q] = 0.0;
+    }
+    for (int d = 0; d < D; ++d)
+#pragma unroll
+      for (int q = 0; q < kStatsILP; ++q)
+        t[q] = __dadd_rn(t[q], __dmul_rn((double)p[q][d], (double)b[q][(int64_t)d * M]));
+  }
 };
 struct SrcT {
   const double* T;
   int M;
   __device__ double at(int64_t row, int m) const { return T[row * M + m]; }
+  __device__ void at_many(int c, int e0, int stride, int per, double* t) const {
+#pragma unroll
+    for (int q = 0; q < kStatsILP; ++q) {
+      const int e = min(e0 + q * stride, per - 1);
+      t[q] = T[(int64_t)c * kK * M + e];
+    }
+  }
 };
 
+template <int NT>
 __device__ double block_reduce(double v, bool take_max, double* s_red) {
   const int tid = threadIdx.x;
   s_red[tid] = v;
   __syncthreads();
-  for (int w = kBuildThreads / 2; w > 0; w >>= 1) {
+  for (int w = NT / 2; w > 0; w >>= 1) {
     if (tid < w) {
       const double o = s_red[tid + w];
       s_red[tid] = take_max ? fmax(s_red[tid], o) : fmin(s_red[tid], o);
@@ -58,28 +90,34 @@ __device__ double block_reduce(double v, bool take_max, double* s_red) {
 }
 
 template <class Src>
-__global__ void __launch_bounds__(kBuildThreads)
+__global__ void __launch_bounds__(kStatsThreads)
 table_stats_kernel(const Src src, int M, float* __restrict__ scale_out, float* __restrict__ offset_out) {
-  __shared__ double s_red[kBuildThreads];
+  __shared__ double s_red[kStatsThreads];
   const int c = blockIdx.x;
   const int per = kK * M;
   double lo = __builtin_inf(), hi = -__builtin_inf();
-  for (int e = threadIdx.x; e < per; e += kBuildThreads) {
-    const int k = e / M, m = e - k * M;
-    const double t = src.at((int64_t)c * kK + k, m);
-    lo = fmin(lo, t);
-    hi = fmax(hi, t);
+  for (int e0 = threadIdx.x; e0 < per; e0 += kStatsILP * kStatsThreads) {
+    double t[kStatsILP];
+    src.at_many(c, e0, kStatsThreads, per, t);
+#pragma unroll
+    for (int q = 0; q < kStatsILP; ++q)
+      if (e0 + q * kStatsThreads < per) {
+        lo = fmin(lo, t[q]);
+        hi = fmax(hi, t[q]);
+      }
   }
-  lo = block_reduce(lo, false, s_red);
-  hi = block_reduce(hi, true, s_red);
+  lo = block_reduce<kStatsThreads>(lo, false, s_red);
+  hi = block_reduce<kStatsThreads>(hi, true, s_red);
   const float o = (float)__ddiv_rn(__dadd_rn(lo, hi), 2.0);
   double r = 0.0;
-  for (int e = threadIdx.x; e < per; e += kBuildThreads) {
-    const int k = e / M, m = e - k * M;
-    const double t = src.at((int64_t)c * kK + k, m);
-    r = fmax(r, fabs(__dsub_rn(t, (double)o)));
+  for (int e0 = threadIdx.x; e0 < per; e0 += kStatsILP * kStatsThreads) {
+    double t[kStatsILP];
+    src.at_many(c, e0, kStatsThreads, per, t);
+#pragma unroll
+    for (int q = 0; q < kStatsILP; ++q)
+      if (e0 + q * kStatsThreads < per) r = fmax(r, fabs(__dsub_rn(t[q], (double)o)));
   }
-  r = block_reduce(r, true, s_red);
+  r = block_reduce<kStatsThreads>(r, true, s_red);
   if (threadIdx.x == 0) {
     int ex = -126;
     while (ex < 127 && r > 127.0 * __builtin_ldexp(1.0, ex)) ++ex;
@@ -152,7 +190,7 @@ static unsigned grid_for(int64_t total) {
 template <class Src>
 static hipError_t quantize(const Src& src, int C, int M, int8_t* lut, float* scale, float* offset, int cap,
                            hipStream_t stream) {
-  hipLaunchKernelGGL(table_stats_kernel<Src>, dim3(C), dim3(kBuildThreads), 0, stream, src, M, scale, offset);
+  hipLaunchKernelGGL(table_stats_kernel<Src>, dim3(C), dim3(kStatsThreads), 0, stream, src, M, scale, offset);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(table_codes_kernel<Src>, dim3(grid_for((int64_t)C * kK * M)), dim3(kBuildThreads), 0,
