@@ -335,7 +335,7 @@ bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
   auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
   // index batches: B rows of C bytes, at most 16 KB and two 16-byte units per thread
   const int RS = 64 / (Mt / 16);
-  int nwb = nw;   // the kernel has 512- and 1024-thread instances
+  int nwb = nw;   // 512-thread workgroups
   while (nwb > 8 && nwb * RS * s.C > 16 * 1024) nwb /= 2;
   if (nwb * RS * s.C > 16 * 1024) return false;
   int J = 1;

@@ -388,8 +388,8 @@ __device__ __forceinline__ uint32_t avg4(uint32_t a, uint32_t b) { return __buil
 // GI at a time (unrolled, their merges resolved at compile time) in GO = GA /
 // GI rounds of a runtime loop whose results (subtrees of 8 GI codebooks) merge
 // through up to three pending levels.  The unrolled subtrees bound the LDS
-// reads in flight, and with them the registers: GI = 4 within 256 VGPRs (512
-// threads), GI = 2 within 128 (1024 threads).
+// reads in flight, and with them the registers: GI = 4 within the 256 VGPRs
+// of a 512-thread workgroup.
 // WIDX: C % 4 == 0, index words read as dwords (else byte by byte).
 template <int GI, int GO, bool WIDX, int NT>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT / 256, NT / 256)))
@@ -770,7 +770,7 @@ static hipError_t alaunch(const TArgs& t, int cus, hipStream_t stream) {
 // GA = P / 8 subtrees (at least 1) split into GI unrolled x GO rounds
 template <int GA, int NT>
 static hipError_t alaunch_g(const TArgs& t, int cus, hipStream_t stream) {
-  constexpr int kGI = GA < (NT == 1024 ? 2 : 4) ? GA : (NT == 1024 ? 2 : 4);
+  constexpr int kGI = GA < 4 ? GA : 4;
   constexpr int kGO = GA / kGI;
   if (t.C % 4 == 0) return alaunch<kGI, kGO, true, NT>(t, cus, stream);
   return alaunch<kGI, kGO, false, NT>(t, cus, stream);
@@ -791,16 +791,13 @@ static hipError_t launch_tavg_nt(const TArgs& t, int cus, hipStream_t stream) {
 }
 
 hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream) {
-  if (nw == 16) return launch_tavg_nt<1024>(t, cus, stream);
   if (nw == 8) return launch_tavg_nt<512>(t, cus, stream);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {
   if (elem == kI8 && nj == 4) return tlaunch<kI8, 4>(t, nw, cus, stream);
-  if (elem == kI8 && nj == 8) return tlaunch<kI8, 8>(t, nw, cus, stream);
   if (elem == kF32 && nj == 4) return tlaunch<kF32, 4>(t, nw, cus, stream);
-  if (elem == kF32 && nj == 8) return tlaunch<kF32, 8>(t, nw, cus, stream);
   return hipErrorInvalidValue;
 }
 
