@@ -319,7 +319,9 @@ bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
   const int C8 = round_up(s.C, 8);   // staged codebooks: whole groups of 8
   int Mt = 256;
   while (Mt > 16 && (int64_t)(C8 + 1) * kK * Mt > 136 * 1024) Mt /= 2;   // + a padding block
-  while (Mt > 16 && Mt / 2 >= s.M) Mt /= 2;   // no wider than the outputs
+  // no wider than the outputs, while a batch of the narrower tile's minimum
+  // rows (8 wavefronts x 64 / lanes-per-row rows) still fits the staging
+  while (Mt > 16 && Mt / 2 >= s.M && nw * (64 / (Mt / 32)) * s.C <= 16 * 1024) Mt /= 2;
   if ((int64_t)(C8 + 1) * kK * Mt > 136 * 1024) return false;
   TArgs a{};
   a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;

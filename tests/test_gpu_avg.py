@@ -34,7 +34,8 @@ def run_avg(orc, idx, lut, scale, offset):
 
 
 CASES = [(1, 16), (2, 10), (3, 64), (5, 17), (8, 256), (9, 300), (16, 128), (33, 1024), (64, 512),
-         (100, 64), (128, 4096), (120, 33)]
+         (100, 64), (128, 4096), (120, 33),
+         (40, 3), (128, 3), (128, 16)]   # narrow outputs: the column tile stays wide enough for a batch
 
 
 @pytest.mark.parametrize("C,M", CASES)
