@@ -13,7 +13,7 @@ from paper_2207_05808_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-SEEDS = list(range(24))
+SEEDS = list(range(40))
 
 
 def dev(x):
@@ -102,3 +102,34 @@ def test_sweep_matmul_act(orc, seed):
     d = z - (z.max(axis=1, keepdims=True) if z.size else 0.0)
     tol = 1.01 * (np.abs(d) + M + 5) * 2.0 ** -24 * ref + 2.0 ** -120
     assert np.all(np.abs(y.astype(np.float64) - ref) <= tol)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_sweep_encode_and_f32_act(orc, seed):
+    rng, A, split, thr, lut, _, _ = draw(seed)
+    idx = host(mdn.encode(dev_rows(A), dev(split), dev(thr)))
+    assert np.array_equal(idx, orc.encode(A, split, thr))
+    C, M = lut.shape[0], lut.shape[2]
+    tab = W.random_fp32_table(C, M, seed=6000 + seed)
+    bias = rng.standard_normal(M).astype(np.float32)
+    act = ["bias", "relu"][seed % 2]
+    y = host(mdn.matmul_act_f32(dev_rows(A), dev(split), dev(thr), dev(tab), col_bias=dev(bias), act=act))
+    _, yref = orc.matmul_f32(A, split, thr, tab)
+    assert np.array_equal(y.astype(np.float64), orc.sigma(yref, bias, {"bias": 1, "relu": 2}[act]))
+
+
+@pytest.mark.parametrize("seed", SEEDS[:16])
+def test_sweep_fit(orc, seed):
+    """Gram counts, G^T Y and the closed-form fit on random shapes (C up to
+    40, so the oracle's dense solve stays fast)."""
+    rng = np.random.default_rng(7000 + seed)
+    N = int(rng.integers(0, 3000))
+    C = int(rng.choice([1, 2, 3, 5, 8, 13, 20, 32, 40]))
+    M = int(rng.choice([1, 2, 7, 63, 64, 65, 130]))
+    idx = W.random_indices(N, C, seed=8000 + seed)
+    Y = (rng.standard_normal((N, M)) * 2).astype(np.float32)
+    T0 = rng.standard_normal((C, 16, M)).astype(np.float32)
+    lam = float(rng.choice([0.01, 0.5, 3.0]))
+    assert np.array_equal(host(mdn.encoder_gram(dev(idx))).astype(np.int64), orc.encoder_gram(idx))
+    assert np.array_equal(host(mdn.encoder_scatter(dev(idx), dev(Y))), orc.encoder_scatter(idx, Y))
+    assert np.array_equal(host(mdn.fit_lut_ridge(dev(idx), dev(Y), dev(T0), lam)), orc.fit_lut_ridge(idx, Y, T0, lam))
