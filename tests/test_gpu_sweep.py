@@ -133,3 +133,33 @@ def test_sweep_fit(orc, seed):
     assert np.array_equal(host(mdn.encoder_gram(dev(idx))).astype(np.int64), orc.encoder_gram(idx))
     assert np.array_equal(host(mdn.encoder_scatter(dev(idx), dev(Y))), orc.encoder_scatter(idx, Y))
     assert np.array_equal(host(mdn.fit_lut_ridge(dev(idx), dev(Y), dev(T0), lam)), orc.fit_lut_ridge(idx, Y, T0, lam))
+
+
+def shifted(x, dtype):
+    """Device copy of x starting one element past a fresh allocation (so not
+    16-byte aligned)."""
+    flat = torch.empty(x.size + 1, dtype=dtype, device=DEV)
+    v = flat[1:].view(x.shape)
+    v.copy_(torch.from_numpy(np.ascontiguousarray(x)).to(DEV))
+    return v
+
+
+@pytest.mark.parametrize("seed", SEEDS[:16])
+def test_sweep_misaligned(orc, seed):
+    """A, tables, indices and outputs off 16-byte alignment: the entry points
+    take their element-wise paths and give the same results."""
+    _, A, split, thr, lut, scale, offset = draw(seed)
+    A = np.ascontiguousarray(A)
+    N, C, M = A.shape[0], lut.shape[0], lut.shape[2]
+    Ad, lutd = shifted(A, torch.float32), shifted(lut, torch.int8)
+    y_out = torch.empty(N * M + 1, dtype=torch.float32, device=DEV)[1:].view(N, M)
+    y, _, _ = mdn.matmul(Ad, dev(split), dev(thr), lutd, dev(scale), dev(offset), y_out=y_out)
+    _, _, ry = orc.matmul(A, split, thr, lut, scale, offset)
+    assert np.array_equal(host(y), ry)
+    idx = W.random_indices(N, C, seed=9000 + seed)
+    idxd = shifted(idx, torch.uint8)
+    _, y = mdn.lut_accumulate(idxd, lutd, dev(scale), dev(offset), y_out=y_out)
+    assert np.array_equal(host(y), orc.lut_accumulate(idx, lut, scale, offset)[1])
+    tab = W.random_fp32_table(C, M, seed=9500 + seed)
+    y = mdn.lut_accumulate_f32(idxd, shifted(tab, torch.float32), y_out=y_out)
+    assert np.array_equal(host(y), orc.lut_accumulate_f32(idx, tab))
