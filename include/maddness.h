@@ -20,8 +20,9 @@
  *    calls only enqueue work on it: no host synchronisation.  Only the fused
  *    entry points (maddness_matmul, maddness_matmul_f32, maddness_matmul_act,
  *    maddness_matmul_act_f32) may allocate (stream-ordered) a temporary index
- *    buffer, when the table is too large for one LDS tile (and, for the first
- *    two, idx_out is NULL); every other call allocates nothing.
+ *    buffer, when the table is too large for one LDS tile and idx_out is
+ *    NULL; every other call allocates nothing (and can be captured in a HIP
+ *    graph).
  *  - Row-major layouts.  A has row stride `lda` (elements, lda >= D); every
  *    other array is dense.
  *  - Return value: MADDNESS_OK or an error status (never aborts, never
@@ -185,21 +186,23 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda,
  *                         fp32 (expf, any summation order): each entry is
  *                         within (|z - max| + M + 5) * 2^-24 relative of the
  *                         exact value (plus underflow below 2^-126).
- * col_bias [M] fp32, 4-byte aligned.  EINVAL: act outside 0..3, plus the
+ * col_bias [M] fp32, 4-byte aligned.  idx_out [N][C] (nullable) receives the
+ * indices as for maddness_matmul.  EINVAL: act outside 0..3, plus the
  * conditions of maddness_matmul; ENOMEM as for maddness_matmul.
  */
 int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda,
                         const int32_t* split_dims, const float* thresholds,
                         int32_t C, const int8_t* lut, const float* scale,
                         const float* offset, int32_t M, const float* col_bias,
-                        int32_t act, float* y_out, void* stream);
+                        int32_t act, float* y_out, uint8_t* idx_out,
+                        void* stream);
 
 /* The same with an unquantized fp32 table (see maddness_matmul_f32). */
 int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda,
                             const int32_t* split_dims, const float* thresholds,
                             int32_t C, const float* lut, int32_t M,
                             const float* col_bias, int32_t act, float* y_out,
-                            void* stream);
+                            uint8_t* idx_out, void* stream);
 
 /*
  * Offline table construction (§2.2: T = P B) followed by 8-bit block

@@ -47,8 +47,8 @@ def lib() -> ctypes.CDLL:
         L.maddness_lut_accumulate_f32.argtypes = [vp, i64, i32, vp, i32, vp, vp]
         L.maddness_matmul.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp]
         L.maddness_matmul_f32.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, i32, vp, vp, vp]
-        L.maddness_matmul_act.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, vp, vp, i32, vp, i32, vp, vp]
-        L.maddness_matmul_act_f32.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, i32, vp, i32, vp, vp]
+        L.maddness_matmul_act.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, vp, vp, i32, vp, i32, vp, vp, vp]
+        L.maddness_matmul_act_f32.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, i32, vp, i32, vp, vp, vp]
         L.maddness_lut_accumulate_avg.argtypes = [vp, i64, i32, vp, vp, vp, i32, vp, vp, vp]
         L.maddness_build_lut_shared.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, vp]
         L.maddness_build_lut.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, vp]

@@ -202,6 +202,7 @@ def matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, acc_out=No
         acc_out = torch.empty((N, M), dtype=torch.int32, device=dev)
     if idx_out is None and want_idx:
         idx_out = torch.empty((N, C), dtype=torch.uint8, device=dev)
+    idx_out = _idx_out(idx_out, N, C)
     st = _lib.lib().maddness_matmul(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
                                     _ptr(lut), _ptr(scale), _ptr(offset), M, _ptr(y_out),
                                     _ptr(acc_out), _ptr(idx_out), _stream(stream))
@@ -225,6 +226,7 @@ def matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None, want_id
         y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
     if idx_out is None and want_idx:
         idx_out = torch.empty((N, C), dtype=torch.uint8, device=A.device)
+    idx_out = _idx_out(idx_out, N, C)
     st = _lib.lib().maddness_matmul_f32(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
                                         _ptr(lut), M, _ptr(y_out), _ptr(idx_out), _stream(stream))
     _lib.check("maddness_matmul_f32", st)
@@ -252,10 +254,20 @@ def _col_bias(col_bias, M):
     return col_bias
 
 
+def _idx_out(idx_out, N, C):
+    if idx_out is not None:
+        _need(idx_out, "idx_out", torch.uint8, 2)
+        _dense(idx_out, "idx_out")
+        if tuple(idx_out.shape) != (N, C):
+            raise ValueError("idx_out must be [N, C]")
+    return idx_out
+
+
 def matmul_act(A, split_dims, thresholds, lut, scale, offset, col_bias=None, act="relu", y_out=None,
-               stream=None, validate=False):
+               idx_out=None, stream=None, validate=False):
     """Fused encode + lookup-accumulate + layer output sigma (bias, then
-    "relu" / "softmax"; "bias" or "none" also accepted); returns y."""
+    "relu" / "softmax"; "bias" or "none" also accepted); returns y.  With
+    idx_out the indices are written there (and nothing is allocated)."""
     N, D, lda = _rows(A)
     C = _tree_args(split_dims, thresholds)
     C2, M = _lut_i8(lut, scale, offset)
@@ -269,15 +281,16 @@ def matmul_act(A, split_dims, thresholds, lut, scale, offset, col_bias=None, act
         y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
     _need(y_out, "y_out", torch.float32, 2)
     _dense(y_out, "y_out")
+    idx_out = _idx_out(idx_out, N, C)
     st = _lib.lib().maddness_matmul_act(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut),
                                         _ptr(scale), _ptr(offset), M, _ptr(col_bias), _act(act), _ptr(y_out),
-                                        _stream(stream))
+                                        _ptr(idx_out), _stream(stream))
     _lib.check("maddness_matmul_act", st)
     return y_out
 
 
-def matmul_act_f32(A, split_dims, thresholds, lut, col_bias=None, act="relu", y_out=None, stream=None,
-                   validate=False):
+def matmul_act_f32(A, split_dims, thresholds, lut, col_bias=None, act="relu", y_out=None, idx_out=None,
+                   stream=None, validate=False):
     """matmul_act over an unquantized fp32 table; returns y."""
     N, D, lda = _rows(A)
     C = _tree_args(split_dims, thresholds)
@@ -293,8 +306,10 @@ def matmul_act_f32(A, split_dims, thresholds, lut, col_bias=None, act="relu", y_
         y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
     _need(y_out, "y_out", torch.float32, 2)
     _dense(y_out, "y_out")
+    idx_out = _idx_out(idx_out, N, C)
     st = _lib.lib().maddness_matmul_act_f32(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
-                                            _ptr(lut), M, _ptr(col_bias), _act(act), _ptr(y_out), _stream(stream))
+                                            _ptr(lut), M, _ptr(col_bias), _act(act), _ptr(y_out),
+                                            _ptr(idx_out), _stream(stream))
     _lib.check("maddness_matmul_act_f32", st)
     return y_out
 

@@ -542,7 +542,7 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda, const
 int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
                         const float* thresholds, int32_t C, const int8_t* lut, const float* scale,
                         const float* offset, int32_t M, const float* col_bias, int32_t act, float* y_out,
-                        void* stream) {
+                        uint8_t* idx_out, void* stream) {
   if (act < MADDNESS_ACT_NONE || act > MADDNESS_ACT_SOFTMAX) return MADDNESS_EINVAL;
   int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
   if (rc != MADDNESS_OK) return rc;
@@ -554,18 +554,18 @@ int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda, const
   Shape s = shape(kFused, kI8);
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out;
-  s.col_bias = col_bias; s.act = act;
+  s.col_bias = col_bias; s.act = act; s.idx_out = idx_out;
   hipStream_t st = static_cast<hipStream_t>(stream);
   GArgs g;
   int ng, uq, nw;
   if (plan_gfused(s, &g, &ng, &uq, &nw))
     return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
-  return two_phase(s, nullptr, st);
+  return two_phase(s, idx_out, st);
 }
 
 int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
                             const float* thresholds, int32_t C, const float* lut, int32_t M,
-                            const float* col_bias, int32_t act, float* y_out, void* stream) {
+                            const float* col_bias, int32_t act, float* y_out, uint8_t* idx_out, void* stream) {
   if (act < MADDNESS_ACT_NONE || act > MADDNESS_ACT_SOFTMAX) return MADDNESS_EINVAL;
   int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
   if (rc != MADDNESS_OK) return rc;
@@ -576,13 +576,13 @@ int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda, c
   Shape s = shape(kFused, kF32);
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.M = M; s.y = y_out;
-  s.col_bias = col_bias; s.act = act;
+  s.col_bias = col_bias; s.act = act; s.idx_out = idx_out;
   hipStream_t st = static_cast<hipStream_t>(stream);
   GArgs g;
   int ng, uq, nw;
   if (plan_gfused(s, &g, &ng, &uq, &nw))
     return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
-  return two_phase(s, nullptr, st);
+  return two_phase(s, idx_out, st);
 }
 
 int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D, int32_t M, int8_t* lut_out,

@@ -89,7 +89,7 @@ def test_matmul_rejects(L):
 
 def test_matmul_act_rejects(L):
     Ma = L.maddness_matmul_act
-    args = [FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, NULL, 2, FAKE, NULL]
+    args = [FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, NULL, 2, FAKE, NULL, NULL]
     for bad_act in (-1, 4):
         bad = list(args); bad[12] = bad_act
         assert Ma(*bad) == 1
@@ -102,8 +102,8 @@ def test_matmul_act_rejects(L):
     zero = list(args); zero[1] = 0                        # N == 0
     assert Ma(*zero) == 0
     F = L.maddness_matmul_act_f32
-    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 7, FAKE, NULL) == 1
-    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 3, NULL, NULL) == 1
+    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 7, FAKE, NULL, NULL) == 1
+    assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, 3, NULL, NULL, NULL) == 1
 
 
 def test_accumulate_avg_rejects(L):
