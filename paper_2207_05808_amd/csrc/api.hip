@@ -302,6 +302,35 @@ bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
   return true;
 }
 
+// Row-uniform accumulate (tiled_accum.hip) for int8 tables at least 512
+// columns wide: scalar loads of 4-byte index words (C % 4 == 0), 16-byte
+// output stores, and enough 256-row work items to occupy a quarter of the CUs.
+bool plan_trow(const Shape& s, TArgs* t) {
+  if (s.elem != kI8 || s.M < kRowTileCols || s.M % 4 != 0 || s.C % 4 != 0) return false;
+  if (!aligned(s.idx_in, 4) || !aligned(s.lut, 4)) return false;
+  if ((s.y && !aligned(s.y, 16)) || (s.acc && !aligned(s.acc, 16))) return false;
+  if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;   // 32-bit buffer offsets
+  TArgs a{};
+  a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;
+  a.N = s.N; a.C = s.C; a.M = s.M;
+  a.Mt = kRowTileCols;
+  a.RB = 256;
+  a.ntm = (s.M + kRowTileCols - 1) / kRowTileCols;
+  a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
+  if (a.nwork * 4 < device_cus()) return false;
+  a.col_bias = s.col_bias;
+  a.act = (s.act == 3 && a.ntm > 1) ? 1 : s.act;   // rows over several tiles: softmax as a second pass
+  int off = 0;
+  auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
+  a.off_tab = take(8 * kK * 2 * kRowTileCols);   // 0: the kernel relies on it
+  a.off_sh = take(s.C * 4);
+  a.off_misc = take(16);
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  *t = a;
+  return true;
+}
+
 int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   Plan p;
   const int rc = plan(s, &p, single_tile_only);
@@ -358,6 +387,11 @@ bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
 int accumulate(const Shape& s, hipStream_t stream) {
   TArgs t;
   int nj, nw;
+  if (plan_trow(s, &t)) {
+    const int rc = status_from(launch_trow(t, device_cus(), stream));
+    if (rc != MADDNESS_OK || t.act == s.act) return rc;
+    return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
+  }
   if (plan_tacc(s, &t, &nj, &nw)) {
     const int rc = status_from(launch_tacc(s.elem, nj, t, nw, device_cus(), stream));
     if (rc != MADDNESS_OK || t.act == s.act) return rc;

@@ -365,6 +365,271 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
   else run(std::integral_constant<int, 2>{});
 }
 
+// Row-uniform accumulate for int8 tables with at least 512 columns (the same
+// sum as tacc_kernel).  A wavefront sums one output row at a time over a
+// 512-column slice; lane l owns output columns 4l..4l+3 and 256+4l..256+4l+3
+// of the slice, held as eight 16-bit entries in a 16-byte slot of each staged
+// table row.  The table row that a codebook selects is then the same for the
+// whole wavefront: the row's index bytes come from scalar loads, a lookup is
+// a uniform row offset added to the lane's slot plus one 16-byte LDS read,
+// no index tile goes through LDS, and every output store instruction writes
+// 1 KB of one row.
+//
+// A work item is RB rows x 512 columns; the table is staged 8 codebooks at a
+// time ([8 x 16 rows][512 entries], 128 KB of LDS, one 1024-thread workgroup
+// per CU), the next tile loaded into registers while the current one is
+// summed.
+//  * When 255 * sum_c 2^(e_c - e_min) <= 65535, an entry is staged as the
+//    unsigned u = (q + 128) << (e_c - e_min): no 16-bit field can carry into
+//    the next while the codebooks are summed, so one 32-bit add sums two
+//    columns and v_add3_u32 adds two codebooks; the int32 sum is the field
+//    minus 128 * sum_c 2^(e_c - e_min).  16 rows per wavefront.
+//  * Otherwise entries are staged as signed q and summed in int32 with the
+//    shifts, 8 rows per wavefront.
+constexpr int kRowWaves = 16;           // wavefronts per workgroup
+constexpr int kRowCT = 8;               // codebooks per staged tile
+constexpr int kRowMt = 512;             // columns per work item
+constexpr int kRowBytes = 2 * kRowMt;   // LDS bytes per staged table row
+constexpr int kRowQ = 16;               // 4-column quads staged per thread per tile
+constexpr int kRowJG = 2;               // rows summed between scheduling barriers
+
+__global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t* __restrict__ idx) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  tlds_t* smem = (tlds_t*)smem_raw;
+  typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t tu32x2 __attribute__((ext_vector_type(2)));
+  typedef __attribute__((address_space(3))) tu32x2 tlds_u32x2;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tuni(tid >> 6);
+  const int C = a.C, M = a.M, ntm = a.ntm;
+  const int64_t N = a.N;
+  tlds_t* s_tab = smem;   // off_tab == 0
+  tlds_i32* s_sh = reinterpret_cast<tlds_i32*>(smem + a.off_sh);
+  tlds_i32* s_misc = reinterpret_cast<tlds_i32*>(smem + a.off_misc);   // bias32, e_min, sum of 2^sh, max shift
+
+  // ---------------- block exponents, shifts and bias32
+  if (tid == 0) { s_misc[1] = INT_MAX; s_misc[2] = 0; s_misc[3] = 0; }
+  __syncthreads();
+  const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
+  for (int c = tid; c < C; c += kRowWaves * 64) atomicMin((int*)&s_misc[1], (int)((sb[c] >> 23) & 0xffu) - 127);
+  __syncthreads();
+  const int emin = tuni(s_misc[1]);
+  for (int c = tid; c < C; c += kRowWaves * 64) {
+    const int sh = min((int)((sb[c] >> 23) & 0xffu) - 127 - emin, 30);
+    s_sh[c] = sh;
+    atomicAdd((int*)&s_misc[2], sh <= 14 ? (1 << sh) : (1 << 15));
+    atomicMax((int*)&s_misc[3], sh);
+  }
+  if (wave == 0) {
+    // bias32: double sum over codebooks in ascending order
+    double sum = 0.0;
+    for (int c0 = 0; c0 < C; c0 += 64) {
+      const float ov = a.offset[min(c0 + lane, C - 1)];
+      const int n = min(64, C - c0);
+      for (int j = 0; j < n; ++j) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), j));
+    }
+    if (lane == 0) s_misc[0] = __float_as_int((float)sum);
+  }
+  __syncthreads();
+  const int S = tuni(s_misc[2]);        // sum of 2^sh (saturated per codebook at 2^15)
+  const bool fields = S <= 257;         // 255 * S <= 65535
+  const bool shifted = tuni(s_misc[3]) != 0;
+  const float step = __builtin_ldexpf(1.0f, emin);
+  const float bias = __int_as_float(tuni(s_misc[0]));
+
+  // ---------------- staging: thread t moves quad (t % 128) of staged rows
+  // t / 128 + 8 j, j < 16 (4 codes -> 8 bytes of its lane slot)
+  const int tq = tid & 127;
+  const int tr = tid >> 7;
+  const int slot = ((tq & 63) << 4) + ((tq >> 6) << 3);
+  const __amdgpu_buffer_rsrc_t trs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M), kBufDword3);
+  uint32_t tv[kRowQ];
+  // (the lane bases are re-derived per tile through an empty asm, so the
+  // compiler does not keep one precomputed address per j in registers)
+  auto load_tile = [&](int c0, int m0) {
+    const int m = m0 + 4 * tq;
+    int base = tr * M + m;   // staged row tr of the tile, this thread's quad
+    asm volatile("" : "+v"(base));
+    const bool full = c0 + kRowCT <= C;   // else 4 codebooks: rows 64.. of the tile are not read
+#pragma unroll
+    for (int j = 0; j < kRowQ; ++j) {
+      // staged row tr + 8 j: codebook c0 + j / 2, prototype (tr + 8 j) % 16
+      const bool ok = (j < kRowQ / 2 || full) && m < M;
+      tv[j] = __builtin_amdgcn_raw_buffer_load_b32(trs, ok ? base + (c0 * 16 + 8 * j) * M : kOob, 0, 0);
+    }
+  };
+  auto store_tile = [&](int c0) {
+    int base = tr * kRowBytes + slot;
+    asm volatile("" : "+v"(base));
+#pragma unroll
+    for (int j = 0; j < kRowQ; ++j) {
+      uint32_t lo, hi;
+      if (fields) {
+        const uint32_t u = tv[j] ^ 0x80808080u;   // q + 128 per byte
+        lo = __builtin_amdgcn_perm(0u, u, 0x0c010c00u);
+        hi = __builtin_amdgcn_perm(0u, u, 0x0c030c02u);
+        if (shifted) {
+          const unsigned short sh = (unsigned short)s_sh[min(c0 + (j >> 1), C - 1)];
+          const us2 s = {sh, sh};
+          lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, lo) << s);
+          hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, hi) << s);
+        }
+      } else {
+        widen4(tv[j], 0, lo, hi);
+      }
+      *reinterpret_cast<tlds_u32x2*>(s_tab + base + 8 * j * kRowBytes) = (tu32x2){lo, hi};
+    }
+  };
+
+  const tlds_t* s_lane = s_tab + lane * 16;
+  auto run = [&](auto nj_tag) {
+    constexpr int NJ = decltype(nj_tag)::value;   // 16: 16-bit fields; 8: int32 sums
+    constexpr bool F = NJ == 16;
+    constexpr int NA = F ? 4 : 8;
+    const int RB = kRowWaves * NJ;
+    const int64_t nwork = (int64_t)ntm * ((N + RB - 1) / RB);
+    for (int64_t w = blockIdx.x; w < nwork; w += gridDim.x) {
+      const int mt = (int)(w % ntm);
+      const int64_t r0 = (w / ntm) * RB + (int64_t)wave * NJ;   // this wavefront's first row
+      const int m0 = mt * kRowMt;
+      uint32_t acc[NJ][NA];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int e = 0; e < NA; ++e) acc[j][e] = 0u;
+
+      load_tile(0, m0);
+      for (int c0 = 0; c0 < C; c0 += kRowCT) {
+        __syncthreads();   // every reader of the previous tile is done
+        store_tile(c0);
+        __syncthreads();
+        if (c0 + kRowCT < C) load_tile(c0 + kRowCT, m0);   // in flight during the sums below
+        const bool full = c0 + kRowCT <= C;                // else 4 codebooks (C % 4 == 0)
+        uint32_t d0[NJ], d1[NJ];   // index bytes of codebooks c0..c0+3 and c0+4..c0+7 (uniform)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const uint8_t* p = idx + min(r0 + j, N - 1) * C + c0;   // rows past N: any valid row
+          d0[j] = *reinterpret_cast<const uint32_t*>(p);
+          d1[j] = full ? *reinterpret_cast<const uint32_t*>(p + 4) : 0u;
+        }
+        // rows go kRowJG at a time between scheduling barriers, which bound
+        // the LDS reads (and row offsets) held in registers
+        if (F) {
+#pragma unroll
+          for (int cp = 0; cp < kRowCT; cp += 2) {
+            if (cp < 4 || full) {
+#pragma unroll
+              for (int j = 0; j < NJ; ++j) {
+                if (j % kRowJG == 0) __builtin_amdgcn_sched_barrier(0);
+                const uint32_t dw = cp < 4 ? d0[j] : d1[j];
+                const int k0 = (dw >> (8 * (cp & 3))) & 15, k1 = (dw >> (8 * ((cp + 1) & 3))) & 15;
+                const tu32x4 v0 = *reinterpret_cast<const tlds_u32x4*>(s_lane + ((cp * 16 + k0) << 10));
+                const tu32x4 v1 = *reinterpret_cast<const tlds_u32x4*>(s_lane + (((cp + 1) * 16 + k1) << 10));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  acc[j][e] += v0[e] + v1[e];
+                  asm volatile("" : "+v"(acc[j][e]));   // no reassociation across codebook pairs
+                }
+              }
+            }
+          }
+        } else {
+#pragma unroll
+          for (int cc = 0; cc < kRowCT; ++cc) {
+            if (cc < 4 || full) {
+              const int sh = tuni(s_sh[c0 + cc]);
+#pragma unroll
+              for (int j = 0; j < NJ; ++j) {
+                if (j % kRowJG == 0) __builtin_amdgcn_sched_barrier(0);
+                const uint32_t dw = cc < 4 ? d0[j] : d1[j];
+                const int k = (dw >> (8 * (cc & 3))) & 15;
+                const tu32x4 v = *reinterpret_cast<const tlds_u32x4*>(s_lane + ((cc * 16 + k) << 10));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  acc[j][2 * e] += (uint32_t)(__builtin_amdgcn_sbfe((int)v[e], 0, 16) << sh);
+                  acc[j][2 * e + 1] += (uint32_t)(((int)v[e] >> 16) << sh);
+                  asm volatile("" : "+v"(acc[j][2 * e]), "+v"(acc[j][2 * e + 1]));
+                }
+              }
+            }
+          }
+        }
+      }
+
+      // ---------------- epilogue: outputs i < 4 are columns colA + i, the rest colB + i - 4
+      const int colA = m0 + 4 * lane, colB = colA + 256;
+      float cb[8];   // this lane's column biases, loaded once per work item (stores to y may alias them)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int col = (i < 4 ? colA : colB - 4) + i;
+        cb[i] = (a.act != 0 && a.col_bias && col < M) ? a.col_bias[col] : 0.0f;
+      }
+      const int off128 = F ? 128 * S : 0;   // S <= 257 in field mode
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int64_t row = r0 + j;
+        int out[8];
+        float yv[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (F) {
+            out[2 * e] = (int)(acc[j][e] & 0xffffu) - off128;
+            out[2 * e + 1] = (int)(acc[j][e] >> 16) - off128;
+          } else {
+            out[2 * e] = (int)acc[j][2 * e];
+            out[2 * e + 1] = (int)acc[j][2 * e + 1];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) yv[i] = __builtin_fmaf((float)out[i], step, bias);
+        if (a.act != 0) {
+          // layer output sigma: z = y + bias, then ReLU, or a softmax over the
+          // row (one column tile: the whole row is in this wavefront)
+          float vmax = -__builtin_inff();
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const bool ok = (i < 4 ? colA : colB - 4) + i < M;
+            float z = yv[i] + cb[i];
+            if (a.act == 2) z = (z > 0.0f) ? z : 0.0f;
+            yv[i] = z;
+            if (ok) vmax = __builtin_fmaxf(vmax, z);
+          }
+          if (a.act == 3) {
+            for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+            float sum = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              yv[i] = ((i < 4 ? colA : colB - 4) + i < M) ? expf(yv[i] - vmax) : 0.0f;
+              sum += yv[i];
+            }
+            for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) yv[i] = yv[i] / sum;
+          }
+        }
+        if (row >= N) continue;   // uniform: one row per wavefront
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int col = h ? colB : colA;
+          if (col >= M) continue;
+          if (a.y)
+            __builtin_nontemporal_store((tf32x4){yv[4 * h], yv[4 * h + 1], yv[4 * h + 2], yv[4 * h + 3]},
+                                        reinterpret_cast<tf32x4*>(a.y + row * M + col));
+          if (a.acc)
+            __builtin_nontemporal_store((tu32x4){(uint32_t)out[4 * h], (uint32_t)out[4 * h + 1],
+                                                 (uint32_t)out[4 * h + 2], (uint32_t)out[4 * h + 3]},
+                                        reinterpret_cast<tu32x4*>(a.acc + row * M + col));
+        }
+      }
+    }
+  };
+  if (fields) run(std::integral_constant<int, 16>{});
+  else run(std::integral_constant<int, 8>{});
+}
+
 // Rounded 8-bit summation over codebooks (§1 names it; reading R20): the
 // codes of a row, biased to bytes u = q + 128 and padded with 128 to P = 2^L
 // codebooks, are reduced by a balanced tree of rounded byte averages in
@@ -793,6 +1058,19 @@ static hipError_t launch_tavg_nt(const TArgs& t, int cus, hipStream_t stream) {
 hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream) {
   if (nw == 8) return launch_tavg_nt<512>(t, cus, stream);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_trow(const TArgs& t, int cus, hipStream_t stream) {
+  const void* fn = reinterpret_cast<const void*>(&trow_kernel);
+  hipError_t err = hipSuccess;
+  const int per_cu = t_prepare(fn, kRowWaves * 64, t.lds_total, &err);
+  if (err != hipSuccess) return err;
+  int64_t blocks = t.nwork;   // work items at 16 rows per wavefront (the kernel recounts for 8)
+  const int64_t resident = (int64_t)per_cu * cus;
+  if (blocks > resident) blocks = resident;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(trow_kernel, dim3((unsigned)blocks), dim3(kRowWaves * 64), t.lds_total, stream, t, t.idx);
+  return hipGetLastError();
 }
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream) {

@@ -1,0 +1,124 @@
+"""Parity of the row-uniform accumulate with the oracle.
+
+The dispatcher takes that kernel for int8 tables at least 512 columns wide
+(C % 4 == 0, aligned buffers) once the 256-row work items fill a quarter of
+the CUs, so every case here has N >= 16384 / (column tiles of 512): smaller
+calls take the column-tiled kernel that the other parity tests cover.  Both
+of its summation modes are exercised: 16-bit fields of (q + 128) << sh when
+255 * sum_c 2^sh <= 65535 (including that bound exactly, with every code at
++127 or -128), and int32 sums with shifts otherwise.  Bar as in the other
+parity tests: int32 sums and fp32 outputs bit-exact; softmax within the
+bound of the sigma tests."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2207_05808_amd as mdn
+from paper_2207_05808_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def rows_for(M):
+    """Rows that reach the row-uniform kernel: 64 work items of 256 rows x
+    512 columns, plus a ragged tail."""
+    tiles = -(-M // 512)
+    return -(-64 // tiles) * 256 + 77
+
+
+def check_accumulate(orc, idx, lut, scale, offset):
+    acc, y = mdn.lut_accumulate(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=True, validate=True)
+    racc, ry = orc.lut_accumulate(idx, lut, scale, offset)
+    assert np.array_equal(host(acc), racc)
+    assert np.array_equal(host(y), ry)
+
+
+# (C, M, max_shift): sum_c 2^sh <= 257 takes the 16-bit fields, else int32 sums
+ROW_CASES = [(64, 512, 0), (64, 512, 2), (64, 512, 5), (32, 1000, 3), (4, 512, 0), (12, 768, 1),
+             (128, 4096, 0), (256, 512, 0), (260, 512, 0), (512, 512, 0), (8, 2048, 7)]
+
+
+@pytest.mark.parametrize("C,M,max_shift", ROW_CASES)
+def test_row_accumulate_random(orc, C, M, max_shift):
+    N = rows_for(M)
+    idx = W.random_indices(N, C, seed=C * 31 + M)
+    lut, scale, offset = W.random_codes(C, M, seed=C + 7 * M + max_shift, max_shift=max_shift)
+    check_accumulate(orc, idx, lut, scale, offset)
+
+
+@pytest.mark.parametrize("code", [127, -128, -127])
+@pytest.mark.parametrize("shifts", [(7, 6, 6, 0), (7, 6, 6, 1)])
+def test_row_accumulate_field_bound(orc, code, shifts):
+    """sum 2^sh = 257: every 16-bit field reaches 255 * 257 = 65535 (codes
+    +127) or 0 (codes -128); 258 is the first sum that takes int32 sums."""
+    C, M = 4, 512
+    N = rows_for(M)
+    idx = W.random_indices(N, C, seed=sum(shifts) + code + 200)
+    lut = np.full((C, 16, M), code, dtype=np.int8)
+    lut[:, 3, ::7] = -code if code != -128 else 127   # a few other codes
+    scale = np.ldexp(np.float32(1.0), np.array(shifts, dtype=np.int32) - 9).astype(np.float32)
+    offset = np.random.default_rng(3).standard_normal(C).astype(np.float32)
+    check_accumulate(orc, idx, lut, scale, offset)
+
+
+def test_row_accumulate_single_outputs(orc):
+    C, M = 64, 512
+    N = rows_for(M)
+    idx = W.random_indices(N, C, seed=11)
+    lut, scale, offset = W.random_codes(C, M, seed=12, max_shift=1)
+    racc, ry = orc.lut_accumulate(idx, lut, scale, offset)
+    acc, y = mdn.lut_accumulate(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=True, want_y=False)
+    assert y is None and np.array_equal(host(acc), racc)
+    acc, y = mdn.lut_accumulate(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=False, want_y=True)
+    assert acc is None and np.array_equal(host(y), ry)
+
+
+@pytest.mark.parametrize("name,N", [("dense_hidden", 16411), ("wide_layer", 2100)])
+def test_row_matmul_workloads(orc, name, N):
+    """Encode, then the row-uniform accumulate (tables larger than LDS)."""
+    p = W.make(name, N=N)
+    lut, scale, offset = mdn.build_lut(dev(p.P), dev(p.B))
+    rl, rs, ro = orc.build_quantized_lut(p.P, p.B)
+    y, acc, idx = mdn.matmul(dev(p.A), dev(p.split), dev(p.thr), lut, scale, offset, want_acc=True,
+                             want_idx=True)
+    ridx, racc, ry = orc.matmul(p.A, p.split, p.thr, rl, rs, ro)
+    assert np.array_equal(host(idx), ridx)
+    assert np.array_equal(host(acc), racc)
+    assert np.array_equal(host(y), ry)
+
+
+@pytest.mark.parametrize("M", [512, 1024])
+@pytest.mark.parametrize("act", ["bias", "relu", "softmax"])
+def test_row_layer_output(orc, M, act):
+    """matmul_act with a table larger than LDS: encode, then sigma in the
+    row-uniform kernel's epilogue (one column tile: M = 512), or bias there
+    and the row softmax as a second pass (M = 1024)."""
+    C, D = 64, 96
+    N = rows_for(M)
+    rng = np.random.default_rng(M + len(act))
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
+    thr = rng.standard_normal((C, 15), dtype=np.float32)
+    lut, scale, offset = W.random_codes(C, M, seed=M + 1, max_shift=2)
+    bias = rng.standard_normal(M).astype(np.float32)
+    code = {"bias": 1, "relu": 2, "softmax": 3}[act]
+    y = host(mdn.matmul_act(dev(A), dev(split), dev(thr), dev(lut), dev(scale), dev(offset),
+                            col_bias=dev(bias), act=act))
+    _, _, yref = orc.matmul(A, split, thr, lut, scale, offset)
+    ref = orc.sigma(yref, bias, code)
+    if act != "softmax":
+        assert np.array_equal(y.astype(np.float64), ref)
+        return
+    z = orc.sigma(yref, bias, 1)
+    tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + M + 5) * 2.0 ** -24 * ref + 2.0 ** -120
+    assert np.all(np.abs(y.astype(np.float64) - ref) <= tol)
