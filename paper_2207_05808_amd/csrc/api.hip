@@ -303,10 +303,11 @@ bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
 }
 
 // Row-uniform accumulate (tiled_accum.hip) for int8 tables at least 512
-// columns wide: scalar loads of 4-byte index words (C % 4 == 0), 16-byte
-// output stores, and enough 256-row work items to occupy a quarter of the CUs.
+// columns wide: scalar loads of 4-byte index words (C % 4 == 0), table rows in
+// whole 16-byte units (M % 16 == 0), 16-byte output stores, and enough
+// 256-row work items to occupy a quarter of the CUs.
 bool plan_trow(const Shape& s, TArgs* t) {
-  if (s.elem != kI8 || s.M < kRowTileCols || s.M % 4 != 0 || s.C % 4 != 0) return false;
+  if (s.elem != kI8 || s.M < kRowTileCols || s.M % 16 != 0 || s.C % 4 != 0) return false;
   if (!aligned(s.idx_in, 4) || !aligned(s.lut, 4)) return false;
   if ((s.y && !aligned(s.y, 16)) || (s.acc && !aligned(s.acc, 16))) return false;
   if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;   // 32-bit buffer offsets

@@ -390,7 +390,6 @@ constexpr int kRowWaves = 16;           // wavefronts per workgroup
 constexpr int kRowCT = 8;               // codebooks per staged tile
 constexpr int kRowMt = 512;             // columns per work item
 constexpr int kRowBytes = 2 * kRowMt;   // LDS bytes per staged table row
-constexpr int kRowQ = 16;               // 4-column quads staged per thread per tile
 constexpr int kRowJG = 2;               // rows summed between scheduling barriers
 
 __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t* __restrict__ idx) {
@@ -439,52 +438,79 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
   const float step = __builtin_ldexpf(1.0f, emin);
   const float bias = __int_as_float(tuni(s_misc[0]));
 
-  // ---------------- staging: thread t moves quad (t % 128) of staged rows
-  // t / 128 + 8 j, j < 16 (4 codes -> 8 bytes of its lane slot)
-  const int tq = tid & 127;
-  const int tr = tid >> 7;
-  const int slot = ((tq & 63) << 4) + ((tq >> 6) << 3);
+  // ---------------- staging.  Lane l = 16 a + 4 b + c's 16-byte slot
+  // (columns 4l..4l+3 and 256+4l..256+4l+3) sits at position 16 a + 4 b +
+  // (c + a) % 4 of each staged row: the 16 lanes of a read pass (fixed a)
+  // cover one 256-byte span, and so do the 16 threads of a write pass below
+  // (fixed c).  Thread t stages, for staged rows t / 16 + 64 j (j < 2), the
+  // 16 columns 16 (t % 16).. of each half of the slice: two 16-byte loads,
+  // the four whole slots of lanes 4 (t % 16) + c.
+  const int tp = tid & 15;
+  const int tr = tid >> 4;
   const __amdgpu_buffer_rsrc_t trs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M), kBufDword3);
-  uint32_t tv[kRowQ];
+  tu32x4 tv[4];   // [row j][half h]
   // (the lane bases are re-derived per tile through an empty asm, so the
   // compiler does not keep one precomputed address per j in registers)
   auto load_tile = [&](int c0, int m0) {
-    const int m = m0 + 4 * tq;
-    int base = tr * M + m;   // staged row tr of the tile, this thread's quad
+    int base = tr * M + m0 + 16 * tp;   // staged row tr of the tile, first half
     asm volatile("" : "+v"(base));
-    const bool full = c0 + kRowCT <= C;   // else 4 codebooks: rows 64.. of the tile are not read
+    const bool full = c0 + kRowCT <= C;   // else 4 codebooks: staged rows 64.. are not read
 #pragma unroll
-    for (int j = 0; j < kRowQ; ++j) {
-      // staged row tr + 8 j: codebook c0 + j / 2, prototype (tr + 8 j) % 16
-      const bool ok = (j < kRowQ / 2 || full) && m < M;
-      tv[j] = __builtin_amdgcn_raw_buffer_load_b32(trs, ok ? base + (c0 * 16 + 8 * j) * M : kOob, 0, 0);
-    }
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // staged row tr + 64 j: codebook c0 + tr / 16 + 4 j (M % 16 == 0: units are whole)
+        const bool ok = (j == 0 || full) && m0 + 256 * h + 16 * tp < M;
+        tv[2 * j + h] = __builtin_amdgcn_raw_buffer_load_b128(
+            trs, ok ? base + (c0 * 16 + 64 * j) * M + 256 * h : kOob, 0, 0);
+      }
   };
   auto store_tile = [&](int c0) {
-    int base = tr * kRowBytes + slot;
+    int base = tr * kRowBytes + tp * 64;   // slot 4 tp + i at position 4 tp + (i + tp / 4) % 4
     asm volatile("" : "+v"(base));
 #pragma unroll
-    for (int j = 0; j < kRowQ; ++j) {
-      uint32_t lo, hi;
-      if (fields) {
-        const uint32_t u = tv[j] ^ 0x80808080u;   // q + 128 per byte
-        lo = __builtin_amdgcn_perm(0u, u, 0x0c010c00u);
-        hi = __builtin_amdgcn_perm(0u, u, 0x0c030c02u);
-        if (shifted) {
-          const unsigned short sh = (unsigned short)s_sh[min(c0 + (j >> 1), C - 1)];
-          const us2 s = {sh, sh};
-          lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, lo) << s);
-          hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, hi) << s);
+    for (int j = 0; j < 2; ++j) {
+      const unsigned short sh = (fields && shifted) ? (unsigned short)s_sh[min(c0 + (tr >> 4) + 4 * j, C - 1)] : 0;
+      const us2 s2 = {sh, sh};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t w[4];   // quad i of each half, 4 entries each
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t x = tv[2 * j + h][i];
+          uint32_t lo, hi;
+          if (fields) {
+            const uint32_t u = x ^ 0x80808080u;   // q + 128 per byte
+            lo = __builtin_amdgcn_perm(0u, u, 0x0c010c00u);
+            hi = __builtin_amdgcn_perm(0u, u, 0x0c030c02u);
+            if (shifted) {
+              lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, lo) << s2);
+              hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, hi) << s2);
+            }
+          } else {
+            widen4(x, 0, lo, hi);
+          }
+          w[2 * h] = lo;
+          w[2 * h + 1] = hi;
         }
-      } else {
-        widen4(tv[j], 0, lo, hi);
+        *reinterpret_cast<tlds_u32x4*>(s_tab + base + 64 * j * kRowBytes + 16 * ((i + (tp >> 2)) & 3)) =
+            (tu32x4){w[0], w[1], w[2], w[3]};
       }
-      *reinterpret_cast<tlds_u32x2*>(s_tab + base + 8 * j * kRowBytes) = (tu32x2){lo, hi};
     }
   };
 
-  const tlds_t* s_lane = s_tab + lane * 16;
+  // the lane's slot of staged row cb * 16 + k: (k << 10) + base in one
+  // v_lshl_add_u32 with the uniform code in a scalar register; codebooks 4..7
+  // of a tile start 64 KB further, past the reach of the 16-bit read offset
+  const uint32_t lane_lo =
+      (uint32_t)(uintptr_t)(s_tab + 16 * ((lane & ~3) + (((lane & 3) + (lane >> 4)) & 3)));
+  const uint32_t lane_hi = lane_lo + 4 * 16 * kRowBytes;
+  auto slot_of = [&](int cb, int k) -> const tlds_t* {
+    uint32_t a;
+    asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(a) : "s"(k), "v"(cb < 4 ? lane_lo : lane_hi));
+    return (const tlds_t*)(uintptr_t)a + (cb & 3) * 16 * kRowBytes;
+  };
   auto run = [&](auto nj_tag) {
     constexpr int NJ = decltype(nj_tag)::value;   // 16: 16-bit fields; 8: int32 sums
     constexpr bool F = NJ == 16;
@@ -522,17 +548,25 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
           for (int cp = 0; cp < kRowCT; cp += 2) {
             if (cp < 4 || full) {
 #pragma unroll
-              for (int j = 0; j < NJ; ++j) {
-                if (j % kRowJG == 0) __builtin_amdgcn_sched_barrier(0);
-                const uint32_t dw = cp < 4 ? d0[j] : d1[j];
-                const int k0 = (dw >> (8 * (cp & 3))) & 15, k1 = (dw >> (8 * ((cp + 1) & 3))) & 15;
-                const tu32x4 v0 = *reinterpret_cast<const tlds_u32x4*>(s_lane + ((cp * 16 + k0) << 10));
-                const tu32x4 v1 = *reinterpret_cast<const tlds_u32x4*>(s_lane + (((cp + 1) * 16 + k1) << 10));
+              for (int g = 0; g < NJ; g += kRowJG) {
+                // the reads of kRowJG rows are issued together, then summed
+                tu32x4 v0[kRowJG], v1[kRowJG];
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  acc[j][e] += v0[e] + v1[e];
-                  asm volatile("" : "+v"(acc[j][e]));   // no reassociation across codebook pairs
+                for (int jj = 0; jj < kRowJG; ++jj) {
+                  const uint32_t dw = cp < 4 ? d0[g + jj] : d1[g + jj];
+                  const int k0 = (dw >> (8 * (cp & 3))) & 15, k1 = (dw >> (8 * ((cp + 1) & 3))) & 15;
+                  v0[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp, k0));
+                  v1[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp + 1, k1));
                 }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int jj = 0; jj < kRowJG; ++jj)
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    acc[g + jj][e] += v0[jj][e] + v1[jj][e];
+                    asm("" : "+v"(acc[g + jj][e]));   // opaque: no reassociation across codebook pairs
+                  }
               }
             }
           }
@@ -542,17 +576,24 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
             if (cc < 4 || full) {
               const int sh = tuni(s_sh[c0 + cc]);
 #pragma unroll
-              for (int j = 0; j < NJ; ++j) {
-                if (j % kRowJG == 0) __builtin_amdgcn_sched_barrier(0);
-                const uint32_t dw = cc < 4 ? d0[j] : d1[j];
-                const int k = (dw >> (8 * (cc & 3))) & 15;
-                const tu32x4 v = *reinterpret_cast<const tlds_u32x4*>(s_lane + ((cc * 16 + k) << 10));
+              for (int g = 0; g < NJ; g += kRowJG) {
+                tu32x4 v[kRowJG];
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  acc[j][2 * e] += (uint32_t)(__builtin_amdgcn_sbfe((int)v[e], 0, 16) << sh);
-                  acc[j][2 * e + 1] += (uint32_t)(((int)v[e] >> 16) << sh);
-                  asm volatile("" : "+v"(acc[j][2 * e]), "+v"(acc[j][2 * e + 1]));
+                for (int jj = 0; jj < kRowJG; ++jj) {
+                  const uint32_t dw = cc < 4 ? d0[g + jj] : d1[g + jj];
+                  const int k = (dw >> (8 * (cc & 3))) & 15;
+                  v[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cc, k));
                 }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int jj = 0; jj < kRowJG; ++jj)
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    acc[g + jj][2 * e] += (uint32_t)(__builtin_amdgcn_sbfe((int)v[jj][e], 0, 16) << sh);
+                    acc[g + jj][2 * e + 1] += (uint32_t)(((int)v[jj][e] >> 16) << sh);
+                    asm("" : "+v"(acc[g + jj][2 * e]), "+v"(acc[g + jj][2 * e + 1]));
+                  }
               }
             }
           }

@@ -44,7 +44,7 @@ def check_accumulate(orc, idx, lut, scale, offset):
 
 
 # (C, M, max_shift): sum_c 2^sh <= 257 takes the 16-bit fields, else int32 sums
-ROW_CASES = [(64, 512, 0), (64, 512, 2), (64, 512, 5), (32, 1000, 3), (4, 512, 0), (12, 768, 1),
+ROW_CASES = [(64, 512, 0), (64, 512, 2), (64, 512, 5), (32, 1008, 3), (4, 512, 0), (12, 768, 1),
              (128, 4096, 0), (256, 512, 0), (260, 512, 0), (512, 512, 0), (8, 2048, 7)]
 
 
