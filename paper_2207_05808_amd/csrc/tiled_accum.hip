@@ -375,10 +375,12 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 // no index tile goes through LDS, and every output store instruction writes
 // 1 KB of one row.
 //
-// A work item is RB rows x 512 columns; the table is staged 8 codebooks at a
-// time ([8 x 16 rows][512 entries], 128 KB of LDS, one 1024-thread workgroup
-// per CU), the next tile loaded into registers while the current one is
-// summed.
+// A work item is RB rows x 512 columns.  The table goes through two LDS
+// buffers of 4 codebooks each ([4 x 16 rows][512 entries], 64 KB; one
+// 1024-thread workgroup per CU): while a tile is summed from one buffer, every
+// wavefront first stages its share of the next tile into the other, from
+// registers loaded one tile ahead, so each tile costs one barrier and no
+// staging-only phase; the last tile's loads fetch the next work item's first.
 //  * When 255 * sum_c 2^(e_c - e_min) <= 65535, an entry is staged as the
 //    unsigned u = (q + 128) << (e_c - e_min): no 16-bit field can carry into
 //    the next while the codebooks are summed, so one 32-bit add sums two
@@ -387,9 +389,10 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
 //  * Otherwise entries are staged as signed q and summed in int32 with the
 //    shifts, 8 rows per wavefront.
 constexpr int kRowWaves = 16;           // wavefronts per workgroup
-constexpr int kRowCT = 8;               // codebooks per staged tile
+constexpr int kRowCT = 4;               // codebooks per staged tile
 constexpr int kRowMt = 512;             // columns per work item
 constexpr int kRowBytes = 2 * kRowMt;   // LDS bytes per staged table row
+constexpr int kRowTileBytes = kRowCT * 16 * kRowBytes;   // one of two tile buffers (64 KB)
 constexpr int kRowJG = 2;               // rows summed between scheduling barriers
 
 __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t* __restrict__ idx) {
@@ -442,162 +445,154 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
   // (columns 4l..4l+3 and 256+4l..256+4l+3) sits at position 16 a + 4 b +
   // (c + a) % 4 of each staged row: the 16 lanes of a read pass (fixed a)
   // cover one 256-byte span, and so do the 16 threads of a write pass below
-  // (fixed c).  Thread t stages, for staged rows t / 16 + 64 j (j < 2), the
-  // 16 columns 16 (t % 16).. of each half of the slice: two 16-byte loads,
-  // the four whole slots of lanes 4 (t % 16) + c.
+  // (fixed c).  Thread t stages staged row t / 16 of a tile (codebook c0 +
+  // t / 256, prototype (t / 16) % 16), the 16 columns 16 (t % 16).. of each
+  // half of the slice: two 16-byte loads, the four whole slots of lanes
+  // 4 (t % 16) + c.
   const int tp = tid & 15;
   const int tr = tid >> 4;
   const __amdgpu_buffer_rsrc_t trs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M), kBufDword3);
-  tu32x4 tv[4];   // [row j][half h]
+  tu32x4 tv[2];   // the two halves
   // (the lane bases are re-derived per tile through an empty asm, so the
-  // compiler does not keep one precomputed address per j in registers)
+  // compiler does not keep precomputed addresses in registers)
   auto load_tile = [&](int c0, int m0) {
-    int base = tr * M + m0 + 16 * tp;   // staged row tr of the tile, first half
+    int base = (c0 * 16 + tr) * M + m0 + 16 * tp;
     asm volatile("" : "+v"(base));
-    const bool full = c0 + kRowCT <= C;   // else 4 codebooks: staged rows 64.. are not read
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int h = 0; h < 2; ++h) {
+      const bool ok = m0 + 256 * h + 16 * tp < M;   // M % 16 == 0: units are whole
+      tv[h] = __builtin_amdgcn_raw_buffer_load_b128(trs, ok ? base + 256 * h : kOob, 0, 0);
+    }
+  };
+  auto store_tile = [&](int c0, int buf) {
+    int base = buf * kRowTileBytes + tr * kRowBytes + tp * 64;   // slot 4 tp + i at position 4 tp + (i + tp / 4) % 4
+    asm volatile("" : "+v"(base));
+    const unsigned short sh = (fields && shifted) ? (unsigned short)s_sh[c0 + (tr >> 4)] : 0;
+    const us2 s2 = {sh, sh};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t w[4];   // quad i of each half, 4 entries each
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        // staged row tr + 64 j: codebook c0 + tr / 16 + 4 j (M % 16 == 0: units are whole)
-        const bool ok = (j == 0 || full) && m0 + 256 * h + 16 * tp < M;
-        tv[2 * j + h] = __builtin_amdgcn_raw_buffer_load_b128(
-            trs, ok ? base + (c0 * 16 + 64 * j) * M + 256 * h : kOob, 0, 0);
-      }
-  };
-  auto store_tile = [&](int c0) {
-    int base = tr * kRowBytes + tp * 64;   // slot 4 tp + i at position 4 tp + (i + tp / 4) % 4
-    asm volatile("" : "+v"(base));
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const unsigned short sh = (fields && shifted) ? (unsigned short)s_sh[min(c0 + (tr >> 4) + 4 * j, C - 1)] : 0;
-      const us2 s2 = {sh, sh};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint32_t w[4];   // quad i of each half, 4 entries each
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const uint32_t x = tv[2 * j + h][i];
-          uint32_t lo, hi;
-          if (fields) {
-            const uint32_t u = x ^ 0x80808080u;   // q + 128 per byte
-            lo = __builtin_amdgcn_perm(0u, u, 0x0c010c00u);
-            hi = __builtin_amdgcn_perm(0u, u, 0x0c030c02u);
-            if (shifted) {
-              lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, lo) << s2);
-              hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, hi) << s2);
-            }
-          } else {
-            widen4(x, 0, lo, hi);
+        const uint32_t x = tv[h][i];
+        uint32_t lo, hi;
+        if (fields) {
+          const uint32_t u = x ^ 0x80808080u;   // q + 128 per byte
+          lo = __builtin_amdgcn_perm(0u, u, 0x0c010c00u);
+          hi = __builtin_amdgcn_perm(0u, u, 0x0c030c02u);
+          if (shifted) {
+            lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, lo) << s2);
+            hi = __builtin_bit_cast(uint32_t, __builtin_bit_cast(us2, hi) << s2);
           }
-          w[2 * h] = lo;
-          w[2 * h + 1] = hi;
+        } else {
+          widen4(x, 0, lo, hi);
         }
-        *reinterpret_cast<tlds_u32x4*>(s_tab + base + 64 * j * kRowBytes + 16 * ((i + (tp >> 2)) & 3)) =
-            (tu32x4){w[0], w[1], w[2], w[3]};
+        w[2 * h] = lo;
+        w[2 * h + 1] = hi;
       }
+      *reinterpret_cast<tlds_u32x4*>(s_tab + base + 16 * ((i + (tp >> 2)) & 3)) = (tu32x4){w[0], w[1], w[2], w[3]};
     }
   };
 
-  // the lane's slot of staged row cb * 16 + k: (k << 10) + base in one
-  // v_lshl_add_u32 with the uniform code in a scalar register; codebooks 4..7
-  // of a tile start 64 KB further, past the reach of the 16-bit read offset
-  const uint32_t lane_lo =
+  // the lane's slot of staged row cb * 16 + k of buffer b: (k << 10) + base
+  // in one v_lshl_add_u32 with the uniform code in a scalar register
+  const uint32_t lane_slot =
       (uint32_t)(uintptr_t)(s_tab + 16 * ((lane & ~3) + (((lane & 3) + (lane >> 4)) & 3)));
-  const uint32_t lane_hi = lane_lo + 4 * 16 * kRowBytes;
-  auto slot_of = [&](int cb, int k) -> const tlds_t* {
-    uint32_t a;
-    asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(a) : "s"(k), "v"(cb < 4 ? lane_lo : lane_hi));
-    return (const tlds_t*)(uintptr_t)a + (cb & 3) * 16 * kRowBytes;
-  };
   auto run = [&](auto nj_tag) {
     constexpr int NJ = decltype(nj_tag)::value;   // 16: 16-bit fields; 8: int32 sums
     constexpr bool F = NJ == 16;
     constexpr int NA = F ? 4 : 8;
     const int RB = kRowWaves * NJ;
     const int64_t nwork = (int64_t)ntm * ((N + RB - 1) / RB);
+    const int T = C / kRowCT;   // tiles per work item (C % 4 == 0)
+    if (blockIdx.x < nwork) load_tile(0, (int)(blockIdx.x % ntm) * kRowMt);
     for (int64_t w = blockIdx.x; w < nwork; w += gridDim.x) {
       const int mt = (int)(w % ntm);
       const int64_t r0 = (w / ntm) * RB + (int64_t)wave * NJ;   // this wavefront's first row
       const int m0 = mt * kRowMt;
+      const int64_t wn = w + gridDim.x;   // this workgroup's next work item
+      // after staging tile s: load tile s + 1, or the next work item's first
+      auto load_after = [&](int s) {
+        if (s + 1 < T) load_tile((s + 1) * kRowCT, m0);
+        else if (wn < nwork) load_tile(0, (int)(wn % ntm) * kRowMt);
+      };
       uint32_t acc[NJ][NA];
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int e = 0; e < NA; ++e) acc[j][e] = 0u;
 
-      load_tile(0, m0);
-      for (int c0 = 0; c0 < C; c0 += kRowCT) {
-        __syncthreads();   // every reader of the previous tile is done
-        store_tile(c0);
-        __syncthreads();
-        if (c0 + kRowCT < C) load_tile(c0 + kRowCT, m0);   // in flight during the sums below
-        const bool full = c0 + kRowCT <= C;                // else 4 codebooks (C % 4 == 0)
-        uint32_t d0[NJ], d1[NJ];   // index bytes of codebooks c0..c0+3 and c0+4..c0+7 (uniform)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          const uint8_t* p = idx + min(r0 + j, N - 1) * C + c0;   // rows past N: any valid row
-          d0[j] = *reinterpret_cast<const uint32_t*>(p);
-          d1[j] = full ? *reinterpret_cast<const uint32_t*>(p + 4) : 0u;
+      // buffer 0 is free: the previous work item ended with a barrier
+      store_tile(0, 0);
+      load_after(0);
+      __syncthreads();
+      for (int t = 0; t < T; ++t) {
+        // tile t is in buffer t % 2; stage tile t + 1 into the other one
+        // (its readers, tile t - 1, finished before the last barrier)
+        if (t + 1 < T) {
+          store_tile((t + 1) * kRowCT, (t + 1) & 1);
+          load_after(t + 1);   // in flight during the sums below
         }
-        // rows go kRowJG at a time between scheduling barriers, which bound
-        // the LDS reads (and row offsets) held in registers
+        const int c0 = t * kRowCT;
+        uint32_t d[NJ];   // index bytes of codebooks c0..c0+3 (uniform)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          d[j] = *reinterpret_cast<const uint32_t*>(idx + min(r0 + j, N - 1) * C + c0);   // rows past N: any valid row
+        const uint32_t lane_buf = lane_slot + (t & 1) * kRowTileBytes;
+        auto slot_of = [&](int cb, int k) -> const tlds_t* {
+          uint32_t adr;
+          asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(adr) : "s"(k), "v"(lane_buf));
+          return (const tlds_t*)(uintptr_t)adr + cb * 16 * kRowBytes;
+        };
         if (F) {
 #pragma unroll
           for (int cp = 0; cp < kRowCT; cp += 2) {
-            if (cp < 4 || full) {
 #pragma unroll
-              for (int g = 0; g < NJ; g += kRowJG) {
-                // the reads of kRowJG rows are issued together, then summed
-                tu32x4 v0[kRowJG], v1[kRowJG];
-                __builtin_amdgcn_sched_barrier(0);
+            for (int g = 0; g < NJ; g += kRowJG) {
+              // the reads of kRowJG rows are issued together, then summed
+              tu32x4 v0[kRowJG], v1[kRowJG];
+              __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int jj = 0; jj < kRowJG; ++jj) {
-                  const uint32_t dw = cp < 4 ? d0[g + jj] : d1[g + jj];
-                  const int k0 = (dw >> (8 * (cp & 3))) & 15, k1 = (dw >> (8 * ((cp + 1) & 3))) & 15;
-                  v0[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp, k0));
-                  v1[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp + 1, k1));
-                }
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int jj = 0; jj < kRowJG; ++jj)
-#pragma unroll
-                  for (int e = 0; e < 4; ++e) {
-                    acc[g + jj][e] += v0[jj][e] + v1[jj][e];
-                    asm("" : "+v"(acc[g + jj][e]));   // opaque: no reassociation across codebook pairs
-                  }
+              for (int jj = 0; jj < kRowJG; ++jj) {
+                const uint32_t dw = d[g + jj];
+                v0[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp, (dw >> (8 * cp)) & 15));
+                v1[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp + 1, (dw >> (8 * cp + 8)) & 15));
               }
+              __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+              for (int jj = 0; jj < kRowJG; ++jj)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  acc[g + jj][e] += v0[jj][e] + v1[jj][e];
+                  asm("" : "+v"(acc[g + jj][e]));   // opaque: no reassociation across codebook pairs
+                }
             }
           }
         } else {
 #pragma unroll
           for (int cc = 0; cc < kRowCT; ++cc) {
-            if (cc < 4 || full) {
-              const int sh = tuni(s_sh[c0 + cc]);
+            const int sh = tuni(s_sh[c0 + cc]);
 #pragma unroll
-              for (int g = 0; g < NJ; g += kRowJG) {
-                tu32x4 v[kRowJG];
-                __builtin_amdgcn_sched_barrier(0);
+            for (int g = 0; g < NJ; g += kRowJG) {
+              tu32x4 v[kRowJG];
+              __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int jj = 0; jj < kRowJG; ++jj) {
-                  const uint32_t dw = cc < 4 ? d0[g + jj] : d1[g + jj];
-                  const int k = (dw >> (8 * (cc & 3))) & 15;
-                  v[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cc, k));
+              for (int jj = 0; jj < kRowJG; ++jj)
+                v[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cc, (d[g + jj] >> (8 * cc)) & 15));
+              __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+              for (int jj = 0; jj < kRowJG; ++jj)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  acc[g + jj][2 * e] += (uint32_t)(__builtin_amdgcn_sbfe((int)v[jj][e], 0, 16) << sh);
+                  acc[g + jj][2 * e + 1] += (uint32_t)(((int)v[jj][e] >> 16) << sh);
+                  asm("" : "+v"(acc[g + jj][2 * e]), "+v"(acc[g + jj][2 * e + 1]));
                 }
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int jj = 0; jj < kRowJG; ++jj)
-#pragma unroll
-                  for (int e = 0; e < 4; ++e) {
-                    acc[g + jj][2 * e] += (uint32_t)(__builtin_amdgcn_sbfe((int)v[jj][e], 0, 16) << sh);
-                    acc[g + jj][2 * e + 1] += (uint32_t)(((int)v[jj][e] >> 16) << sh);
-                    asm("" : "+v"(acc[g + jj][2 * e]), "+v"(acc[g + jj][2 * e + 1]));
-                  }
-              }
             }
           }
         }
+        __syncthreads();   // tile t + 1 visible; every reader of buffer t % 2 done
       }
 
       // ---------------- epilogue: outputs i < 4 are columns colA + i, the rest colB + i - 4
