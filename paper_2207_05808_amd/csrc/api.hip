@@ -302,21 +302,24 @@ bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
   return true;
 }
 
-// Row-uniform accumulate (tiled_accum.hip) for int8 tables at least 512
-// columns wide: scalar loads of 4-byte index words (C % 4 == 0), table rows in
-// whole 16-byte units (M % 16 == 0), 16-byte output stores, and enough
+// Row-uniform accumulate (tiled_accum.hip) for tables at least one column
+// tile wide (512 int8 or 256 fp32 columns): scalar loads of 4-byte index words
+// (C % 4 == 0), table rows in whole 16-byte units (int8: M % 16 == 0, fp32:
+// M % 4 == 0 and a 16-byte aligned table), 16-byte output stores, and enough
 // 256-row work items to occupy a quarter of the CUs.
 bool plan_trow(const Shape& s, TArgs* t) {
-  if (s.elem != kI8 || s.M < kRowTileCols || s.M % 16 != 0 || s.C % 4 != 0) return false;
-  if (!aligned(s.idx_in, 4) || !aligned(s.lut, 4)) return false;
+  const bool f32 = s.elem == kF32;
+  const int cols = f32 ? kRowTileColsF32 : kRowTileCols;
+  if (s.M < cols || s.M % (f32 ? 4 : 16) != 0 || s.C % 4 != 0) return false;
+  if (!aligned(s.idx_in, 4) || !aligned(s.lut, f32 ? 16 : 4)) return false;
   if ((s.y && !aligned(s.y, 16)) || (s.acc && !aligned(s.acc, 16))) return false;
-  if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;   // 32-bit buffer offsets
+  if ((int64_t)s.C * kK * s.M * (f32 ? 4 : 1) >= (1ll << 31)) return false;   // 32-bit buffer offsets
   TArgs a{};
   a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;
   a.N = s.N; a.C = s.C; a.M = s.M;
-  a.Mt = kRowTileCols;
+  a.Mt = cols;
   a.RB = 256;
-  a.ntm = (s.M + kRowTileCols - 1) / kRowTileCols;
+  a.ntm = (s.M + cols - 1) / cols;
   a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
   if (a.nwork * 4 < device_cus()) return false;
   a.col_bias = s.col_bias;
@@ -389,7 +392,7 @@ int accumulate(const Shape& s, hipStream_t stream) {
   TArgs t;
   int nj, nw;
   if (plan_trow(s, &t)) {
-    const int rc = status_from(launch_trow(t, device_cus(), stream));
+    const int rc = status_from(launch_trow(s.elem, t, device_cus(), stream));
     if (rc != MADDNESS_OK || t.act == s.act) return rc;
     return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
   }

@@ -123,11 +123,12 @@ hipError_t launch_softmax_rows(float* y, int64_t N, int M, int cus, hipStream_t 
 
 hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStream_t stream);
 
-// Row-uniform accumulate for int8 tables (tiled_accum.hip): one 1024-thread
-// workgroup per CU, work items of 256 rows x 512 columns; idx must not overlap
-// the outputs.
+// Row-uniform accumulate (tiled_accum.hip): one 1024-thread workgroup per CU,
+// work items of 256 rows x 512 columns (int8 tables) or 256 columns (fp32);
+// idx must not overlap the outputs.
 constexpr int kRowTileCols = 512;
-hipError_t launch_trow(const TArgs& t, int cus, hipStream_t stream);
+constexpr int kRowTileColsF32 = 256;
+hipError_t launch_trow(int elem, const TArgs& t, int cus, hipStream_t stream);
 
 // Rounded 8-bit summation over codebooks: the whole [C][16][Mt] column slice
 // (one byte per entry) staged once per workgroup, Mt = 16 * lanes per row.

@@ -666,6 +666,142 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
   else run(std::integral_constant<int, 8>{});
 }
 
+// fp32 tables: the same row-uniform scheme with four fp32 columns per lane.
+// A work item is 256 rows x 256 columns; lane l owns columns 4l..4l+3 in their
+// own order, so lane slot l of a staged row is the row's 16-byte unit l: each
+// staged row arrives by one direct-to-LDS buffer load per wavefront (64 lanes x
+// 16 bytes into consecutive LDS), with no registers or LDS writes on the way,
+// and each output store instruction writes 1 KB of one row.  Each lane adds
+// the selected entries to its sums codebook by codebook, strictly ascending
+// from +0.0f, so the sums are the ordered fp32 sums of tacc_kernel.  Tiles of
+// 4 codebooks alternate between the two 64 KB buffers over the workgroup's
+// whole sequence of tiles: the loads of the next tile (the next work item's
+// first after a work item's last) are in flight while a tile is summed, and
+// each tile costs one wait and one barrier.
+constexpr int kRowMtF = 256;   // columns per work item (fp32 tables)
+
+__global__ void __launch_bounds__(1024) trow_f32_kernel(const TArgs a, const uint8_t* __restrict__ idx) {
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  tlds_t* s_tab = (tlds_t*)smem_raw;   // two tile buffers of kRowTileBytes
+  constexpr int NJ = 16;               // rows per wavefront
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tuni(tid >> 6);
+  const int C = a.C, M = a.M, ntm = a.ntm;
+  const int64_t N = a.N;
+
+  const __amdgpu_buffer_rsrc_t trs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.lut), 0, (int)((int64_t)C * 16 * M * 4), kBufDword3);
+  // stage tile c0 of column tile m0 into buffer buf: wavefront w loads staged
+  // rows 4w..4w+3 (codebook c0 + w / 4, prototypes 4 (w % 4)..); columns past
+  // M read as zeros
+  auto stage = [&](int c0, int m0, int buf) {
+    const bool ok = m0 + 4 * lane < M;   // M % 4 == 0: units are whole
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * wave + i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          trs, (__attribute__((address_space(3))) void*)(s_tab + buf * kRowTileBytes + r * kRowBytes), 16,
+          ok ? ((c0 * 16 + r) * M + m0 + 4 * lane) * 4 : kOob, 0, 0, 0);
+    }
+  };
+  auto publish = [&]() {   // this wavefront's staged rows are in LDS, then the barrier
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  };
+
+  const uint32_t lane_slot = (uint32_t)(uintptr_t)(s_tab + lane * 16);
+  const int RB = kRowWaves * NJ;
+  const int64_t nwork = (int64_t)ntm * ((N + RB - 1) / RB);
+  const int T = C / 4;   // tiles per work item (C % 4 == 0)
+  int gb = 0;            // buffer of the current tile (alternates over the whole sequence)
+  if (blockIdx.x < nwork) {
+    stage(0, (int)(blockIdx.x % ntm) * kRowMtF, 0);
+    publish();
+  }
+  for (int64_t w = blockIdx.x; w < nwork; w += gridDim.x) {
+    const int mt = (int)(w % ntm);
+    const int64_t r0 = (w / ntm) * RB + (int64_t)wave * NJ;   // this wavefront's first row
+    const int m0 = mt * kRowMtF;
+    const int64_t wn = w + gridDim.x;
+    float acc[NJ][4];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[j][e] = 0.0f;
+
+    for (int t = 0; t < T; ++t) {
+      // the other buffer's readers (the previous tile) finished before the last barrier
+      if (t + 1 < T) stage((t + 1) * 4, m0, gb ^ 1);
+      else if (wn < nwork) stage(0, (int)(wn % ntm) * kRowMtF, gb ^ 1);
+      const int c0 = t * 4;
+      uint32_t d[NJ];   // index bytes of codebooks c0..c0+3 (uniform)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        d[j] = *reinterpret_cast<const uint32_t*>(idx + min(r0 + j, N - 1) * C + c0);   // rows past N: any valid row
+      const uint32_t lane_buf = lane_slot + gb * kRowTileBytes;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+#pragma unroll
+        for (int g = 0; g < NJ; g += kRowJG) {
+          tu32x4 v[kRowJG];
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int jj = 0; jj < kRowJG; ++jj) {
+            uint32_t adr;
+            asm("v_lshl_add_u32 %0, %1, 10, %2" : "=v"(adr) : "s"((d[g + jj] >> (8 * cb)) & 15), "v"(lane_buf));
+            v[jj] = *reinterpret_cast<const tlds_u32x4*>((const tlds_t*)(uintptr_t)adr + cb * 16 * kRowBytes);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int jj = 0; jj < kRowJG; ++jj)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[g + jj][e] += __uint_as_float(v[jj][e]);   // codebooks ascending
+        }
+      }
+      publish();   // the next tile visible; every reader of this buffer done
+      gb ^= 1;
+    }
+
+    // ---------------- epilogue: this lane's columns col..col+3
+    const int col = m0 + 4 * lane;
+    float cb[4];   // column biases, loaded once per work item (stores to y may alias them)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cb[e] = (a.act != 0 && a.col_bias && col + e < M) ? a.col_bias[col + e] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int64_t row = r0 + j;
+      float yv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) yv[e] = acc[j][e];
+      if (a.act != 0) {
+        float vmax = -__builtin_inff();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float z = yv[e] + cb[e];
+          if (a.act == 2) z = (z > 0.0f) ? z : 0.0f;
+          yv[e] = z;
+          if (col + e < M) vmax = __builtin_fmaxf(vmax, z);
+        }
+        if (a.act == 3) {   // one column tile: the whole row is in this wavefront
+          for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+          float sum = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            yv[e] = (col + e < M) ? expf(yv[e] - vmax) : 0.0f;
+            sum += yv[e];
+          }
+          for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) yv[e] = yv[e] / sum;
+        }
+      }
+      if (row >= N || col >= M) continue;   // row: uniform; col: whole quads (M % 4 == 0)
+      __builtin_nontemporal_store((tf32x4){yv[0], yv[1], yv[2], yv[3]}, reinterpret_cast<tf32x4*>(a.y + row * M + col));
+    }
+  }
+}
+
 // Rounded 8-bit summation over codebooks (§1 names it; reading R20): the
 // codes of a row, biased to bytes u = q + 128 and padded with 128 to P = 2^L
 // codebooks, are reduced by a balanced tree of rounded byte averages in
@@ -1096,8 +1232,9 @@ hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_trow(const TArgs& t, int cus, hipStream_t stream) {
-  const void* fn = reinterpret_cast<const void*>(&trow_kernel);
+hipError_t launch_trow(int elem, const TArgs& t, int cus, hipStream_t stream) {
+  const void* fn = elem == kF32 ? reinterpret_cast<const void*>(&trow_f32_kernel)
+                                : reinterpret_cast<const void*>(&trow_kernel);
   hipError_t err = hipSuccess;
   const int per_cu = t_prepare(fn, kRowWaves * 64, t.lds_total, &err);
   if (err != hipSuccess) return err;
@@ -1105,7 +1242,10 @@ hipError_t launch_trow(const TArgs& t, int cus, hipStream_t stream) {
   const int64_t resident = (int64_t)per_cu * cus;
   if (blocks > resident) blocks = resident;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(trow_kernel, dim3((unsigned)blocks), dim3(kRowWaves * 64), t.lds_total, stream, t, t.idx);
+  if (elem == kF32)
+    hipLaunchKernelGGL(trow_f32_kernel, dim3((unsigned)blocks), dim3(kRowWaves * 64), t.lds_total, stream, t, t.idx);
+  else
+    hipLaunchKernelGGL(trow_kernel, dim3((unsigned)blocks), dim3(kRowWaves * 64), t.lds_total, stream, t, t.idx);
   return hipGetLastError();
 }
 

@@ -97,24 +97,79 @@ def test_row_matmul_workloads(orc, name, N):
     assert np.array_equal(host(y), ry)
 
 
-@pytest.mark.parametrize("M", [512, 1024])
+@pytest.mark.parametrize("M,max_shift", [(512, 2), (1024, 2), (512, 6)])
 @pytest.mark.parametrize("act", ["bias", "relu", "softmax"])
-def test_row_layer_output(orc, M, act):
+def test_row_layer_output(orc, M, max_shift, act):
     """matmul_act with a table larger than LDS: encode, then sigma in the
     row-uniform kernel's epilogue (one column tile: M = 512), or bias there
-    and the row softmax as a second pass (M = 1024)."""
+    and the row softmax as a second pass (M = 1024); max_shift 6 takes the
+    int32 sums."""
     C, D = 64, 96
     N = rows_for(M)
     rng = np.random.default_rng(M + len(act))
     A = rng.standard_normal((N, D), dtype=np.float32)
     split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
     thr = rng.standard_normal((C, 15), dtype=np.float32)
-    lut, scale, offset = W.random_codes(C, M, seed=M + 1, max_shift=2)
+    lut, scale, offset = W.random_codes(C, M, seed=M + 1, max_shift=max_shift)
     bias = rng.standard_normal(M).astype(np.float32)
     code = {"bias": 1, "relu": 2, "softmax": 3}[act]
     y = host(mdn.matmul_act(dev(A), dev(split), dev(thr), dev(lut), dev(scale), dev(offset),
                             col_bias=dev(bias), act=act))
     _, _, yref = orc.matmul(A, split, thr, lut, scale, offset)
+    ref = orc.sigma(yref, bias, code)
+    if act != "softmax":
+        assert np.array_equal(y.astype(np.float64), ref)
+        return
+    z = orc.sigma(yref, bias, 1)
+    tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + M + 5) * 2.0 ** -24 * ref + 2.0 ** -120
+    assert np.all(np.abs(y.astype(np.float64) - ref) <= tol)
+
+
+# ------------------------------------------------------------- fp32 tables
+def rows_for_f32(M):
+    """Rows that reach the fp32 row-uniform kernel: 64 work items of 256 rows
+    x 256 columns, plus a ragged tail."""
+    tiles = -(-M // 256)
+    return -(-64 // tiles) * 256 + 77
+
+
+@pytest.mark.parametrize("C,M", [(256, 1024), (4, 256), (8, 260), (64, 1000), (12, 512), (100, 4096)])
+def test_row_accumulate_f32(orc, C, M):
+    """Ordered fp32 sums, codebooks ascending from +0.0f: bit-identical."""
+    N = rows_for_f32(M)
+    idx = W.random_indices(N, C, seed=C * 13 + M)
+    tab = W.random_fp32_table(C, M, seed=C + 5 * M)
+    y = host(mdn.lut_accumulate_f32(dev(idx), dev(tab), validate=True))
+    assert np.array_equal(y, orc.lut_accumulate_f32(idx, tab))
+
+
+def test_row_matmul_f32_workload(orc):
+    p = W.make("encode_heavy_f32", N=rows_for_f32(1024))
+    tab = mdn.build_lut_f32(dev(p.P), dev(p.B))
+    rtab = orc.build_lut_f32(p.P, p.B)
+    assert np.array_equal(host(tab), rtab)
+    y, idx = mdn.matmul_f32(dev(p.A), dev(p.split), dev(p.thr), tab, want_idx=True)
+    ridx, ry = orc.matmul_f32(p.A, p.split, p.thr, rtab)
+    assert np.array_equal(host(idx), ridx)
+    assert np.array_equal(host(y), ry)
+
+
+@pytest.mark.parametrize("M", [256, 512])
+@pytest.mark.parametrize("act", ["bias", "relu", "softmax"])
+def test_row_layer_output_f32(orc, M, act):
+    """sigma in the fp32 kernel's epilogue (one column tile: M = 256), or bias
+    there and the row softmax as a second pass (M = 512)."""
+    C, D = 32, 80
+    N = rows_for_f32(M)
+    rng = np.random.default_rng(3 * M + len(act))
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
+    thr = rng.standard_normal((C, 15), dtype=np.float32)
+    tab = W.random_fp32_table(C, M, seed=M + 7)
+    bias = rng.standard_normal(M).astype(np.float32)
+    code = {"bias": 1, "relu": 2, "softmax": 3}[act]
+    y = host(mdn.matmul_act_f32(dev(A), dev(split), dev(thr), dev(tab), col_bias=dev(bias), act=act))
+    _, yref = orc.matmul_f32(A, split, thr, tab)
     ref = orc.sigma(yref, bias, code)
     if act != "softmax":
         assert np.array_equal(y.astype(np.float64), ref)
