@@ -49,6 +49,28 @@ __device__ __forceinline__ uint32_t tpk_add16(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, (s2)(__builtin_bit_cast(s2, a) + __builtin_bit_cast(s2, b)));
 }
 
+// max / sum over the 64 lanes of a wavefront, the same value in every lane:
+// DPP within each row of 16 lanes (pairs, quads, mirrored halves, mirrored
+// rows), then the four row results through readlane.  No LDS round trips.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+template <bool MAX>
+__device__ __forceinline__ float wave_reduce64(float x) {
+  auto op = [](float a, float b) { return MAX ? __builtin_fmaxf(a, b) : a + b; };
+  x = op(x, dpp_f32<0xB1>(x));    // quad_perm [1,0,3,2]
+  x = op(x, dpp_f32<0x4E>(x));    // quad_perm [2,3,0,1]
+  x = op(x, dpp_f32<0x141>(x));   // row_half_mirror
+  x = op(x, dpp_f32<0x140>(x));   // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return op(op(r0, r1), op(r2, r3));
+}
+
 // four int8 codes -> two dwords of int16 q << sh (0 <= sh <= 8), column order
 // kept: v_perm puts each code in the high byte of its 16-bit half, then a
 // packed arithmetic shift right by 8 - sh sign-extends and scales it
@@ -634,16 +656,16 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
             if (ok) vmax = __builtin_fmaxf(vmax, z);
           }
           if (a.act == 3) {
-            for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+            vmax = wave_reduce64<true>(vmax);
             float sum = 0.0f;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
               yv[i] = ((i < 4 ? colA : colB - 4) + i < M) ? expf(yv[i] - vmax) : 0.0f;
               sum += yv[i];
             }
-            for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+            const float rs = 1.0f / wave_reduce64<false>(sum);   // correctly rounded reciprocal, then products
 #pragma unroll
-            for (int i = 0; i < 8; ++i) yv[i] = yv[i] / sum;
+            for (int i = 0; i < 8; ++i) yv[i] = yv[i] * rs;
           }
         }
         if (row >= N) continue;   // uniform: one row per wavefront
@@ -784,16 +806,16 @@ __global__ void __launch_bounds__(1024) trow_f32_kernel(const TArgs a, const uin
           if (col + e < M) vmax = __builtin_fmaxf(vmax, z);
         }
         if (a.act == 3) {   // one column tile: the whole row is in this wavefront
-          for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+          vmax = wave_reduce64<true>(vmax);
           float sum = 0.0f;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             yv[e] = (col + e < M) ? expf(yv[e] - vmax) : 0.0f;
             sum += yv[e];
           }
-          for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+          const float rs = 1.0f / wave_reduce64<false>(sum);   // correctly rounded reciprocal, then products
 #pragma unroll
-          for (int e = 0; e < 4; ++e) yv[e] = yv[e] / sum;
+          for (int e = 0; e < 4; ++e) yv[e] = yv[e] * rs;
         }
       }
       if (row >= N || col >= M) continue;   // row: uniform; col: whole quads (M % 4 == 0)
@@ -1141,7 +1163,7 @@ __global__ void __launch_bounds__(256) softmax_rows_kernel(float* y, int64_t N, 
       v[i] = q < nq ? __builtin_nontemporal_load(yr + q) : (tf32x4){-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
       vmax = __builtin_fmaxf(vmax, __builtin_fmaxf(__builtin_fmaxf(v[i].x, v[i].y), __builtin_fmaxf(v[i].z, v[i].w)));
     }
-    for (int o = 1; o < 64; o <<= 1) vmax = __builtin_fmaxf(vmax, __shfl_xor(vmax, o));
+    vmax = wave_reduce64<true>(vmax);
     float sum = 0.0f;
 #pragma unroll
     for (int i = 0; i < kSoftChunks; ++i) {
@@ -1151,11 +1173,11 @@ __global__ void __launch_bounds__(256) softmax_rows_kernel(float* y, int64_t N, 
         sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
       }
     }
-    for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o);
+    const float rs = 1.0f / wave_reduce64<false>(sum);   // correctly rounded reciprocal, then products
 #pragma unroll
     for (int i = 0; i < kSoftChunks; ++i) {
       const int q = lane + 64 * i;
-      if (q < nq) __builtin_nontemporal_store((tf32x4){v[i].x / sum, v[i].y / sum, v[i].z / sum, v[i].w / sum}, yr + q);
+      if (q < nq) __builtin_nontemporal_store((tf32x4){v[i].x * rs, v[i].y * rs, v[i].z * rs, v[i].w * rs}, yr + q);
     }
   }
 }
