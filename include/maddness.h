@@ -33,7 +33,11 @@
  *    indices in [0, 16), scales exact normal fp32 powers of two with
  *    127 * sum_c 2^(e_c - e_min) < 2^31.  Violations give unspecified values,
  *    never out-of-bounds accesses.
- *  - Thread safety: no mutable global state; concurrent calls on different
+ *  - Output arrays must not overlap each other or any input array of the same
+ *    call (kernels may read inputs, indices in particular, through the scalar
+ *    cache while outputs are being written).  Inputs may overlap each other.
+ *  - Thread safety: the only global state is a per-kernel cache of launch
+ *    attributes, filled once under a mutex; concurrent calls on different
  *    streams are independent.
  */
 #ifndef MADDNESS_H

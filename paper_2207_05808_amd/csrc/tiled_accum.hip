@@ -1,6 +1,13 @@
-// Column-tiled lookup-accumulate (§1 of McCarter & Dronen: the product is the
-// sum over codebooks of the table rows the encoder selected) for tables larger
-// than LDS and for the accumulate-only entry points.
+// Lookup-accumulate kernels for tables larger than LDS and for the
+// accumulate-only entry points (§1 of McCarter & Dronen: the product is the
+// sum over codebooks of the table rows the encoder selected):
+//  * trow_kernel / trow_f32_kernel, the row-uniform kernels, for tables at
+//    least 512 int8 or 256 fp32 columns wide (below);
+//  * tacc_kernel, the column-tiled kernel, for every other shape (first);
+//  * tavg_kernel, the rounded 8-bit summation (last);
+//  * softmax_rows_kernel, the row softmax for rows spanning several tiles.
+//
+// Column-tiled kernel.
 //
 // A work item is RB rows x Mt output columns.  The lanes of a wavefront form
 // groups of LPR lanes, one group per output row; lane g of a group covers Mt /
