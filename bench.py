@@ -30,6 +30,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, published
+LDS_PEAK_TBS = 157.3   # 256 B/clk per CU x 256 CUs x 2.4 GHz (a ds_read_b128 probe reaches about 88% of it)
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 
 
@@ -257,6 +258,16 @@ def main():
         enc_us = region_us(lambda i: split_calls[i % 2]())
         acc_us = region_us(lambda i: acc_call())
         result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
+        if not headline:
+            # the accumulate of the two-phase workloads is bound by LDS reads:
+            # N C M lookups of 2 bytes (int8 tables, staged as 16-bit
+            # entries) or 4 bytes (fp32), against 256 B/clk/CU x 256 CUs x
+            # 2.4 GHz
+            lds_bytes = N * spec.C * spec.M * (2 if spec.quantized else 4)
+            lds_tbps = lds_bytes / (acc_us * 1e-6) / 1e12
+            result["context"]["accumulate_lds_roofline"] = {
+                "bound": "lds", "achieved": round(lds_tbps, 2), "peak": LDS_PEAK_TBS, "unit": "TB/s",
+                "frac": round(lds_tbps / LDS_PEAK_TBS, 4), "lds_read_bytes": lds_bytes}
         if spec.quantized:
             # the rounded 8-bit averaging accumulate (approximate) over a
             # shared-exponent table of the same weights, on the same indices
