@@ -177,3 +177,42 @@ def test_row_layer_output_f32(orc, M, act):
     z = orc.sigma(yref, bias, 1)
     tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + M + 5) * 2.0 ** -24 * ref + 2.0 ** -120
     assert np.all(np.abs(y.astype(np.float64) - ref) <= tol)
+
+
+# ------------------------------------------- rounded 8-bit summation (R20)
+# The averaging accumulate at the row counts of the cases above (its kernel
+# keeps one column slice of the table per workgroup and streams row batches):
+# many batches per workgroup, ragged last batch.
+def rows_for_avg(M):
+    tiles = -(-M // 512)
+    return -(-64 // tiles) * 128 + 77
+
+
+# (C, M): P < 8; one subtree of 8; padding codebooks in the last subtree
+# (C 12); whole padding subtrees (C 36: P 64); C > 64; column tails
+AVG_ROW_CASES = [(4, 512), (8, 512), (12, 768), (36, 1024), (64, 512), (100, 512), (128, 4096), (60, 1008)]
+
+
+@pytest.mark.parametrize("C,M", AVG_ROW_CASES)
+def test_row_accumulate_avg(orc, C, M):
+    N = rows_for_avg(M)
+    idx = W.random_indices(N, C, seed=C * 17 + M)
+    lut, scale, offset = W.random_codes(C, M, seed=C + 3 * M, max_shift=0)
+    acc, y = mdn.lut_accumulate_avg(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=True)
+    racc, ry = orc.lut_accumulate_avg(idx, lut, scale, offset)
+    assert np.array_equal(host(acc), racc)
+    assert np.array_equal(host(y), ry)
+
+
+def test_row_accumulate_avg_extreme_and_single_outputs(orc):
+    """Codes at +-127 and -128, then acc only and y only."""
+    C, M = 64, 512
+    N = rows_for_avg(M)
+    idx = W.random_indices(N, C, seed=5)
+    lut, scale, offset = W.random_codes(C, M, seed=6, max_shift=0, extreme=True)
+    lut[::3, 5, ::11] = -128
+    racc, ry = orc.lut_accumulate_avg(idx, lut, scale, offset)
+    acc, y = mdn.lut_accumulate_avg(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=True, want_y=False)
+    assert y is None and np.array_equal(host(acc), racc)
+    acc, y = mdn.lut_accumulate_avg(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=False, want_y=True)
+    assert acc is None and np.array_equal(host(y), ry)
