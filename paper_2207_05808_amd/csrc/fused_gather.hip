@@ -28,7 +28,6 @@
 // Codebooks are padded to a multiple of 4 with offsets of an all-zero row.
 #include "internal.hpp"
 
-#include <mutex>
 
 namespace mdn {
 
@@ -539,31 +538,11 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   }
 }
 
-// Per (kernel, block, LDS size): the LDS attribute is raised once and the
-// number of resident workgroups per CU is queried once.
-static int g_prepare(const void* fn, int block, int lds, hipError_t* err) {
-  struct Entry { const void* fn; int block, lds, n; };
-  static Entry cache[64];
-  static int used = 0;
-  static std::mutex mu;
-  std::lock_guard<std::mutex> lock(mu);
-  for (int i = 0; i < used; ++i)
-    if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
-  if (lds > 64 * 1024) {
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) { *err = e; return 0; }
-  }
-  int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
-  if (used < 64) cache[used++] = Entry{fn, block, lds, n};
-  return n;
-}
-
 template <int ELEM, int NG, int UQ>
 static hipError_t glaunch(const GArgs& g, int nw, int cus, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&gfused_kernel<ELEM, NG, UQ>);
   hipError_t err = hipSuccess;
-  const int per_cu = g_prepare(fn, nw * 64, g.lds_total, &err);
+  const int per_cu = launch_prepare(fn, nw * 64, g.lds_total, &err);
   if (err != hipSuccess) return err;
   const int64_t steps = (g.N + g.R - 1) / g.R;
   int64_t blocks = (steps + nw - 1) / nw;

@@ -134,8 +134,13 @@ hipError_t launch_trow(int elem, const TArgs& t, int cus, hipStream_t stream);
 // (one byte per entry) staged once per workgroup, Mt = 16 * lanes per row.
 hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream);
 
-// Compute units of the current device (queried once per process).
+// Compute units of the current device (queried once per device).
 int device_cus();
+
+// Per (device, kernel, block size, dynamic LDS bytes): raises the kernel's
+// dynamic-LDS limit when it needs more than 64 KB and returns how many such
+// workgroups one CU holds (at least 1); *err receives a failed attribute call.
+int launch_prepare(const void* fn, int block, int lds, hipError_t* err);
 
 // Launch one kernel of the family; returns hipSuccess or the launch error.
 hipError_t launch_path(int mode, int elem, int pf, int uq, const KArgs& a,

@@ -569,39 +569,42 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   X(MODE, ELEM, 0, UQ) X(MODE, ELEM, 1, UQ) X(MODE, ELEM, 2, UQ) X(MODE, ELEM, 4, UQ) \
   X(MODE, ELEM, 8, UQ) X(MODE, ELEM, 9, UQ) X(MODE, ELEM, 16, UQ)
 
-// Per (kernel, block, LDS size): the LDS attribute is raised once and the
-// number of resident workgroups per CU is queried once.
-static int prepare_kernel(const void* fn, int block, int lds, hipError_t* err) {
-  struct Entry { const void* fn; int block, lds, n; };
-  static Entry cache[128];
+// Per (device, kernel, block, LDS size): the LDS attribute is raised once and
+// the number of resident workgroups per CU is queried once (a full cache only
+// means querying again).
+int launch_prepare(const void* fn, int block, int lds, hipError_t* err) {
+  struct Entry { int dev; const void* fn; int block, lds, n; };
+  static Entry cache[256];
   static int used = 0;
   static std::mutex mu;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = -1;
   std::lock_guard<std::mutex> lock(mu);
   for (int i = 0; i < used; ++i)
-    if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
+    if (cache[i].dev == dev && cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
   if (lds > 64 * 1024) {
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) { *err = e; return 0; }
   }
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
-  if (used < 128) cache[used++] = Entry{fn, block, lds, n};
+  if (used < 256) cache[used++] = Entry{dev, fn, block, lds, n};
   return n;
 }
 
+// Compute units of the current device, queried once per device.
 int device_cus() {
-  static std::atomic<int> cus{0};
-  int v = cus.load();
-  if (v == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-      v = n;
-    else
-      v = 256;
-    cus.store(v);
+  constexpr int kDevs = 64;
+  static std::atomic<int> cus[kDevs] = {};
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  if (dev >= 0 && dev < kDevs) {
+    const int v = cus[dev].load();
+    if (v != 0) return v;
   }
-  return v;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+  if (dev >= 0 && dev < kDevs) cus[dev].store(n);
+  return n;
 }
 
 // The persistent grid never exceeds what is resident at once, so no wave of
@@ -610,7 +613,7 @@ template <int MODE, int ELEM, int PF, int UQ>
 static hipError_t launch_one(const KArgs& a, dim3 grid, dim3 block, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&path_kernel<MODE, ELEM, PF, UQ>);
   hipError_t err = hipSuccess;
-  const int per_cu = prepare_kernel(fn, (int)block.x, a.L.total, &err);
+  const int per_cu = launch_prepare(fn, (int)block.x, a.L.total, &err);
   if (err != hipSuccess) return err;
   const int64_t resident = (int64_t)per_cu * device_cus();
   int64_t gx = (int64_t)grid.x;

@@ -29,7 +29,6 @@
 #include "internal.hpp"
 
 #include <climits>
-#include <mutex>
 #include <type_traits>
 
 namespace mdn {
@@ -428,8 +427,6 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   tlds_t* smem = (tlds_t*)smem_raw;
   typedef unsigned short us2 __attribute__((ext_vector_type(2)));
-  typedef uint32_t tu32x2 __attribute__((ext_vector_type(2)));
-  typedef __attribute__((address_space(3))) tu32x2 tlds_u32x2;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -1116,31 +1113,12 @@ tavg_kernel(const TArgs a) {
   }
 }
 
-// Per (kernel, block, LDS size): the LDS attribute is raised once and the
-// number of resident workgroups per CU is queried once.
-static int t_prepare(const void* fn, int block, int lds, hipError_t* err) {
-  struct Entry { const void* fn; int block, lds, n; };
-  static Entry cache[32];
-  static int used = 0;
-  static std::mutex mu;
-  std::lock_guard<std::mutex> lock(mu);
-  for (int i = 0; i < used; ++i)
-    if (cache[i].fn == fn && cache[i].block == block && cache[i].lds == lds) return cache[i].n;
-  if (lds > 64 * 1024) {
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) { *err = e; return 0; }
-  }
-  int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n < 1) n = 1;
-  if (used < 32) cache[used++] = Entry{fn, block, lds, n};
-  return n;
-}
 
 template <int ELEM, int NJ>
 static hipError_t tlaunch(const TArgs& t, int nw, int cus, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&tacc_kernel<ELEM, NJ>);
   hipError_t err = hipSuccess;
-  const int per_cu = t_prepare(fn, nw * 64, t.lds_total, &err);
+  const int per_cu = launch_prepare(fn, nw * 64, t.lds_total, &err);
   if (err != hipSuccess) return err;
   int64_t blocks = t.nwork;
   const int64_t resident = (int64_t)per_cu * cus;
@@ -1221,7 +1199,7 @@ template <int GI, int GO, bool WIDX, int NT>
 static hipError_t alaunch(const TArgs& t, int cus, hipStream_t stream) {
   const void* fn = reinterpret_cast<const void*>(&tavg_kernel<GI, GO, WIDX, NT>);
   hipError_t err = hipSuccess;
-  const int per_cu = t_prepare(fn, NT, t.lds_total, &err);
+  const int per_cu = launch_prepare(fn, NT, t.lds_total, &err);
   if (err != hipSuccess) return err;
   // every workgroup keeps one column tile: a whole number of workgroups per tile
   int64_t per_tile = ((int64_t)per_cu * cus) / t.ntm;
@@ -1265,7 +1243,7 @@ hipError_t launch_trow(int elem, const TArgs& t, int cus, hipStream_t stream) {
   const void* fn = elem == kF32 ? reinterpret_cast<const void*>(&trow_f32_kernel)
                                 : reinterpret_cast<const void*>(&trow_kernel);
   hipError_t err = hipSuccess;
-  const int per_cu = t_prepare(fn, kRowWaves * 64, t.lds_total, &err);
+  const int per_cu = launch_prepare(fn, kRowWaves * 64, t.lds_total, &err);
   if (err != hipSuccess) return err;
   int64_t blocks = t.nwork;   // work items at 16 rows per wavefront (the kernel recounts for 8)
   const int64_t resident = (int64_t)per_cu * cus;
