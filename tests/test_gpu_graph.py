@@ -118,3 +118,39 @@ def test_accumulate_avg_replays(orc):
         assert np.array_equal(host(y), refs[i]), (i, rnd)
 
     replay_and_check(g, idx, inputs, [y], expected)
+
+
+@pytest.mark.parametrize("name,N", [("dense_hidden", 16411), ("encode_heavy_f32", 4173)])
+def test_two_phase_row_kernels_replay(orc, name, N):
+    """Row counts large enough for the row-uniform accumulate (int8 table:
+    dense_hidden; fp32 table: encode_heavy_f32), captured with a caller index
+    buffer and replayed with new inputs."""
+    p = W.make(name, N=N)
+    rng = np.random.default_rng(N + 3)
+    inputs = [p.A, rng.standard_normal(p.A.shape).astype(np.float32)]
+    A = dev(inputs[0])
+    split, thr = dev(p.split), dev(p.thr)
+    y = torch.empty((N, p.spec.M), device=DEV)
+    idx = torch.empty((N, p.spec.C), dtype=torch.uint8, device=DEV)
+    if p.spec.quantized:
+        lut, scale, offset = mdn.build_lut(dev(p.P), dev(p.B))
+        rl, rs, ro = orc.build_quantized_lut(p.P, p.B)
+        call = lambda: mdn.matmul(A, split, thr, lut, scale, offset, y_out=y, idx_out=idx)
+        refs = [orc.matmul(x, p.split, p.thr, rl, rs, ro) for x in inputs]
+        refs = [(r[0], r[2]) for r in refs]
+    else:
+        tab = mdn.build_lut_f32(dev(p.P), dev(p.B))
+        rtab = orc.build_lut_f32(p.P, p.B)
+        call = lambda: mdn.matmul_f32(A, split, thr, tab, y_out=y, idx_out=idx)
+        refs = [orc.matmul_f32(x, p.split, p.thr, rtab) for x in inputs]
+    call()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+
+    def expected(i, rnd):
+        assert np.array_equal(host(idx), refs[i][0]), (i, rnd)
+        assert np.array_equal(host(y), refs[i][1]), (i, rnd)
+
+    replay_and_check(g, A, inputs, [y, idx], expected)
