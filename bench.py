@@ -296,6 +296,38 @@ def main():
                 f = lambda i, a=act: mdn.matmul_act_f32(A_bufs[i % 2], split, thr, lut, col_bias=cb, act=a, y_out=y)
             result["context"][f"step_with_{act}_us"] = round(region_us(f), 2)
 
+        # the same step replayed from a captured HIP graph of 20 steps, as a
+        # serving loop that captures its launches runs it (launch-bound
+        # layers gain); two-phase workloads get a caller index buffer, so the
+        # captured calls allocate nothing
+        gidx = None if headline or name == "classifier_tiny" else torch.empty((N, spec.C), dtype=torch.uint8, device=dev)
+
+        def graph_step(i):
+            if spec.quantized:
+                mdn.matmul(A_bufs[i % 2], split, thr, lut, scale, offset, y_out=y, idx_out=gidx)
+            else:
+                mdn.matmul_f32(A_bufs[i % 2], split, thr, lut, y_out=y, idx_out=gidx)
+
+        for i in range(2):
+            graph_step(i)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        gsteps = 20
+        with torch.cuda.graph(graph):
+            for i in range(gsteps):
+                graph_step(i)
+        graph.replay()
+        torch.cuda.synchronize()
+        gr0, gr1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        greps = 5
+        gr0.record()
+        for _ in range(greps):
+            graph.replay()
+        gr1.record()
+        torch.cuda.synchronize()
+        result["context"]["graph_step_us"] = round(gr0.elapsed_time(gr1) / (greps * gsteps) * 1e3, 2)
+        del graph, gidx
+
         # dense fp32 GEMM of the same shape (torch -> hipBLASLt / rocBLAS), TF32 off
         torch.backends.cuda.matmul.allow_tf32 = False
         out = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
