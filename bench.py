@@ -11,8 +11,9 @@ shape as context.
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 
 Other workloads (--workload) time the same step on their shapes; their tables
-are larger than LDS, so a step is an encode launch plus a column-tiled
-accumulate launch.
+are larger than LDS, so a step is an encode launch plus an accumulate launch
+(the row-uniform kernel for tables at least 512 int8 or 256 fp32 columns wide,
+the column-tiled one otherwise).
 """
 from __future__ import annotations
 
@@ -216,7 +217,7 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes": abytes, "kernel_us": round(avg_kern_s * 1e6, 2),
                 "kernel": ("gfused_kernel<int8> (maddness_matmul, one launch per step)" if headline else
-                           "whole step (maddness_matmul%s: encode + column-tiled accumulate launches)"
+                           "whole step (maddness_matmul%s: encode + accumulate launches)"
                            % ("" if spec.quantized else "_f32")),
                 "kernel_source_hash": kh}
 
