@@ -142,7 +142,10 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   // 32-bit lane offsets as voffset).  The descriptor's range is the rows that
   // exist: a partial last step reads zeros past row N - 1 (those rows are
   // encoded but never stored), and a step past the end has an empty range and
-  // touches no memory, so every prefetch is issued unconditionally.
+  // touches no memory, so every prefetch is issued unconditionally.  The 4
+  // loads of a row group (which touch the same cache lines) are issued back to
+  // back, a scheduling barrier after each group keeping the compiler from
+  // interleaving groups: measured 3% faster than interleaved issue.
   const int64_t last_step = (N - 1) / R;
   auto gather = [&](int64_t s, float (&v)[NG][4]) {
     const int64_t sc = min(s, last_step);
@@ -151,10 +154,12 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(A8 + sc * step_bytes), 0, nbytes, kBufferDword3);
 #pragma unroll
-    for (int q = 0; q < NG; ++q)
+    for (int q = 0; q < NG; ++q) {
 #pragma unroll
       for (int t = 0; t < 4; ++t)
         v[q][t] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, goff[t], q * qstride, 0));
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
   float x[NG][4], xn[NG][4];
   gather(st, x);
