@@ -572,27 +572,29 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
           return (const tlds_t*)(uintptr_t)adr + cb * 16 * kRowBytes;
         };
         if (F) {
+          // items i = (codebook pair cp = 2 (i / NJ), row j = i % NJ), software
+          // pipelined: the two reads of item i + 1 are issued before item i is
+          // summed, so each wavefront keeps reads in flight during its sums
+          constexpr int NI = (kRowCT / 2) * NJ;
+          tu32x4 v0[2], v1[2];
+          auto rd = [&](int i, tu32x4& x0, tu32x4& x1) {
+            const int cp = 2 * (i / NJ);
+            const uint32_t dw = d[i % NJ];
+            x0 = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp, (dw >> (8 * cp)) & 15));
+            x1 = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp + 1, (dw >> (8 * cp + 8)) & 15));
+          };
+          __builtin_amdgcn_sched_barrier(0);   // every index load issued before the first table read
+          rd(0, v0[0], v1[0]);
 #pragma unroll
-          for (int cp = 0; cp < kRowCT; cp += 2) {
+          for (int i = 0; i < NI; ++i) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (i + 1 < NI) rd(i + 1, v0[(i + 1) & 1], v1[(i + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            const int j = i % NJ;
 #pragma unroll
-            for (int g = 0; g < NJ; g += kRowJG) {
-              // the reads of kRowJG rows are issued together, then summed
-              tu32x4 v0[kRowJG], v1[kRowJG];
-              __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-              for (int jj = 0; jj < kRowJG; ++jj) {
-                const uint32_t dw = d[g + jj];
-                v0[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp, (dw >> (8 * cp)) & 15));
-                v1[jj] = *reinterpret_cast<const tlds_u32x4*>(slot_of(cp + 1, (dw >> (8 * cp + 8)) & 15));
-              }
-              __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-              for (int jj = 0; jj < kRowJG; ++jj)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  acc[g + jj][e] += v0[jj][e] + v1[jj][e];
-                  asm("" : "+v"(acc[g + jj][e]));   // opaque: no reassociation across codebook pairs
-                }
+            for (int e = 0; e < 4; ++e) {
+              acc[j][e] += v0[i & 1][e] + v1[i & 1][e];
+              asm("" : "+v"(acc[j][e]));   // opaque: no reassociation across codebook pairs
             }
           }
         } else {
