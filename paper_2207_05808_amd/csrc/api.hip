@@ -329,6 +329,10 @@ bool plan_trow(const Shape& s, TArgs* t) {
   a.off_tab = take(8 * kK * 2 * kRowTileCols);   // 0: the kernel relies on it
   a.off_sh = take(s.C * 4);
   a.off_misc = take(16);
+  if (a.act != 0 && a.col_bias && (int64_t)off + round_up(s.M * 4, 16) <= kLdsBytes) {
+    a.bias_lds = 1;   // the whole bias row, staged once per workgroup
+    a.off_bias = take(s.M * 4);
+  }
   a.lds_total = off;
   if (off > kLdsBytes) return false;
   *t = a;

@@ -115,6 +115,7 @@ struct TArgs {
   const float* col_bias;  // [M] or null (layer output sigma)
   int act;                // 0 none, 1 bias, 2 bias + ReLU, 3 bias + row softmax (one column tile only)
   int off_tab, off_idx, off_sh, off_misc, lds_total;  // LDS byte offsets
+  int bias_lds, off_bias; // row-uniform kernels: column biases staged in LDS at off_bias (else read from memory)
 };
 
 // Row softmax in place over y [N][M] (layer outputs whose rows span several

@@ -42,6 +42,7 @@ typedef __attribute__((address_space(3))) uint32_t tlds_u32;
 typedef __attribute__((address_space(3))) int32_t tlds_i32;
 typedef __attribute__((address_space(3))) tu32x4 tlds_u32x4;
 typedef __attribute__((address_space(3))) tf32x4 tlds_f32x4;
+typedef __attribute__((address_space(3))) float tlds_f32;
 
 constexpr int kBufDword3 = 0x00020000;   // raw, unswizzled buffer descriptor (gfx9 family)
 constexpr int kTU = 4;                   // 16-byte table units per thread per tile (vector staging)
@@ -460,6 +461,11 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
     }
     if (lane == 0) s_misc[0] = __float_as_int((float)sum);
   }
+  // column biases of the layer output, staged once (the epilogue of every
+  // work item then reads them from LDS instead of waiting on global loads)
+  tlds_f32x4* s_bias = reinterpret_cast<tlds_f32x4*>(smem + a.off_bias);
+  if (a.bias_lds)   // (col_bias is only 4-byte aligned: one float per load)
+    for (int m = tid; m < M; m += kRowWaves * 64) reinterpret_cast<tlds_f32*>(s_bias)[m] = a.col_bias[m];
   __syncthreads();
   const int S = tuni(s_misc[2]);        // sum of 2^sh (saturated per codebook at 2^15)
   const bool fields = S <= 257;         // 255 * S <= 65535
@@ -625,11 +631,21 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
 
       // ---------------- epilogue: outputs i < 4 are columns colA + i, the rest colB + i - 4
       const int colA = m0 + 4 * lane, colB = colA + 256;
-      float cb[8];   // this lane's column biases, loaded once per work item (stores to y may alias them)
+      float cb[8];   // this lane's column biases, once per work item (stores to y may alias the global row)
+      if (a.bias_lds) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int col = (i < 4 ? colA : colB - 4) + i;
-        cb[i] = (a.act != 0 && a.col_bias && col < M) ? a.col_bias[col] : 0.0f;
+        for (int h = 0; h < 2; ++h) {   // M % 16 == 0: a quad is in range as a whole
+          const int col = h ? colB : colA;
+          const tf32x4 b4 = col < M ? s_bias[col >> 2] : (tf32x4){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cb[4 * h + e] = b4[e];
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int col = (i < 4 ? colA : colB - 4) + i;
+          cb[i] = (a.act != 0 && a.col_bias && col < M) ? a.col_bias[col] : 0.0f;
+        }
       }
       const int off128 = F ? 128 * S : 0;   // S <= 257 in field mode
 #pragma unroll
@@ -743,6 +759,10 @@ __global__ void __launch_bounds__(1024) trow_f32_kernel(const TArgs a, const uin
   const int64_t nwork = (int64_t)ntm * ((N + RB - 1) / RB);
   const int T = C / 4;   // tiles per work item (C % 4 == 0)
   int gb = 0;            // buffer of the current tile (alternates over the whole sequence)
+  // column biases of the layer output, staged once (visible after the first barrier)
+  tlds_f32x4* s_bias = reinterpret_cast<tlds_f32x4*>(s_tab + a.off_bias);
+  if (a.bias_lds)   // (col_bias is only 4-byte aligned: one float per load)
+    for (int m = tid; m < M; m += kRowWaves * 64) reinterpret_cast<tlds_f32*>(s_bias)[m] = a.col_bias[m];
   if (blockIdx.x < nwork) {
     stage(0, (int)(blockIdx.x % ntm) * kRowMtF, 0);
     publish();
@@ -793,9 +813,15 @@ __global__ void __launch_bounds__(1024) trow_f32_kernel(const TArgs a, const uin
 
     // ---------------- epilogue: this lane's columns col..col+3
     const int col = m0 + 4 * lane;
-    float cb[4];   // column biases, loaded once per work item (stores to y may alias them)
+    float cb[4];   // column biases, once per work item (stores to y may alias the global row)
+    if (a.bias_lds) {   // M % 4 == 0: a quad is in range as a whole
+      const tf32x4 b4 = col < M ? s_bias[col >> 2] : (tf32x4){0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) cb[e] = (a.act != 0 && a.col_bias && col + e < M) ? a.col_bias[col + e] : 0.0f;
+      for (int e = 0; e < 4; ++e) cb[e] = b4[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) cb[e] = (a.act != 0 && a.col_bias && col + e < M) ? a.col_bias[col + e] : 0.0f;
+    }
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int64_t row = r0 + j;
