@@ -319,6 +319,10 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   // accumulate step st.
   auto step_body = [&](float (&cur)[NG][4]) {
     const int64_t row0 = st * R;
+    // walks and the next gathers at raised wavefront priority, so that a
+    // wavefront whose data has arrived issues its next loads ahead of the
+    // other wavefronts' accumulate work
+    __builtin_amdgcn_s_setprio(2);
     // encode: one walk per (row, codebook) of this lane
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
@@ -332,6 +336,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
       }
     }
     gather(st + 2 * tw, cur);
+    __builtin_amdgcn_s_setprio(0);
     wsync();
 
     for (int rb = 0; rb < R; rb += RA) {
