@@ -409,14 +409,18 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     const int64_t row0 = ch << a.rw_log2;
     const int rows_valid = (int)min<int64_t>(RW, a.N - row0);
 
-    // 1. stage this chunk's rows in LDS, start loading the next chunk
+    // 1. stage this chunk's rows in LDS, start loading the next chunk (at
+    // raised wavefront priority: a wavefront whose rows have arrived issues
+    // its next loads ahead of the other wavefronts' walks and sums)
     if (PF > 0) {
+      __builtin_amdgcn_s_setprio(2);
       pf.store(kEnc ? sA : sI);
       const int64_t nx = ch + tw;
       if (nx < a.nchunks) {
         const int64_t nrow0 = nx << a.rw_log2;
         pf.load(src0 + nrow0 * src_rs, (int)min<int64_t>(RW, a.N - nrow0), RW, (int)src_rs);
       }
+      __builtin_amdgcn_s_setprio(0);
     } else if (kEnc) {
       for (int r = 0; r < rows_valid; ++r) {
         const float* src = a.A + (row0 + r) * a.lda;
