@@ -125,6 +125,30 @@ def test_row_layer_output(orc, M, max_shift, act):
     assert np.all(np.abs(y.astype(np.float64) - ref) <= tol)
 
 
+@pytest.mark.parametrize("M,act,bias_off", [(8192, "relu", 0), (1024, "bias", 1)])
+def test_row_layer_output_bias_placement(orc, M, act, bias_off):
+    """Column biases staged in LDS once per workgroup (M = 1024, with the bias
+    row 4 bytes off 16-byte alignment), or read from memory in every work
+    item's epilogue when the row does not fit next to the table tiles (M =
+    8192: 32 KB)."""
+    C, D = 8, 64
+    N = rows_for(M)
+    rng = np.random.default_rng(M + bias_off)
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
+    thr = rng.standard_normal((C, 15), dtype=np.float32)
+    lut, scale, offset = W.random_codes(C, M, seed=M + 3, max_shift=2)
+    bias_all = rng.standard_normal(M + bias_off).astype(np.float32)
+    bias = bias_all[bias_off:]
+    bias_dev = dev(bias_all)[bias_off:]
+    assert (bias_dev.data_ptr() % 16 == 0) == (bias_off == 0)
+    code = {"bias": 1, "relu": 2}[act]
+    y = host(mdn.matmul_act(dev(A), dev(split), dev(thr), dev(lut), dev(scale), dev(offset),
+                            col_bias=bias_dev, act=act))
+    _, _, yref = orc.matmul(A, split, thr, lut, scale, offset)
+    assert np.array_equal(y.astype(np.float64), orc.sigma(yref, bias, code))
+
+
 # ------------------------------------------------------------- fp32 tables
 def rows_for_f32(M):
     """Rows that reach the fp32 row-uniform kernel: 64 work items of 256 rows
