@@ -400,6 +400,16 @@ int accumulate(const Shape& s, hipStream_t stream) {
     if (rc != MADDNESS_OK || t.act == s.act) return rc;
     return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
   }
+  {
+    // C divides 64 and the table fits in LDS: the gather-fused kernel with
+    // index loads in place of the encode
+    GArgs g;
+    int ng, uq, gnw;
+    if (plan_gfused(s, &g, &ng, &uq, &gnw)) {
+      g.idx_in = s.idx_in;
+      return status_from(launch_gfused(s.elem, ng, uq, g, gnw, device_cus(), stream));
+    }
+  }
   if (plan_tacc(s, &t, &nj, &nw)) {
     const int rc = status_from(launch_tacc(s.elem, nj, t, nw, device_cus(), stream));
     if (rc != MADDNESS_OK || t.act == s.act) return rc;

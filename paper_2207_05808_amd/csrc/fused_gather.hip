@@ -19,7 +19,7 @@
 // table row.  The accumulate gives each lane 8 consecutive columns of one row
 // and, 4 codebooks at a time, adds the selected rows:
 //  * int8 tables whose shifted codes cannot overflow 16 bits in total
-//    (127 * sum_c 2^(e_c - e_min) <= 32767) are staged in LDS as int16
+//    (128 * sum_c 2^(e_c - e_min) <= 32768) are staged in LDS as int16
 //    values q << (e_c - e_min) and summed with packed 16-bit adds: the
 //    arithmetic is modular and the exact total fits, so the sum is exact;
 //  * other int8 tables are staged as int8 and summed with v_dot4c_i32_i8
@@ -80,7 +80,10 @@ __device__ __forceinline__ uint32_t pk_add16(uint32_t a, uint32_t b) {
 // LDS layout (bytes): [table: C*16 rows + 1 zero row, rs bytes each (sized for
 // the widest staging)][shift per codebook][misc]
 // [per wavefront: R rows x NSP int32 table offsets]
-template <int ELEM, int NG, int UQ>
+// IDX: the accumulate-only entry points.  The same kernel with the encode
+// replaced by loads of the given indices: lane (row, codebook) loads one
+// index byte per row group instead of 4 values of A, two steps in flight.
+template <int ELEM, int NG, int UQ, bool IDX>
 __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   glds_t* smem = (glds_t*)smem_raw;
@@ -111,7 +114,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   // while the table is staged.
   int sp[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) sp[t] = g.split[c * 4 + t];
+  for (int t = 0; t < 4; ++t) sp[t] = IDX ? 0 : g.split[c * 4 + t];
   const uint32_t sbits = (ELEM == kI8) ? __float_as_uint(g.scale[c]) : 0u;
   const float ofs = (ELEM == kI8) ? g.offset[c] : 0.0f;
 
@@ -125,18 +128,20 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   for (int j = 0; j < kTabUnits; ++j)
     tv[j] = __builtin_amdgcn_raw_buffer_load_b128(trs, (tid + j * (int)blockDim.x) * 16, 0, 0);
 
-  const unsigned dmax = (unsigned)(g.D - 1);
+  const unsigned dmax = IDX ? 0u : (unsigned)(g.D - 1);
   // byte offsets from the step's first row (split columns clamped: memory
   // safety); group q of G rows adds the uniform q * G * lda * 4 as soffset
   int goff[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) goff[t] = (int)(((int64_t)gsub * g.lda + min((unsigned)sp[t], dmax)) * 4);
-  const int qstride = (int)((int64_t)G * g.lda * 4);
+  for (int t = 0; t < 4; ++t)
+    goff[t] = IDX ? gsub * C + c : (int)(((int64_t)gsub * g.lda + min((unsigned)sp[t], dmax)) * 4);
+  // (indices: rows of C bytes)
+  const int qstride = IDX ? G * C : (int)((int64_t)G * g.lda * 4);
 
   const int64_t tw = (int64_t)gridDim.x * nw;
   int64_t st = (int64_t)blockIdx.x * nw + wave;   // step index: rows [st * R, st * R + R)
-  const char* A8 = reinterpret_cast<const char*>(g.A);
-  const int64_t step_bytes = (int64_t)R * g.lda * 4;
+  const char* A8 = IDX ? reinterpret_cast<const char*>(g.idx_in) : reinterpret_cast<const char*>(g.A);
+  const int64_t step_bytes = IDX ? (int64_t)R * C : (int64_t)R * g.lda * 4;
 
   // Buffer loads against a per-step descriptor (uniform base in SGPRs, the
   // 32-bit lane offsets as voffset).  The descriptor's range is the rows that
@@ -150,9 +155,18 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   auto gather = [&](int64_t s, float (&v)[NG][4]) {
     const int64_t sc = min(s, last_step);
     const int64_t rows = s > last_step ? 0 : min((int64_t)R, N - s * R);
-    const int32_t nbytes = rows > 0 ? (int32_t)min(step_bytes, (rows - 1) * g.lda * 4 + (int64_t)g.D * 4) : 0;
+    const int32_t nbytes =
+        rows > 0 ? (int32_t)(IDX ? rows * C : min(step_bytes, (rows - 1) * g.lda * 4 + (int64_t)g.D * 4)) : 0;
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(A8 + sc * step_bytes), 0, nbytes, kBufferDword3);
+    if (IDX) {
+#pragma unroll
+      for (int q = 0; q < NG; ++q) {
+        v[q][0] = __int_as_float((int)__builtin_amdgcn_raw_buffer_load_b8(rsrc, goff[0], q * qstride, 0));
+        v[q][1] = v[q][2] = v[q][3] = 0.0f;
+      }
+      return;
+    }
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
 #pragma unroll
@@ -165,10 +179,13 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   gather(st, x);
   gather(st + tw, xn);
 
-  const float* th = g.thr + c * kNodes;
-  const float t0 = th[0], t1 = th[1], t2 = th[2], t3 = th[3], t4 = th[4], t5 = th[5], t6 = th[6],
-              t7 = th[7], t8 = th[8], t9 = th[9], t10 = th[10], t11 = th[11], t12 = th[12], t13 = th[13],
-              t14 = th[14];
+  float t0 = 0, t1 = 0, t2 = 0, t3 = 0, t4 = 0, t5 = 0, t6 = 0, t7 = 0, t8 = 0, t9 = 0, t10 = 0, t11 = 0,
+        t12 = 0, t13 = 0, t14 = 0;
+  if (!IDX) {
+    const float* th = g.thr + c * kNodes;
+    t0 = th[0]; t1 = th[1]; t2 = th[2]; t3 = th[3]; t4 = th[4]; t5 = th[5]; t6 = th[6]; t7 = th[7];
+    t8 = th[8]; t9 = th[9]; t10 = th[10]; t11 = th[11]; t12 = th[12]; t13 = th[13]; t14 = th[14];
+  }
 
   // ---------------- dequantization constants, reduced inside each wavefront
   // (lane l holds codebook l % C; every wavefront reaches the same values)
@@ -180,7 +197,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   int pw = (lane < C) ? (sh <= 14 ? (1 << sh) : (1 << 15)) : 0;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) pw += __shfl_xor(pw, o);
-  const bool narrow = (ELEM == kI8) && (127 * pw <= 32767);
+  const bool narrow = (ELEM == kI8) && (128 * pw <= 32768);   // every int8 code, -128 included
   const int rs = (ELEM == kF32) ? g.rs32 : (narrow ? g.rs16 : g.rs8);
   const float step = __builtin_ldexpf(1.0f, emin);
   if (wave == 0) {
@@ -326,8 +343,10 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
     // encode: one walk per (row, codebook) of this lane
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
-      const int k = walk(cur[q][0], cur[q][1], cur[q][2], cur[q][3], t0, t1, t2, t3, t4, t5, t6, t7, t8, t9,
-                         t10, t11, t12, t13, t14);
+      // (indices are preconditions in [0, 16); the mask keeps LDS reads in the table)
+      const int k = IDX ? (__float_as_int(cur[q][0]) & 15)
+                        : walk(cur[q][0], cur[q][1], cur[q][2], cur[q][3], t0, t1, t2, t3, t4, t5, t6, t7, t8, t9,
+                               t10, t11, t12, t13, t14);
       const int r = q * G + gsub;
       s_off[r * NSP + c] = cbase + k * rs;
       if (g.idx_out) {
@@ -460,8 +479,9 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
           if (qd >= nq4) continue;
           const int mh = 4 * qd;
           if (g.vec_out && mh + 4 <= M) {
-            __builtin_nontemporal_store((f32x4g){o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]},
-                                        reinterpret_cast<f32x4g*>(yrow + mh));
+            if (g.y)
+              __builtin_nontemporal_store((f32x4g){o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]},
+                                          reinterpret_cast<f32x4g*>(yrow + mh));
             if (arow)
               __builtin_nontemporal_store((u32x4g){(uint32_t)iacc[u][4 * h], (uint32_t)iacc[u][4 * h + 1],
                                                    (uint32_t)iacc[u][4 * h + 2], (uint32_t)iacc[u][4 * h + 3]},
@@ -470,7 +490,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               if (mh + e < M) {
-                yrow[mh + e] = o[4 * h + e];
+                if (g.y) yrow[mh + e] = o[4 * h + e];
                 if (arow) arow[mh + e] = iacc[u][4 * h + e];
               }
           }
@@ -548,9 +568,9 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   }
 }
 
-template <int ELEM, int NG, int UQ>
+template <int ELEM, int NG, int UQ, bool IDX>
 static hipError_t glaunch(const GArgs& g, int nw, int cus, hipStream_t stream) {
-  const void* fn = reinterpret_cast<const void*>(&gfused_kernel<ELEM, NG, UQ>);
+  const void* fn = reinterpret_cast<const void*>(&gfused_kernel<ELEM, NG, UQ, IDX>);
   hipError_t err = hipSuccess;
   const int per_cu = launch_prepare(fn, nw * 64, g.lds_total, &err);
   if (err != hipSuccess) return err;
@@ -559,12 +579,13 @@ static hipError_t glaunch(const GArgs& g, int nw, int cus, hipStream_t stream) {
   const int64_t resident = (int64_t)per_cu * cus;
   if (blocks > resident) blocks = resident;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL((gfused_kernel<ELEM, NG, UQ>), dim3((unsigned)blocks), dim3(nw * 64), g.lds_total, stream, g);
+  hipLaunchKernelGGL((gfused_kernel<ELEM, NG, UQ, IDX>), dim3((unsigned)blocks), dim3(nw * 64), g.lds_total, stream, g);
   return hipGetLastError();
 }
 
 #define MDN_G_CASE(E, NG, UQ) \
-  if (elem == E && ng == NG && uq == UQ) return glaunch<E, NG, UQ>(g, nw, cus, stream);
+  if (elem == E && ng == NG && uq == UQ)                                   \
+    return g.idx_in ? glaunch<E, NG, UQ, true>(g, nw, cus, stream) : glaunch<E, NG, UQ, false>(g, nw, cus, stream);
 
 hipError_t launch_gfused(int elem, int ng, int uq, const GArgs& g, int nw, int cus, hipStream_t stream) {
   MDN_G_CASE(kI8, 1, 1) MDN_G_CASE(kI8, 2, 1) MDN_G_CASE(kI8, 4, 1)

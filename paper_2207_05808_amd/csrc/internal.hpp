@@ -71,9 +71,10 @@ struct GArgs {
   const void* lut;        // [C][16][M] int8 or fp32
   const float* scale;     // [C]
   const float* offset;    // [C]
-  float* y;               // [N][M]
+  float* y;               // [N][M] (null: accumulate-only calls with acc only)
   int32_t* acc;           // [N][M] or null
   uint8_t* idx_out;       // [N][C] or null
+  const uint8_t* idx_in;  // [N][C]: accumulate only (no encode) when not null
   int64_t N;
   int64_t lda;
   int D, C, M;

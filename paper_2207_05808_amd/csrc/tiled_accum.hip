@@ -19,7 +19,7 @@
 // current tile is summed.  Accumulators stay in registers across codebook
 // tiles, so fp32 sums keep the ascending codebook order.
 //  * int8 tables whose shifted codes cannot overflow 16 bits in total
-//    (127 * sum_c 2^(e_c - e_min) <= 32767) are staged as int16 q << (e_c -
+//    (128 * sum_c 2^(e_c - e_min) <= 32768) are staged as int16 q << (e_c -
 //    e_min) and summed with packed 16-bit adds: modular arithmetic whose exact
 //    total fits, so the sum equals the int32 sum;
 //  * other int8 tables are staged as int16 q and summed in int32 with shifts;
@@ -146,7 +146,7 @@ __global__ void __launch_bounds__(512, 4) tacc_kernel(const TArgs a) {
       if (lane == 0) s_misc[0] = __float_as_int((float)sum);
     }
     __syncthreads();
-    narrow = 127 * tuni(s_misc[2]) <= 32767;
+    narrow = 128 * tuni(s_misc[2]) <= 32768;   // every int8 code, -128 included
     step = __builtin_ldexpf(1.0f, emin);
     bias = __int_as_float(tuni(s_misc[0]));
   }

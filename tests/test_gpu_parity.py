@@ -136,6 +136,25 @@ def test_lut_accumulate_single_outputs(orc):
     assert_y(host(y), ry)
 
 
+@pytest.mark.parametrize("C,shifts", [(4, (7, 6, 6, 0)), (12, (7, 6, 5, 3, 3, 2, 2, 1, 1, 1, 1, 0))])
+@pytest.mark.parametrize("code", [-128, 127])
+def test_lut_accumulate_16bit_bound(orc, C, shifts, code):
+    """sum_c 2^sh = 257: 127 * 257 fits a 16-bit lane but -128 * 257 does
+    not, so these tables must take the 32-bit sums (C = 4: the gather-fused
+    kernel with index loads; C = 12: the column-tiled kernel)."""
+    N, M = 3000, 64
+    rng = np.random.default_rng(C + code + 256)
+    idx = rng.integers(0, 16, size=(N, C)).astype(np.uint8)
+    lut = np.full((C, 16, M), code, dtype=np.int8)
+    lut[:, :, 1] = rng.integers(-128, 128, size=(C, 16)).astype(np.int8)
+    scale = np.ldexp(np.float32(1.0), np.array(shifts, dtype=np.int32) - 10).astype(np.float32)
+    offset = rng.standard_normal(C).astype(np.float32)
+    acc, y = mdn.lut_accumulate(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=True, validate=True)
+    racc, ry = orc.lut_accumulate(idx, lut, scale, offset)
+    assert np.array_equal(host(acc), racc)
+    assert np.array_equal(host(y), ry)
+
+
 @pytest.mark.parametrize("C,M", [(1, 1), (3, 10), (32, 64), (64, 512), (256, 1024), (7, 33), (200, 5)])
 def test_lut_accumulate_f32_random(orc, C, M):
     N = 1111
