@@ -21,7 +21,8 @@ Functions and the passages they follow (the paper: McCarter & Dronen,
 * :func:`encoder_gram`, :func:`encoder_scatter`, :func:`fit_lut_ridge` --
   §2.2, Eq. 3 (model-aware table fit) with sigma affine, reading R21.
 * :func:`fit_lut_gd` -- Eq. 3 with sigma = ReLU (squared error) or softmax
-  (KL divergence, the objective of §3.1), gradient descent, reading R22.
+  (KL divergence, the alternative §3.1 uses for classifiers, or the squared
+  error of Eq. 3 itself), gradient descent, reading R22.
 """
 from __future__ import annotations
 
@@ -273,7 +274,8 @@ class Oracle:
 
     def fit_lut_gd(self, idx, Y, T0, act, lam, eta, iters, bias=None):
         """Eq. 3 with a nonlinear sigma (R22): act 2 = ReLU + squared error,
-        3 = softmax + KL divergence; gradient descent from T0.  float64 [C, 16, M]."""
+        3 = softmax + KL divergence, 4 = softmax + squared error; gradient
+        descent from T0.  float64 [C, 16, M]."""
         idx = np.ascontiguousarray(idx, dtype=np.uint8)
         Y = np.ascontiguousarray(Y, dtype=np.float32)
         T0 = np.ascontiguousarray(T0, dtype=np.float32)

@@ -27,8 +27,13 @@
  *   R6  quantizer: offset = midrange, exponent = the smallest that fits every
  *       code in [-127, 127] (no clipping), raised to within `cap` of the
  *       largest exponent so the int32 sum stays exact in fp32.
- *   R9  y = fl32( float(acc) * 2^e_min + bias32 ), one rounding (fmaf), with
- *       bias32 = fl32( sum_c offset_c accumulated in double, c ascending ).
+ *   R7  acc = sum_c q_c 2^(e_c - e_min) exactly in int32: any int8 codes are
+ *       admitted when 128 * sum_c 2^(e_c - e_min) <= 2^31.
+ *   R9  y = fmaf( float(acc), 2^e_min, bias32 ), with bias32 = fl32( sum_c
+ *       offset_c accumulated in double, c ascending ).  float(acc) is exact
+ *       while |acc| <= 2^24 (always so for tables from the quantizer, R6), and
+ *       y is then one rounding of acc 2^e_min + bias32; a larger |acc| is
+ *       rounded to fp32 first (two roundings).
  *   R10 unquantized mode: y = (((0 + T_0) + T_1) + ...) in fp32, c ascending.
  *   R21 model-aware table fit (Eq. 3) with sigma affine (bias and identity,
  *       so the bias cancels): minimise sum_n ||y_n - g_n^T T||^2 +
@@ -47,8 +52,13 @@
  *       ascending, in double) + b.  ReLU: objective sum_n ||relu(y_n + b) -
  *       relu(z_n)||^2, residual r = 2 (relu(z) - relu(y + b)) [z > 0].
  *       Softmax: objective sum_n KL(softmax(y_n + b) || softmax(z_n)),
- *       residual r = softmax(z) - softmax(y + b).  Step: R = G^T r (rows
- *       ascending from 0), g = R + 2 lambda (T - T0), T = T - eta g.
+ *       residual r = softmax(z) - softmax(y + b).  Softmax with the squared
+ *       error of Eq. 3 itself: objective sum_n ||softmax(z_n) -
+ *       softmax(y_n + b)||^2; with p = softmax(z), d = p - softmax(y + b)
+ *       and s = sum_m d_m p_m (m ascending), the residual (the chain rule
+ *       through the softmax Jacobian diag(p) - p p^T) is r_m = 2 p_m (d_m - s).
+ *       Step: R = G^T r (rows ascending from 0), g = R + 2 lambda (T - T0),
+ *       T = T - eta g.
  *   R19 layer output sigma: z = fl32(y + bias_m); ReLU keeps z when z > 0 and
  *       gives +0 otherwise; softmax is taken over the M outputs of a row.
  *   R20 rounded 8-bit summation: one shared block exponent; biased codes
@@ -131,7 +141,9 @@ int oracle_block_exponent(float scale, int32_t* e)
 
 /* Dequantization constants shared by every output (R5, R9): per-codebook
  * shifts sh_c = e_c - e_min, e_min, and bias32.  Also checks that the int32
- * accumulator cannot overflow: 127 * sum_c 2^sh_c < 2^31. */
+ * accumulator cannot overflow for any int8 codes (R7): the most negative sum
+ * is -128 * sum_c 2^sh_c, which must be >= -2^31, and the largest,
+ * 127 * sum_c 2^sh_c, is then below 2^31 - 1. */
 int oracle_dequant_params(const float* scale, const float* offset, int32_t C,
                           int32_t* sh, int32_t* e_min, float* bias32)
 {
@@ -147,9 +159,9 @@ int oracle_dequant_params(const float* scale, const float* offset, int32_t C,
     for (int32_t c = 0; c < C; ++c) {
         sh[c] -= emin;
         if (sh[c] > 30) return -3;
-        bound += 127.0 * ldexp(1.0, sh[c]);
+        bound += 128.0 * ldexp(1.0, sh[c]);
     }
-    if (bound >= 2147483648.0) return -3;
+    if (bound > 2147483648.0) return -3;
     double s = 0.0;
     for (int32_t c = 0; c < C; ++c) s += (double)offset[c];
     *e_min = emin;
@@ -544,7 +556,9 @@ static void softmax_row(const double* z, int32_t M, double* q)
 /*
  * Model-aware table fit, Eq. 3 with a nonlinear layer output (reading R22):
  * act 2 = bias + ReLU with the squared-error objective, act 3 = bias + row
- * softmax with the KL-divergence objective, both plus lambda ||T - T0||^2.
+ * softmax with the KL-divergence objective (the alternative §3.1 uses for
+ * classifier layers), act 4 = bias + row softmax with the squared-error
+ * objective (Eq. 3 as written), each plus lambda ||T - T0||^2.
  * Full-batch gradient descent from T = T0: `iters` steps of size eta.  The
  * bias is optional (NULL = zeros).  T is [C][16][M] double.  Returns -1 on
  * bad sizes, -2 on a bad act, lambda, eta or iteration count.
@@ -554,7 +568,7 @@ int oracle_fit_lut_gd(const uint8_t* idx, int64_t N, int32_t C, const float* Y, 
                       int32_t iters, double* T)
 {
     if (N < 0 || C <= 0 || M <= 0 || !T0 || !T || (N > 0 && (!idx || !Y))) return -1;
-    if ((act != 2 && act != 3) || !(lambda >= 0.0) || !isfinite(lambda) || !(eta > 0.0) ||
+    if ((act != 2 && act != 3 && act != 4) || !(lambda >= 0.0) || !isfinite(lambda) || !(eta > 0.0) ||
         !isfinite(eta) || iters < 0)
         return -2;
     const int64_t n16 = (int64_t)C * ORACLE_K;
@@ -584,9 +598,17 @@ int oracle_fit_lut_gd(const uint8_t* idx, int64_t N, int32_t C, const float* Y, 
             if (act == 2) {
                 for (int32_t m = 0; m < M; ++m)
                     q[m] = z[m] > 0.0 ? 2.0 * (z[m] - P[n * M + m]) : 0.0;
-            } else {
+            } else if (act == 3) {
                 softmax_row(z, M, q);
                 for (int32_t m = 0; m < M; ++m) q[m] = q[m] - P[n * M + m];
+            } else {
+                softmax_row(z, M, q);                    /* q = p */
+                double sdp = 0.0;
+                for (int32_t m = 0; m < M; ++m) sdp += (q[m] - P[n * M + m]) * q[m];
+                for (int32_t m = 0; m < M; ++m) {
+                    const double d = q[m] - P[n * M + m];
+                    q[m] = 2.0 * (q[m] * (d - sdp));
+                }
             }
             for (int32_t c = 0; c < C; ++c) {
                 const int64_t r = (int64_t)c * ORACLE_K + idx[n * C + c];

@@ -349,10 +349,50 @@ def check_quantizer(orc, seed=8):
         assert offset[c] == np.float32((lo + hi) / 2)
 
 
+def rne32_or_inf(x: Fraction) -> float:
+    """rne32 extended past the top binade: a value that rounds to 2^128 or
+    beyond (at or above FLT_MAX + half an ulp, ties to even) is infinite."""
+    r = rne32(x)
+    return math.copysign(math.inf, r) if abs(r) >= 2.0 ** 128 else r
+
+
+def check_round_table_f32(orc, seed=23):
+    """Unquantized tables: every double entry is rounded to the nearest fp32,
+    ties to even (R10's table), checked bit for bit against exact rational
+    rounding on random doubles of every magnitude, exact halfway cases
+    (even and odd neighbours), the top of the range (FLT_MAX, the halfway
+    point above it, overflow to infinity), subnormals and signed zeros."""
+    rng = np.random.default_rng(seed)
+    vals = list(rng.standard_normal(400) * 10.0 ** rng.integers(-30, 30, size=400))
+    vals += list(rng.standard_normal(100) * 2.0 ** -140)               # subnormal results
+    for _ in range(200):                                                 # exact halfway cases
+        f = float(np.float32(rng.standard_normal() * 10.0 ** int(rng.integers(-20, 20))))
+        ulp = float(np.spacing(np.float32(abs(f))))
+        vals.append(f + math.copysign(ulp / 2, f))
+        vals.append(-(abs(f) + ulp / 2))
+    fmax = float(np.finfo(np.float32).max)
+    top = 2.0 ** 104                                                     # ulp of the top binade
+    vals += [fmax, -fmax, fmax + top / 4, fmax + top / 2, -(fmax + top / 2), fmax * 1.5, 1e300,
+             2.0 ** -149, 2.0 ** -150, 3 * 2.0 ** -151, 2.0 ** -151, 2.0 ** -126 - 2.0 ** -150,
+             0.0, -0.0, 1.0, -1.0, 1.0 + 2.0 ** -24, 1.0 + 3 * 2.0 ** -24]
+    T = np.array(vals, np.float64)
+    out = orc.round_table_f32(T)
+    assert out.dtype == np.float32 and out.shape == T.shape
+    for t, o in zip(T, out):
+        want = np.float32(rne32_or_inf(Fraction(float(t))))
+        if t == 0.0:
+            want = np.float32(t)                                         # the sign of zero is kept
+        assert o.tobytes() == want.tobytes(), f"round({t!r}) = {o!r}, want {want!r}"
+
+
 def check_f32_reconstruction(orc, seed=9):
     """Unquantized mode against the fp64 reconstruction A_hat B, A_hat the
-    sum of the selected prototypes: |y - A_hat B| <= gamma_C^(32) sum|T32|
-    + sum_c |T32 - T| with T the exact table entries (rigorous bound)."""
+    sum of the selected prototypes.  With T the exact table entries, each
+    fp32 entry is within 2^-24 |T| of T (round to nearest) and the ordered
+    fp32 sum of C entries errs by at most gamma_C^(32) sum |T32| <=
+    gamma_C^(32) (1 + 2^-24) sum |T|, so |y - A_hat B| <= (gamma_C^(32)
+    (1 + 2^-24) + 2^-24) sum_c |T_c| plus the double roundings of T and of
+    the reference: a rigorous bound that does not use the oracle's own table."""
     rng = np.random.default_rng(seed)
     N, C, L, M = 40, 6, 3, 7
     D = C * L
@@ -370,9 +410,9 @@ def check_f32_reconstruction(orc, seed=9):
         Ahat = sum(P[c, idx[n, c]].astype(np.float64) for c in range(C))
         for m in range(M):
             ref = math.fsum(Ahat * B[:, m].astype(np.float64))
-            t32 = np.array([T32[c, idx[n, c], m] for c in range(C)], np.float64)
             tx = np.array([Tx[c, idx[n, c], m] for c in range(C)])
-            bound = gamma(C, U32) * np.abs(t32).sum() + np.abs(t32 - tx).sum() + 4 * U64 * abs(ref)
+            ax = float(np.abs(tx).sum())
+            bound = (gamma(C, U32) * (1 + U32) + U32) * ax + 2 * U64 * ax + 4 * U64 * abs(ref)
             assert abs(float(y[n, m]) - ref) <= bound, f"({n},{m}) outside reconstruction bound"
 
 
@@ -402,6 +442,45 @@ def check_quantized_reconstruction(orc, seed=10):
             bound = (half + abs(float(bias) - S) + U32 * abs(float(y[n, m])) + gamma(D, U64) * tab
                      + 4 * U64 * abs(ref))
             assert abs(float(y[n, m]) - ref) <= bound * (1 + 1e-9), f"({n},{m}) outside bound"
+
+
+def bound_shifts():
+    """Shifts e_c - e_min whose sum of 2^sh is exactly 2^24: 23, 22, ..., 0, 0.
+    With every code -128 the sum is -128 * 2^24 = -2^31, the int32 minimum."""
+    return np.array(list(range(23, -1, -1)) + [0], np.int64)
+
+
+def check_accumulator_bound(orc, seed=24):
+    """R7: any int8 codes are admitted exactly when the most negative sum,
+    -128 sum_c 2^sh_c, fits int32.  At sum 2^sh = 2^24 every code -128 sums
+    to exactly -2^31 and every code 127 to 127 * 2^24 (both admitted, both
+    exact); one more unit of 2^sh, or shifts (24, 0), is rejected although
+    127 sum 2^sh is still below 2^31."""
+    from oracle import OracleError
+    rng = np.random.default_rng(seed)
+    sh = bound_shifts()
+    C, N, M = len(sh), 30, 5
+    assert int((2 ** sh).sum()) == 2 ** 24
+    e_min = -40
+    scale = np.ldexp(np.float32(1), (sh + e_min).astype(np.int32)).astype(np.float32)
+    idx = rng.integers(0, K, size=(N, C)).astype(np.uint8)
+    for code, want in ((-128, -2 ** 31), (127, 127 * 2 ** 24)):
+        acc, y = orc.lut_accumulate(idx, np.full((C, K, M), code, np.int8), scale, np.zeros(C, np.float32))
+        assert np.all(acc.astype(np.int64) == want), f"codes {code}: acc {acc[0, 0]} != {want}"
+        assert np.all(y == np.float32(rne32(Fraction(want) * Fraction(2) ** e_min)))
+    # mixed codes at the bound against the exact integer sum
+    lut = rng.integers(-128, 128, size=(C, K, M)).astype(np.int8)
+    acc, _ = orc.lut_accumulate(idx, lut, scale, np.zeros(C, np.float32))
+    assert np.array_equal(acc.astype(np.int64), one_hot(idx) @ (lut.astype(np.int64) * (2 ** sh)[:, None, None]).reshape(C * K, M))
+    over = [np.append(sh, 0), np.array([24, 0])]
+    for bad in over:
+        assert 127 * int((2 ** bad).sum()) < 2 ** 31 < 128 * int((2 ** bad).sum())
+        sc = np.ldexp(np.float32(1), (bad + e_min).astype(np.int32)).astype(np.float32)
+        try:
+            orc.dequant_params(sc, np.zeros(len(bad), np.float32))
+        except OracleError:
+            continue
+        raise AssertionError(f"shifts {bad.tolist()} admitted although -128 codes overflow int32")
 
 
 def check_rejects_bad_inputs(orc):
@@ -701,7 +780,8 @@ def check_fit_optimality(orc, seed=19):
 # ------------------------------------------- table fit, nonlinear sigma (R22)
 def _gd_objective(idx, Y, T, T0, lam, act, bias):
     """Eq. 3 evaluated directly: act 2 = squared error after bias + ReLU, act 3
-    = KL divergence between the row softmaxes (scipy), plus lam ||T - T0||^2."""
+    = KL divergence between the row softmaxes (scipy), act 4 = squared error
+    between the row softmaxes (scipy), plus lam ||T - T0||^2."""
     from scipy.special import rel_entr, softmax
     b = np.zeros(Y.shape[1]) if bias is None else bias.astype(np.float64)
     z = _gather(idx, T) + b
@@ -709,8 +789,11 @@ def _gd_objective(idx, Y, T, T0, lam, act, bias):
     if act == 2:
         r = np.maximum(t, 0.0) - np.maximum(z, 0.0)
         f = float((r * r).sum())
-    else:
+    elif act == 3:
         f = float(rel_entr(softmax(t, axis=1), softmax(z, axis=1)).sum())
+    else:
+        r = softmax(z, axis=1) - softmax(t, axis=1)
+        f = float((r * r).sum())
     d = np.asarray(T, np.float64) - np.asarray(T0, np.float64)
     return f + lam * float((d * d).sum())
 
@@ -719,10 +802,11 @@ def check_fit_gd_gradient(orc, seed=20):
     """One gradient step moves T by -eta times the gradient of Eq. 3's
     objective: (T_k - T_{k+1}) / eta matches central finite differences of the
     objective (evaluated directly), at T0 and after a first step (where the
-    penalty contributes), for ReLU and softmax, with and without a bias."""
+    penalty contributes), for ReLU, softmax with the KL divergence and softmax
+    with the squared error, with and without a bias."""
     rng = np.random.default_rng(seed)
     idx, Y, T0 = _fit_problem(30, 2, 4, seed)
-    for act in (2, 3):
+    for act in (2, 3, 4):
         for bias in (None, rng.standard_normal(4).astype(np.float32)):
             lam, eta = 0.3, 1e-3
             T1 = orc.fit_lut_gd(idx, Y, T0, act, lam, eta, 1, bias)
@@ -755,34 +839,38 @@ def check_fit_gd_fixed_point(orc, seed=21):
     assert np.array_equal(T, T0.astype(np.float64))
     shift = rng.integers(-4, 5, size=(N, 1)).astype(np.float64)
     Ys = (_gather(idx, T0) + shift).astype(np.float32)
-    T = orc.fit_lut_gd(idx, Ys, T0, 3, 0.5, 0.01, 25, bias)
-    assert np.abs(T - T0).max() <= 1e-12
+    for act in (3, 4):
+        T = orc.fit_lut_gd(idx, Ys, T0, act, 0.5, 0.01, 25, bias)
+        assert np.abs(T - T0).max() <= 1e-12
 
 
 def check_fit_gd_descent_and_limit(orc, seed=22):
-    """Small steps never raise the objective (softmax: convex; ReLU from a
-    generic start), and many steps reach the minimiser a generic method
-    (scipy BFGS on the directly evaluated objective) finds on a tiny case."""
+    """Small steps never raise the objective (softmax with KL: convex; ReLU
+    and softmax with the squared error from a generic start), and many steps
+    reach the minimiser a generic method (scipy BFGS on the directly
+    evaluated objective) finds on a tiny case."""
     from scipy.optimize import minimize
     idx, Y, T0 = _fit_problem(40, 2, 3, seed)
     bias = np.array([0.2, -0.1, 0.4], np.float32)
-    for act in (2, 3):
+    for act in (2, 3, 4):
         fs = [_gd_objective(idx, Y, orc.fit_lut_gd(idx, Y, T0, act, 0.2, 5e-3, k, bias), T0, 0.2, act, bias)
               for k in range(0, 6)]
         assert all(b <= a + 1e-12 for a, b in zip(fs, fs[1:])) and fs[-1] < fs[0]
     idx, Y, T0 = _fit_problem(16, 1, 2, seed + 1)
     lam = 0.5
-    T = orc.fit_lut_gd(idx, Y, T0, 3, lam, 0.2, 4000)
-    res = minimize(lambda v: _gd_objective(idx, Y, v.reshape(1, K, 2), T0, lam, 3, None),
-                   T0.astype(np.float64).ravel(), method="BFGS", options={"gtol": 1e-12})
-    assert np.abs(res.x.reshape(1, K, 2) - T).max() <= 1e-5
+    for act in (3, 4):
+        T = orc.fit_lut_gd(idx, Y, T0, act, lam, 0.2, 4000)
+        res = minimize(lambda v: _gd_objective(idx, Y, v.reshape(1, K, 2), T0, lam, act, None),
+                       T0.astype(np.float64).ravel(), method="BFGS", options={"gtol": 1e-12})
+        assert np.abs(res.x.reshape(1, K, 2) - T).max() <= 1e-5, act
 
 
 ALL_CHECKS = [
     check_encode_brute_force, check_encode_search_tree, check_encode_nan, check_encode_permutation,
     check_encode_golden, check_one_hot_identity, check_decoder_table, check_output_rounding,
     check_scale_linearity, check_f32_order, check_table_build, check_quantizer,
-    check_f32_reconstruction, check_quantized_reconstruction, check_rejects_bad_inputs,
+    check_round_table_f32, check_f32_reconstruction, check_quantized_reconstruction, check_accumulator_bound,
+    check_rejects_bad_inputs,
     check_sigma_bias_relu, check_sigma_softmax, check_avg_closed_forms, check_avg_bounds,
     check_shared_quantizer, check_encoder_gram, check_encoder_scatter, check_fit_closed_forms,
     check_fit_optimality, check_fit_gd_gradient, check_fit_gd_fixed_point, check_fit_gd_descent_and_limit,

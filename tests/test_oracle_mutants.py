@@ -66,6 +66,24 @@ MUTANTS = [
     ("step up the gradient", "T[j] = T[j] - eta * g;", "T[j] = T[j] + eta * g;"),
     ("softmax sum over half the row", "for (int32_t m = 0; m < M; ++m) { q[m] = exp(z[m] - mx); sum += q[m]; }",
      "for (int32_t m = 0; m < M; ++m) { q[m] = exp(z[m] - mx); if (m < M / 2 + 1) sum += q[m]; }"),
+    ("fp32 table zeroed", "for (int64_t j = 0; j < n; ++j) out[j] = (float)T[j];",
+     "for (int64_t j = 0; j < n; ++j) out[j] = 0.0f * (float)T[j];"),
+    ("fp32 table scaled by 1.001", "for (int64_t j = 0; j < n; ++j) out[j] = (float)T[j];",
+     "for (int64_t j = 0; j < n; ++j) out[j] = (float)(T[j] * 1.001);"),
+    ("fp32 table rounded toward zero", "for (int64_t j = 0; j < n; ++j) out[j] = (float)T[j];",
+     "for (int64_t j = 0; j < n; ++j) { float f = (float)T[j]; "
+     "if (fabs((double)f) > fabs(T[j])) f = nextafterf(f, 0.0f); out[j] = f; }"),
+    ("overflow bound for codes up to 127 only", "bound += 128.0 * ldexp(1.0, sh[c]);",
+     "bound += 127.0 * ldexp(1.0, sh[c]);"),
+    ("overflow bound excludes its edge", "if (bound > 2147483648.0) return -3;",
+     "if (bound >= 2147483648.0) return -3;"),
+    ("softmax squared-error residual without the Jacobian", "q[m] = 2.0 * (q[m] * (d - sdp));",
+     "q[m] = 2.0 * d;"),
+    ("softmax squared-error residual without the centring term", "q[m] = 2.0 * (q[m] * (d - sdp));",
+     "q[m] = 2.0 * (q[m] * d);"),
+    ("softmax squared-error centring term unweighted",
+     "for (int32_t m = 0; m < M; ++m) sdp += (q[m] - P[n * M + m]) * q[m];",
+     "for (int32_t m = 0; m < M; ++m) sdp += (q[m] - P[n * M + m]);"),
 ]
 
 
