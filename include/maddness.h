@@ -17,12 +17,12 @@
  *    library keeps no pointer after the call returns; the caller keeps the
  *    buffers alive until the work on `stream` has completed.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  The
- *    calls only enqueue work on it: no host synchronisation.  Only the fused
- *    entry points (maddness_matmul, maddness_matmul_f32, maddness_matmul_act,
- *    maddness_matmul_act_f32) may allocate (stream-ordered) a temporary index
- *    buffer, when the table is too large for one LDS tile and idx_out is
- *    NULL; every other call allocates nothing (and can be captured in a HIP
- *    graph).
+ *    calls only enqueue work on it: no host synchronisation and no device
+ *    allocation, so every call can be captured in a HIP graph.  Where a call
+ *    needs device memory beyond its inputs and outputs, the caller passes it:
+ *    the index array of the fused entry points for tables too large for
+ *    their single-launch kernels (maddness_matmul_index_bytes), and the
+ *    workspaces of the table fit.
  *  - Row-major layouts.  A has row stride `lda` (elements, lda >= D); every
  *    other array is dense.
  *  - Return value: MADDNESS_OK or an error status (never aborts, never
@@ -31,7 +31,8 @@
  *  - Device-array CONTENTS are preconditions that the hot path does not
  *    check: split dims in [0, D) (kernels clamp them for memory safety only),
  *    indices in [0, 16), scales exact normal fp32 powers of two with
- *    127 * sum_c 2^(e_c - e_min) < 2^31.  Violations give unspecified values,
+ *    128 * sum_c 2^(e_c - e_min) <= 2^31 (so that no sum of int8 codes,
+ *    -128 included, leaves int32).  Violations give unspecified values,
  *    never out-of-bounds accesses.
  *  - Output arrays must not overlap each other or any input array of the same
  *    call (kernels may read inputs, indices in particular, through the scalar
@@ -54,7 +55,7 @@ enum {
     MADDNESS_EINVAL = 1,       /* bad size, NULL or misaligned pointer      */
     MADDNESS_EHIP = 2,         /* a HIP runtime call or a launch failed     */
     MADDNESS_EUNSUPPORTED = 3, /* shape beyond what the kernels handle      */
-    MADDNESS_ENOMEM = 4        /* temporary index buffer could not be made  */
+    MADDNESS_ENOMEM = 4        /* reserved: no entry point allocates         */
 };
 
 /* Layer output sigma for maddness_matmul_act[_f32] (§2.2: the bias term
@@ -64,6 +65,14 @@ enum {
     MADDNESS_ACT_BIAS = 1,     /* z = y + bias[m]                            */
     MADDNESS_ACT_RELU = 2,     /* z > 0 ? z : +0                             */
     MADDNESS_ACT_SOFTMAX = 3   /* softmax of z over the M outputs of a row   */
+};
+
+/* Objectives of the gradient-descent table fit, maddness_fit_lut_gd (§2.2,
+   Eq. 3 with a nonlinear layer output; the bias is added first). */
+enum {
+    MADDNESS_FIT_RELU_SQERR = 2,     /* ReLU, squared error                       */
+    MADDNESS_FIT_SOFTMAX_KLD = 3,    /* row softmax, KL divergence (as in §3.1)   */
+    MADDNESS_FIT_SOFTMAX_SQERR = 4   /* row softmax, squared error (Eq. 3)        */
 };
 
 #define MADDNESS_K 16          /* prototypes per codebook (4-bit indices)   */
@@ -113,8 +122,12 @@ int maddness_encode(const float* A, int64_t N, int32_t D, int64_t lda,
  *   acc_out [N][M] int32 or NULL:  acc = sum_c q[c][idx[n][c]][m] << (e_c - e_min),
  *           exact (no overflow under the precondition above).
  *   y_out   [N][M] fp32 or NULL (not both NULL):
- *           y = fmaf((float)acc, 2^e_min, bias32), a single rounding, where
+ *           y = fmaf((float)acc, 2^e_min, bias32), where
  *           bias32 = (float)(sum_c offset[c] accumulated in double, c = 0..C-1).
+ *           (float)acc is exact while |acc| <= 2^24, which tables from
+ *           maddness_build_lut always satisfy, and y is then the single
+ *           rounding of acc 2^e_min + bias32; a larger |acc| (possible only
+ *           with other tables) is rounded to fp32 before the fma.
  *
  * EINVAL: a NULL required array, both outputs NULL, N < 0, C <= 0, M <= 0,
  * misaligned scale/offset/acc_out/y_out.  EUNSUPPORTED: C > 512.
@@ -159,11 +172,12 @@ int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C,
 /*
  * Fused encode + lookup-accumulate: the whole inference path for one layer
  * (§1).  Same arguments and results as maddness_encode followed by
- * maddness_lut_accumulate; y_out is required, acc_out and idx_out are
- * optional extra outputs.  When the table [C][16][M] fits in LDS the indices
- * never leave the chip; otherwise the rows are encoded into idx_out (or a
- * stream-ordered temporary buffer, ENOMEM if it cannot be made) and
- * accumulated in column tiles.
+ * maddness_lut_accumulate; y_out is required, acc_out is an optional extra
+ * output.  When the table [C][16][M] fits the single-launch kernels the
+ * indices never leave the chip and idx_out is optional (written when given).
+ * Otherwise the rows are encoded into idx_out and then accumulated, and
+ * idx_out is required: EINVAL when it is NULL.  maddness_matmul_index_bytes
+ * tells which case a call is.
  */
 int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda,
                     const int32_t* split_dims, const float* thresholds,
@@ -171,7 +185,8 @@ int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda,
                     const float* offset, int32_t M, float* y_out,
                     int32_t* acc_out, uint8_t* idx_out, void* stream);
 
-/* Fused encode + fp32-table accumulate (unquantized mode); see above. */
+/* Fused encode + fp32-table accumulate (unquantized mode); see above,
+   idx_out included. */
 int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda,
                         const int32_t* split_dims, const float* thresholds,
                         int32_t C, const float* lut, int32_t M, float* y_out,
@@ -190,9 +205,9 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda,
  *                         fp32 (expf, any summation order): each entry is
  *                         within (|z - max| + M + 5) * 2^-24 relative of the
  *                         exact value (plus underflow below 2^-126).
- * col_bias [M] fp32, 4-byte aligned.  idx_out [N][C] (nullable) receives the
- * indices as for maddness_matmul.  EINVAL: act outside 0..3, plus the
- * conditions of maddness_matmul; ENOMEM as for maddness_matmul.
+ * col_bias [M] fp32, 4-byte aligned.  idx_out [N][C] receives the indices;
+ * it is optional or required as for maddness_matmul.  EINVAL: act outside
+ * 0..3, plus the conditions of maddness_matmul.
  */
 int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda,
                         const int32_t* split_dims, const float* thresholds,
@@ -207,6 +222,19 @@ int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda,
                             int32_t C, const float* lut, int32_t M,
                             const float* col_bias, int32_t act, float* y_out,
                             uint8_t* idx_out, void* stream);
+
+/*
+ * Device bytes the fused entry points need in idx_out for this call: 0 when
+ * the table fits their single-launch kernels (idx_out optional), N * C when
+ * the indices go through memory (idx_out required).  The answer depends on
+ * the shape, on whether the table is fp32 (f32 != 0), on act (the layer
+ * output of maddness_matmul_act[_f32]; 0 for maddness_matmul[_f32]) and on
+ * the alignment of A, so pass the A of the call.  Returns -1 for arguments
+ * the entry points reject with EINVAL, -3 for shapes they reject with
+ * EUNSUPPORTED.  Makes no HIP call.
+ */
+int64_t maddness_matmul_index_bytes(const float* A, int64_t N, int32_t D, int64_t lda, int32_t C,
+                                    int32_t M, int32_t f32, int32_t act);
 
 /*
  * Offline table construction (§2.2: T = P B) followed by 8-bit block
@@ -282,11 +310,15 @@ int maddness_fit_lut_ridge(const uint8_t* idx, int64_t N, int32_t C,
  * Model-aware table fit (§2.2, Eq. 3) with a nonlinear layer output, by
  * full-batch gradient descent from T = T0 (the paper names the objectives,
  * not an optimiser; eta and iters are the caller's).  With
- * z_n = (sum_c T[c][idx[n][c]][.], c ascending, double) + col_bias:
- *   act = MADDNESS_ACT_RELU:    objective sum_n ||relu(Y[n] + b) - relu(z_n)||^2,
- *                               residual 2 (relu(z) - relu(y + b)) [z > 0];
- *   act = MADDNESS_ACT_SOFTMAX: objective sum_n KL(softmax(Y[n] + b) || softmax(z_n)),
- *                               residual softmax(z) - softmax(y + b);
+ * z_n = (sum_c T[c][idx[n][c]][.], c ascending, double) + col_bias and `act`
+ * one of the MADDNESS_FIT_* objectives:
+ *   RELU_SQERR:    objective sum_n ||relu(Y[n] + b) - relu(z_n)||^2,
+ *                  residual 2 (relu(z) - relu(y + b)) [z > 0];
+ *   SOFTMAX_KLD:   objective sum_n KL(softmax(Y[n] + b) || softmax(z_n)),
+ *                  residual softmax(z) - softmax(y + b);
+ *   SOFTMAX_SQERR: objective sum_n ||softmax(z_n) - softmax(Y[n] + b)||^2,
+ *                  residual 2 p (d - s) with p = softmax(z),
+ *                  d = p - softmax(y + b), s = sum_m d_m p_m;
  * each plus lambda ||T - T0||^2.  A step: R = G^T residual (rows ascending),
  * g = R + 2 lambda (T - T0), T = T - eta g, all in double.  ReLU steps are
  * exactly reproducible; softmax steps differ from another implementation only

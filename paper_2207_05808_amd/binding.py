@@ -80,8 +80,8 @@ def _validate_scales(scale: torch.Tensor):
     if not (np.all(m == 0.5) and np.all(e - 1 >= -126)):
         raise ValueError("scales must be exact normal powers of two")
     sh = (e - 1) - (e - 1).min()
-    if np.any(sh > 30) or float(np.sum(127.0 * np.ldexp(1.0, sh))) >= 2.0 ** 31:
-        raise ValueError("scale exponents too far apart: the int32 sum could overflow")
+    if np.any(sh > 30) or float(np.sum(128.0 * np.ldexp(1.0, sh))) > 2.0 ** 31:
+        raise ValueError("scale exponents too far apart: a sum of int8 codes could leave int32")
 
 
 def _validate_idx(idx: torch.Tensor):
@@ -203,9 +203,10 @@ def matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, acc_out=No
     if idx_out is None and want_idx:
         idx_out = torch.empty((N, C), dtype=torch.uint8, device=dev)
     idx_out = _idx_out(idx_out, N, C)
+    idx_arg = _index_array(idx_out, A, N, D, lda, C, M, False, 0, stream)
     st = _lib.lib().maddness_matmul(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
                                     _ptr(lut), _ptr(scale), _ptr(offset), M, _ptr(y_out),
-                                    _ptr(acc_out), _ptr(idx_out), _stream(stream))
+                                    _ptr(acc_out), _ptr(idx_arg), _stream(stream))
     _lib.check("maddness_matmul", st)
     return y_out, acc_out, idx_out
 
@@ -227,13 +228,16 @@ def matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None, want_id
     if idx_out is None and want_idx:
         idx_out = torch.empty((N, C), dtype=torch.uint8, device=A.device)
     idx_out = _idx_out(idx_out, N, C)
+    idx_arg = _index_array(idx_out, A, N, D, lda, C, M, True, 0, stream)
     st = _lib.lib().maddness_matmul_f32(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
-                                        _ptr(lut), M, _ptr(y_out), _ptr(idx_out), _stream(stream))
+                                        _ptr(lut), M, _ptr(y_out), _ptr(idx_arg), _stream(stream))
     _lib.check("maddness_matmul_f32", st)
     return y_out, idx_out
 
 
 ACT = {"none": 0, "bias": 1, "relu": 2, "softmax": 3}
+# objectives of fit_lut_gd (MADDNESS_FIT_*): the layer output and the loss
+FIT = {"relu": 2, "softmax": 3, "softmax_kld": 3, "softmax_sqerr": 4}
 
 
 def _act(act):
@@ -263,11 +267,39 @@ def _idx_out(idx_out, N, C):
     return idx_out
 
 
+def matmul_index_bytes(A, C, M, f32=False, act=0) -> int:
+    """Device bytes the fused entry points need in idx_out for this A and
+    shape (maddness_matmul_index_bytes): 0 when the call runs as one launch,
+    else N * C."""
+    N, D, lda = _rows(A)
+    n = int(_lib.lib().maddness_matmul_index_bytes(_ptr(A), N, D, lda, C, M, 1 if f32 else 0, _act(act)))
+    if n < 0:
+        _lib.check("maddness_matmul_index_bytes", _lib.EINVAL if n == -1 else _lib.EUNSUPPORTED)
+    return n
+
+
+def _index_array(idx_out, A, N, D, lda, C, M, f32, act, stream):
+    """idx_out when the caller gave one; else, when the call needs an index
+    array (the table does not fit the single-launch kernels), a new one from
+    torch's allocator, kept alive for `stream`; else None.  The library
+    itself never allocates."""
+    if idx_out is not None:
+        return idx_out
+    n = int(_lib.lib().maddness_matmul_index_bytes(_ptr(A), N, D, lda, C, M, 1 if f32 else 0, int(act)))
+    if n <= 0:
+        return None   # one launch, or arguments the call itself rejects
+    t = torch.empty((N, C), dtype=torch.uint8, device=A.device)
+    if stream is not None:
+        t.record_stream(stream)
+    return t
+
+
 def matmul_act(A, split_dims, thresholds, lut, scale, offset, col_bias=None, act="relu", y_out=None,
                idx_out=None, stream=None, validate=False):
     """Fused encode + lookup-accumulate + layer output sigma (bias, then
     "relu" / "softmax"; "bias" or "none" also accepted); returns y.  With
-    idx_out the indices are written there (and nothing is allocated)."""
+    idx_out the indices are written there; without it an index array is
+    allocated here when the shape needs one (matmul_index_bytes)."""
     N, D, lda = _rows(A)
     C = _tree_args(split_dims, thresholds)
     C2, M = _lut_i8(lut, scale, offset)
@@ -282,9 +314,10 @@ def matmul_act(A, split_dims, thresholds, lut, scale, offset, col_bias=None, act
     _need(y_out, "y_out", torch.float32, 2)
     _dense(y_out, "y_out")
     idx_out = _idx_out(idx_out, N, C)
+    idx_arg = _index_array(idx_out, A, N, D, lda, C, M, False, _act(act), stream)
     st = _lib.lib().maddness_matmul_act(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut),
                                         _ptr(scale), _ptr(offset), M, _ptr(col_bias), _act(act), _ptr(y_out),
-                                        _ptr(idx_out), _stream(stream))
+                                        _ptr(idx_arg), _stream(stream))
     _lib.check("maddness_matmul_act", st)
     return y_out
 
@@ -307,9 +340,10 @@ def matmul_act_f32(A, split_dims, thresholds, lut, col_bias=None, act="relu", y_
     _need(y_out, "y_out", torch.float32, 2)
     _dense(y_out, "y_out")
     idx_out = _idx_out(idx_out, N, C)
+    idx_arg = _index_array(idx_out, A, N, D, lda, C, M, True, _act(act), stream)
     st = _lib.lib().maddness_matmul_act_f32(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
                                             _ptr(lut), M, _ptr(col_bias), _act(act), _ptr(y_out),
-                                            _ptr(idx_out), _stream(stream))
+                                            _ptr(idx_arg), _stream(stream))
     _lib.check("maddness_matmul_act_f32", st)
     return y_out
 
@@ -412,9 +446,11 @@ def prepare_matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None,
         y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
     _need(y_out, "y_out", torch.float32, 2)
     _dense(y_out, "y_out")
+    idx_out = _idx_out(idx_out, N, C)
+    idx_arg = _index_array(idx_out, A, N, D, lda, C, M, True, 0, stream)
     args = (_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut), M, _ptr(y_out),
-            _ptr(idx_out), _stream(stream))
-    keep = (A, split_dims, thresholds, lut, y_out, idx_out)
+            _ptr(idx_arg), _stream(stream))
+    keep = (A, split_dims, thresholds, lut, y_out, idx_arg)
     return PreparedCall("maddness_matmul_f32", args, keep, (y_out, idx_out))
 
 
@@ -433,9 +469,11 @@ def prepare_matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, ac
         y_out = torch.empty((N, M), dtype=torch.float32, device=A.device)
     _need(y_out, "y_out", torch.float32, 2)
     _dense(y_out, "y_out")
+    idx_out = _idx_out(idx_out, N, C)
+    idx_arg = _index_array(idx_out, A, N, D, lda, C, M, False, 0, stream)
     args = (_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C, _ptr(lut), _ptr(scale),
-            _ptr(offset), M, _ptr(y_out), _ptr(acc_out), _ptr(idx_out), _stream(stream))
-    keep = (A, split_dims, thresholds, lut, scale, offset, y_out, acc_out, idx_out)
+            _ptr(offset), M, _ptr(y_out), _ptr(acc_out), _ptr(idx_arg), _stream(stream))
+    keep = (A, split_dims, thresholds, lut, scale, offset, y_out, acc_out, idx_arg)
     return PreparedCall("maddness_matmul", args, keep, (y_out, acc_out, idx_out))
 
 
@@ -534,14 +572,17 @@ def fit_lut_workspace_bytes(N: int, C: int) -> int:
 
 def fit_lut_gd(idx, Y, T0, act, lam, eta, iters, col_bias=None, workspace=None, stream=None):
     """Model-aware table fit (Eq. 3) with a nonlinear output by gradient
-    descent from T0: act "relu" (squared error after bias + ReLU) or
-    "softmax" (KL divergence between row softmaxes); float64 [C,16,M]."""
+    descent from T0: act "relu" (squared error after bias + ReLU),
+    "softmax" / "softmax_kld" (KL divergence between row softmaxes) or
+    "softmax_sqerr" (squared error between row softmaxes); float64 [C,16,M]."""
     N, C, M = _fit_inputs(idx, Y)
     _need(T0, "T0", torch.float32, 3)
     _dense(T0, "T0")
     if tuple(T0.shape) != (C, K, M):
         raise ValueError("T0 must be [C,16,M]")
-    code = ACT[act] if isinstance(act, str) else int(act)
+    if isinstance(act, str) and act not in FIT:
+        raise ValueError(f"act must be one of {sorted(FIT)}")
+    code = FIT[act] if isinstance(act, str) else int(act)
     if col_bias is not None:
         _need(col_bias, "col_bias", torch.float32, 1)
         _dense(col_bias, "col_bias")

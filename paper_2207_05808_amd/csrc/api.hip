@@ -446,29 +446,44 @@ Shape shape(int mode, int elem) {
   return s;
 }
 
-// Two-phase path for tables larger than one LDS tile: encode, then tiled accumulate.
-int two_phase(Shape s, uint8_t* idx_user, hipStream_t stream) {
-  uint8_t* idx = idx_user;
-  bool temp = false;
-  if (!idx) {
-    if (hipMallocAsync(reinterpret_cast<void**>(&idx), (size_t)s.N * (size_t)s.C, stream) != hipSuccess ||
-        !idx)
-      return MADDNESS_ENOMEM;
-    temp = true;
-  }
+// Two-phase path for tables larger than the single-launch kernels take:
+// encode into the caller's index array, then accumulate from it.
+int two_phase(const Shape& s, uint8_t* idx, hipStream_t stream) {
   Shape e = s;
   e.mode = kEncode;
   e.idx_out = idx;
   int rc = run(e, false, stream);
-  if (rc == MADDNESS_OK) {
-    Shape q = s;
-    q.mode = kAccum;
-    q.idx_in = idx;
-    q.idx_out = nullptr;
-    rc = accumulate(q, stream);
-  }
-  if (temp && hipFreeAsync(idx, stream) != hipSuccess && rc == MADDNESS_OK) rc = MADDNESS_EHIP;
-  return rc;
+  if (rc != MADDNESS_OK) return rc;
+  Shape q = s;
+  q.mode = kAccum;
+  q.idx_in = idx;
+  q.idx_out = nullptr;
+  return accumulate(q, stream);
+}
+
+// Whether a fused call runs as one launch (the gather-fused kernel, or the
+// general kernel with the whole table in one column tile; the latter has no
+// layer-output epilogue).
+bool single_launch(const Shape& s) {
+  GArgs g;
+  int ng, uq, nw;
+  if (plan_gfused(s, &g, &ng, &uq, &nw)) return true;
+  Plan p;
+  return s.act == 0 && plan(s, &p, true) == MADDNESS_OK;
+}
+
+// Every fused entry point: one launch when the shape allows it, else the
+// two-phase path through the caller's index array (required there).
+int fused(const Shape& s, hipStream_t st) {
+  GArgs g;
+  int ng, uq, nw;
+  if (plan_gfused(s, &g, &ng, &uq, &nw))
+    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
+  Plan p;
+  if (s.act == 0 && plan(s, &p, true) == MADDNESS_OK)
+    return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, st));
+  if (!s.idx_out) return MADDNESS_EINVAL;
+  return two_phase(s, s.idx_out, st);
 }
 
 }  // namespace
@@ -486,7 +501,7 @@ const char* maddness_status_string(int status) {
     case MADDNESS_EINVAL: return "invalid argument";
     case MADDNESS_EHIP: return "HIP runtime error";
     case MADDNESS_EUNSUPPORTED: return "unsupported shape";
-    case MADDNESS_ENOMEM: return "out of device memory";
+    case MADDNESS_ENOMEM: return "out of device memory (reserved)";
     default: return "unknown status";
   }
 }
@@ -560,14 +575,7 @@ int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda, const int
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out; s.acc = acc_out;
   s.idx_out = idx_out;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  GArgs g;
-  int ng, uq, nw;
-  if (plan_gfused(s, &g, &ng, &uq, &nw))
-    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
-  Plan p;
-  if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
-  return two_phase(s, idx_out, st);
+  return fused(s, static_cast<hipStream_t>(stream));
 }
 
 int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
@@ -581,14 +589,7 @@ int maddness_matmul_f32(const float* A, int64_t N, int32_t D, int64_t lda, const
   Shape s = shape(kFused, kF32);
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.M = M; s.y = y_out; s.idx_out = idx_out;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  GArgs g;
-  int ng, uq, nw;
-  if (plan_gfused(s, &g, &ng, &uq, &nw))
-    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
-  Plan p;
-  if (plan(s, &p, true) == MADDNESS_OK) return run(s, true, st);
-  return two_phase(s, idx_out, st);
+  return fused(s, static_cast<hipStream_t>(stream));
 }
 
 int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
@@ -607,12 +608,7 @@ int maddness_matmul_act(const float* A, int64_t N, int32_t D, int64_t lda, const
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out;
   s.col_bias = col_bias; s.act = act; s.idx_out = idx_out;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  GArgs g;
-  int ng, uq, nw;
-  if (plan_gfused(s, &g, &ng, &uq, &nw))
-    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
-  return two_phase(s, idx_out, st);
+  return fused(s, static_cast<hipStream_t>(stream));
 }
 
 int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
@@ -629,12 +625,19 @@ int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda, c
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
   s.lut = lut; s.M = M; s.y = y_out;
   s.col_bias = col_bias; s.act = act; s.idx_out = idx_out;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  GArgs g;
-  int ng, uq, nw;
-  if (plan_gfused(s, &g, &ng, &uq, &nw))
-    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
-  return two_phase(s, idx_out, st);
+  return fused(s, static_cast<hipStream_t>(stream));
+}
+
+int64_t maddness_matmul_index_bytes(const float* A, int64_t N, int32_t D, int64_t lda, int32_t C, int32_t M,
+                                    int32_t f32, int32_t act) {
+  if (N < 0 || D <= 0 || C <= 0 || M <= 0 || lda < D) return -1;
+  if (act < MADDNESS_ACT_NONE || act > MADDNESS_ACT_SOFTMAX) return -1;
+  if (C > kMaxC) return -3;
+  if (N == 0) return 0;
+  if (!A || !aligned(A, 4)) return -1;
+  Shape s = shape(kFused, f32 ? kF32 : kI8);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.C = C; s.M = M; s.act = act;
+  return single_launch(s) ? 0 : N * (int64_t)C;
 }
 
 int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D, int32_t M, int8_t* lut_out,
@@ -738,7 +741,8 @@ int maddness_fit_lut_gd(const uint8_t* idx, int64_t N, int32_t C, const float* Y
                         void* workspace, int64_t workspace_bytes, void* stream) {
   if (N < 0 || C <= 0 || M <= 0 || !T0 || !T_out || !workspace || (N > 0 && (!idx || !Y)))
     return MADDNESS_EINVAL;
-  if (act != MADDNESS_ACT_RELU && act != MADDNESS_ACT_SOFTMAX) return MADDNESS_EINVAL;
+  if (act != MADDNESS_FIT_RELU_SQERR && act != MADDNESS_FIT_SOFTMAX_KLD && act != MADDNESS_FIT_SOFTMAX_SQERR)
+    return MADDNESS_EINVAL;
   if (!(lambda >= 0.0) || !std::isfinite(lambda) || !(eta > 0.0) || !std::isfinite(eta) || iters < 0)
     return MADDNESS_EINVAL;
   if (!aligned(T_out, 8) || !aligned(T0, 4) || !aligned(workspace, 256) || (N > 0 && !aligned(Y, 4)) ||

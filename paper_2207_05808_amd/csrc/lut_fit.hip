@@ -411,7 +411,7 @@ __device__ void softmax_row_inplace(double* __restrict__ out, int M, int lane) {
   for (int m = lane; m < M; m += 64) out[m] = __ddiv_rn(out[m], sum);
 }
 
-// P = sigma(Y + b): ReLU (act 2) or row softmax (act 3), in double
+// P = sigma(Y + b): ReLU (act 2) or row softmax (acts 3 and 4), in double
 __global__ void __launch_bounds__(256)
 target_kernel(const float* __restrict__ Y, int64_t N, int M, const float* __restrict__ bias, int act,
               double* __restrict__ P) {
@@ -422,11 +422,14 @@ target_kernel(const float* __restrict__ Y, int64_t N, int M, const float* __rest
       const double z = __dadd_rn((double)Y[n * M + m], bias ? (double)bias[m] : 0.0);
       pr[m] = (act == 2) ? (z > 0.0 ? z : 0.0) : z;
     }
-    if (act == 3) softmax_row_inplace(pr, M, lane);
+    if (act >= 3) softmax_row_inplace(pr, M, lane);
   }
 }
 
-// D = dObjective / dz per row: ReLU 2 (relu(z) - P) [z > 0]; softmax softmax(z) - P
+// D = dObjective / dz per row: ReLU 2 (relu(z) - P) [z > 0]; softmax with the
+// KL divergence softmax(z) - P; softmax with the squared error 2 p (d - s),
+// p = softmax(z), d = p - P, s = sum_m d_m p_m (the softmax Jacobian
+// diag(p) - p p^T applied to 2 d).
 __global__ void __launch_bounds__(256)
 resid_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, const double* __restrict__ T, int M,
              const float* __restrict__ bias, int act, const double* __restrict__ P, double* __restrict__ D) {
@@ -444,6 +447,15 @@ resid_kernel(const uint8_t* __restrict__ idx, int64_t N, int C, const double* __
     if (act == 3) {
       softmax_row_inplace(dr, M, lane);
       for (int m = lane; m < M; m += 64) dr[m] = __dsub_rn(dr[m], pr[m]);
+    } else if (act == 4) {
+      softmax_row_inplace(dr, M, lane);
+      double s = 0.0;
+      for (int m = lane; m < M; m += 64) s = __dadd_rn(s, __dmul_rn(__dsub_rn(dr[m], pr[m]), dr[m]));
+      s = wave_sum(s);
+      for (int m = lane; m < M; m += 64) {
+        const double p = dr[m];
+        dr[m] = __dmul_rn(2.0, __dmul_rn(p, __dsub_rn(__dsub_rn(p, pr[m]), s)));
+      }
     }
   }
 }

@@ -87,6 +87,56 @@ def test_matmul_rejects(L):
     assert F(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 10, NULL, NULL, NULL) == 1
 
 
+def test_matmul_index_bytes(L):
+    """The fused entry points need a caller index array exactly when their
+    single-launch kernels cannot take the table: 0 for the im2col conv layer
+    (C = 32, M = 64) and the tiny classifier, N * C for the dense hidden
+    layer, the wide layer and the fp32 search-tree layer."""
+    Q = L.maddness_matmul_index_bytes
+    assert Q(FAKE, 131072, 576, 576, 32, 64, 0, 0) == 0
+    assert Q(FAKE, 131072, 576, 576, 32, 64, 0, 3) == 0
+    assert Q(FAKE, 1024, 64, 64, 4, 10, 0, 3) == 0
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 0) == (1 << 20) * 64
+    assert Q(FAKE, 262144, 1024, 1024, 128, 4096, 0, 2) == 262144 * 128
+    assert Q(FAKE, 524288, 256, 256, 256, 1024, 1, 0) == 524288 * 256
+    assert Q(NULL, 0, 512, 512, 64, 512, 0, 0) == 0          # N == 0: nothing to do
+    assert Q(FAKE, -1, 64, 64, 4, 10, 0, 0) == -1
+    assert Q(FAKE, 10, 64, 63, 4, 10, 0, 0) == -1             # lda < D
+    assert Q(FAKE, 10, 64, 64, 4, 10, 0, 4) == -1             # act outside 0..3
+    assert Q(ctypes.c_void_p(0x1002), 10, 64, 64, 4, 10, 0, 0) == -1   # misaligned A
+    assert Q(FAKE, 10, 64, 64, 600, 10, 0, 0) == -3           # too many codebooks
+
+
+def test_fused_two_phase_needs_index_array(L):
+    """Without idx_out a call whose table does not fit the single-launch
+    kernels is rejected (EINVAL) before any HIP call: the library never
+    allocates."""
+    big = [FAKE, 4096, 512, 512, FAKE, FAKE, 64, FAKE, FAKE, FAKE, 512, FAKE, NULL, NULL, NULL]
+    assert L.maddness_matmul(*big) == 1
+    assert L.maddness_matmul_f32(FAKE, 4096, 256, 256, FAKE, FAKE, 256, FAKE, 1024, FAKE, NULL, NULL) == 1
+    assert L.maddness_matmul_act(FAKE, 4096, 512, 512, FAKE, FAKE, 64, FAKE, FAKE, FAKE, 512, NULL, 2, FAKE,
+                                 NULL, NULL) == 1
+    assert L.maddness_matmul_act_f32(FAKE, 4096, 256, 256, FAKE, FAKE, 256, FAKE, 1024, NULL, 3, FAKE,
+                                     NULL, NULL) == 1
+
+
+def test_library_imports_no_allocator():
+    """No device (or host-pinned) allocation routine is referenced by the
+    library: every buffer beyond the inputs and outputs is the caller's."""
+    import shutil
+    import subprocess
+    from paper_2207_05808_amd import _lib
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--undefined-only", _lib.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    syms = [l.split()[-1].split("@")[0] for l in out.splitlines() if l.strip()]
+    alloc = [s for s in syms if re.match(r"hip(Ext)?(Malloc|Free|HostMalloc|HostAlloc|MallocManaged|"
+                                         r"MallocAsync|FreeAsync|MallocFromPool|MemPool|HostRegister)", s)]
+    assert not alloc, f"allocation routines referenced: {alloc}"
+
+
 def test_matmul_act_rejects(L):
     Ma = L.maddness_matmul_act
     args = [FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, NULL, 2, FAKE, NULL, NULL]
@@ -167,6 +217,8 @@ def test_fit_gd_rejects(L):
     assert ws > 0
     G = L.maddness_fit_lut_gd
     assert G(FAKE, 10, 4, FAKE, 5, NULL, 1, FAKE, 0.1, 0.01, 3, FAKE, FAKE, ws, NULL) == 1   # act 1
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 5, FAKE, 0.1, 0.01, 3, FAKE, FAKE, ws, NULL) == 1   # objective 5
+    assert G(FAKE, 10, 4, FAKE, 5, NULL, 4, FAKE, -0.1, 0.01, 3, FAKE, FAKE, ws, NULL) == 1  # objective 4, lambda < 0
     assert G(FAKE, 10, 4, FAKE, 5, NULL, 3, FAKE, -0.1, 0.01, 3, FAKE, FAKE, ws, NULL) == 1  # lambda < 0
     assert G(FAKE, 10, 4, FAKE, 5, NULL, 3, FAKE, 0.1, 0.0, 3, FAKE, FAKE, ws, NULL) == 1    # eta = 0
     assert G(FAKE, 10, 4, FAKE, 5, NULL, 2, FAKE, 0.1, 0.01, -1, FAKE, FAKE, ws, NULL) == 1  # iters < 0

@@ -178,12 +178,81 @@ def test_fit_gd_softmax_matches_oracle(orc, N, C, M, lam, frac, iters, with_bias
     assert err <= tol, f"max |diff| {err:.3g} > bound {tol:.3g}"
 
 
+def softmax_sqerr_tolerance(idx, C, M, eta, iters, tmax, lip):
+    """Bound on max |T_gpu - T_oracle| after K steps of the squared error
+    between row softmaxes.  Per side, against the exact step from the same
+    T: with each probability within e = (2M + 4) u relative (as above), the
+    difference d = p - p* errs by (e + u)(p + p*), the weighted sum
+    s = sum d p by 4 e + (2M + 4) u, and the residual r = 2 p (d - s) by
+    2 (10 e + (2M + 14) u) <= (44 M + 108) u; |r| <= 6, so a gradient entry
+    over its Nb rows errs by Nb (44 M + 108) u + 6 Nb^2 u and the update by
+    4 u |T|.  This objective is not convex, so the exact step is not
+    non-expansive: with its gradient L-Lipschitz (L = lip) the step map is
+    (1 + eta L)-Lipschitz, and the two sides drift apart by at most
+    K (1 + eta L)^(K - 1) times both sides' per-step errors (2-norm over the
+    16 C M entries)."""
+    u = 2.0 ** -53
+    Nb = max(int(np.bincount(idx[:, c], minlength=16).max()) for c in range(C))
+    step = (eta * (Nb * (44 * M + 108) + 6 * Nb * Nb) + 4 * tmax) * u * np.sqrt(16 * C * M)
+    return 2 * iters * (1 + eta * lip) ** max(iters - 1, 0) * step
+
+
+def lipschitz_sqerr(orc, idx, lam):
+    """The Hessian of ||softmax(z) - p*||^2 in z has norm <= 10.5 (2 J^T J
+    with ||J|| <= 1/2, plus sum_i d_i Hess(p_i) with ||Hess(p_i)|| <= 2.5 p_i
+    and sum_i |d_i| p_i <= 2), so L = 10.5 lambda_max(G^T G) + 2 lambda."""
+    H = orc.encoder_gram(idx).astype(np.float64)
+    return 10.5 * float(np.linalg.eigvalsh(H)[-1]) + 2.0 * lam
+
+
+@pytest.mark.parametrize("N,C,M,lam,frac,iters,with_bias", GD_CASES)
+def test_fit_gd_softmax_sqerr_matches_oracle(orc, N, C, M, lam, frac, iters, with_bias):
+    """Eq. 3 as written for a softmax output: the squared error between the
+    row softmaxes of the table's outputs and the targets."""
+    idx, Y, T0 = problem(N, C, M, seed=N + 3 * C + M)
+    bias = np.random.default_rng(N + 2).standard_normal(M).astype(np.float32) if with_bias else None
+    lip = lipschitz_sqerr(orc, idx, lam)
+    eta = min(frac, 1.0) / lip
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "softmax_sqerr", lam, eta, iters,
+                            col_bias=dev(bias) if with_bias else None))
+    ref = orc.fit_lut_gd(idx, Y, T0, 4, lam, eta, iters, bias)
+    tol = softmax_sqerr_tolerance(idx, C, M, eta, iters, float(np.abs(ref).max()), lip)
+    err = float(np.abs(T - ref).max())
+    assert err <= tol, f"max |diff| {err:.3g} > bound {tol:.3g}"
+    assert np.abs(T - T0).max() > 100 * tol   # the steps moved the table well past the bound
+
+
+def test_fit_gd_softmax_sqerr_classifier(orc):
+    """The classifier workload (C = 4, M = 10) under Eq. 3's squared error
+    between softmaxes: the GPU fit matches the oracle within the bound and
+    lowers that objective below the prototype table's."""
+    p = W.make("classifier_tiny")
+    idx = orc.encode(p.A[:512], p.split, p.thr)
+    Y = (p.A[:512].astype(np.float64) @ p.B.astype(np.float64)).astype(np.float32)
+    T0 = orc.build_lut_f32(p.P, p.B)
+    lam, iters = 0.1, 40
+    lip = lipschitz_sqerr(orc, idx, lam)
+    eta = 1.0 / lip
+    T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "softmax_sqerr", lam, eta, iters))
+    ref = orc.fit_lut_gd(idx, Y, T0, 4, lam, eta, iters)
+    assert np.abs(T - ref).max() <= softmax_sqerr_tolerance(idx, 4, 10, eta, iters, float(np.abs(ref).max()), lip)
+    from scipy.special import softmax
+
+    def sqerr(Tx):
+        z = sum(np.asarray(Tx, np.float64)[c][idx[:, c]] for c in range(4))
+        d = softmax(z, axis=1) - softmax(Y.astype(np.float64), axis=1)
+        return float((d * d).sum())
+
+    assert sqerr(T) < sqerr(T0)
+
+
 def test_fit_gd_zero_steps_and_rejects(orc):
     idx, Y, T0 = problem(100, 3, 7, seed=9)
     T = host(mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), "softmax", 0.1, 0.01, 0))
     assert np.array_equal(T, T0.astype(np.float64))
-    for act, lam, eta, iters in (("bias", 0.1, 0.01, 2), ("relu", -1.0, 0.01, 2), ("relu", 0.1, 0.0, 2),
-                                 ("softmax", 0.1, 0.01, -1)):
+    for act, lam, eta, iters in (("relu", -1.0, 0.01, 2), ("relu", 0.1, 0.0, 2),
+                                 ("softmax", 0.1, 0.01, -1), ("softmax_sqerr", -0.5, 0.01, 2), (1, 0.1, 0.01, 2),
+                                 (5, 0.1, 0.01, 2)):
         with pytest.raises(mdn.MaddnessError):
             mdn.fit_lut_gd(dev(idx), dev(Y), dev(T0), act, lam, eta, iters)
 

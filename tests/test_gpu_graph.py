@@ -3,8 +3,9 @@ call enqueues kernels only, so a serving loop can capture it once and replay
 it.  Every case is captured after one eager call, then replayed several
 times with eager work, new input contents and synchronisations between the
 replays; every replay is checked against the oracle for the inputs it saw.
-The two-phase matmul gets a caller-provided index buffer (without one it
-allocates, which a capture must not contain)."""
+The library never allocates: the two-phase matmul writes its indices to a
+caller index array, which the Python binding takes from torch's allocator
+(the graph's private pool under capture) when the caller passes none."""
 import numpy as np
 import pytest
 import torch
@@ -154,3 +155,39 @@ def test_two_phase_row_kernels_replay(orc, name, N):
         assert np.array_equal(host(y), refs[i][1]), (i, rnd)
 
     replay_and_check(g, A, inputs, [y, idx], expected)
+
+
+@pytest.mark.parametrize("name,N", [("dense_hidden", 2000), ("dense_hidden", 16411), ("wide_layer", 3000),
+                                    ("encode_heavy_f32", 4173)])
+def test_two_phase_without_caller_index_array_replays(orc, name, N):
+    """The two-phase path captured with no index array from the caller: the
+    binding asks maddness_matmul_index_bytes, takes the array from torch's
+    allocator inside the capture, and the replays match the oracle."""
+    p = W.make(name, N=N)
+    rng = np.random.default_rng(N + 7)
+    inputs = [p.A, rng.standard_normal(p.A.shape).astype(np.float32)]
+    A = dev(inputs[0])
+    split, thr = dev(p.split), dev(p.thr)
+    y = torch.empty((N, p.spec.M), device=DEV)
+    f32 = not p.spec.quantized
+    assert mdn.matmul_index_bytes(A, p.spec.C, p.spec.M, f32=f32) == N * p.spec.C
+    if not f32:
+        lut, scale, offset = mdn.build_lut(dev(p.P), dev(p.B))
+        rl, rs, ro = orc.build_quantized_lut(p.P, p.B)
+        call = lambda: mdn.matmul(A, split, thr, lut, scale, offset, y_out=y)
+        refs = [orc.matmul(x, p.split, p.thr, rl, rs, ro)[2] for x in inputs]
+    else:
+        tab = mdn.build_lut_f32(dev(p.P), dev(p.B))
+        rtab = orc.build_lut_f32(p.P, p.B)
+        call = lambda: mdn.matmul_f32(A, split, thr, tab, y_out=y)
+        refs = [orc.matmul_f32(x, p.split, p.thr, rtab)[1] for x in inputs]
+    call()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+
+    def expected(i, rnd):
+        assert np.array_equal(host(y), refs[i]), (i, rnd)
+
+    replay_and_check(g, A, inputs, [y], expected)

@@ -37,8 +37,10 @@ def assert_y(y, ref):
 
 
 def max_shift_for(C):
+    """Largest shift s (at most 12) with 128 C 2^s <= 2^31: any codes of C
+    codebooks shifted by up to s keep the int32 sum exact."""
     s = 0
-    while 127.0 * C * 2.0 ** (s + 1) < 2.0 ** 31 and s < 12:
+    while 128.0 * C * 2.0 ** (s + 1) <= 2.0 ** 31 and s < 12:
         s += 1
     return s
 
@@ -153,6 +155,51 @@ def test_lut_accumulate_16bit_bound(orc, C, shifts, code):
     racc, ry = orc.lut_accumulate(idx, lut, scale, offset)
     assert np.array_equal(host(acc), racc)
     assert np.array_equal(host(y), ry)
+
+
+EDGE_SHIFTS = {
+    # C = 2: the gather-fused kernel with index loads, 32-bit sums
+    2: [23, 0],
+    # C = 25: the column-tiled kernel; sum 2^sh = 2^24, so -128 codes sum to -2^31
+    25: list(range(23, -1, -1)) + [0],
+    # C = 28: the row-uniform kernel's 32-bit sums; sum 2^sh = 2^24 again
+    28: list(range(23, 3, -1)) + [2, 1, 1, 1, 1, 1, 0, 0],
+}
+
+
+@pytest.mark.parametrize("C", sorted(EDGE_SHIFTS))
+@pytest.mark.parametrize("code", [-128, 127, None])
+def test_lut_accumulate_int32_edge(orc, C, code):
+    """Tables at the accumulator's precondition, 128 sum_c 2^sh <= 2^31: all
+    codes -128 (the sum reaches -2^31 for C = 25 and 28), all 127, or random
+    int8 codes; acc and y bit-identical to the oracle in each kernel."""
+    sh = np.array(EDGE_SHIFTS[C], np.int64)
+    assert 128 * int((2 ** sh).sum()) <= 2 ** 31
+    N, M = (16384 + 77, 512) if C == 28 else (3000, 64)
+    rng = np.random.default_rng(C * 3 + (0 if code is None else code + 200))
+    idx = W.random_indices(N, C, seed=C + 5)
+    if code is None:
+        lut = rng.integers(-128, 128, size=(C, 16, M)).astype(np.int8)
+    else:
+        lut = np.full((C, 16, M), code, np.int8)
+    scale = np.ldexp(np.float32(1.0), (sh - 30).astype(np.int32)).astype(np.float32)
+    offset = rng.standard_normal(C).astype(np.float32)
+    acc, y = mdn.lut_accumulate(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=True, validate=True)
+    racc, ry = orc.lut_accumulate(idx, lut, scale, offset)
+    if code == -128 and C != 2:
+        assert np.all(racc == np.int32(-2 ** 31))
+    assert np.array_equal(host(acc), racc)
+    assert np.array_equal(host(y), ry)
+
+
+def test_validator_rejects_past_int32_edge():
+    """Shifts (24, 0) pass 127 sum 2^sh < 2^31 but a -128 code would leave
+    int32: the binding's validator rejects them."""
+    idx = dev(np.zeros((4, 2), np.uint8))
+    lut = dev(np.zeros((2, 16, 8), np.int8))
+    scale = dev(np.array([2.0 ** 4, 2.0 ** -20], np.float32))
+    with pytest.raises(ValueError):
+        mdn.lut_accumulate(idx, lut, scale, dev(np.zeros(2, np.float32)), validate=True)
 
 
 @pytest.mark.parametrize("C,M", [(1, 1), (3, 10), (32, 64), (64, 512), (256, 1024), (7, 33), (200, 5)])
