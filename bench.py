@@ -10,10 +10,17 @@ shape as context.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 
-Other workloads (--workload) time the same step on their shapes; their tables
-are larger than LDS, so a step is an encode launch plus an accumulate launch
-(the row-uniform kernel for tables at least 512 int8 or 256 fp32 columns wide,
-the column-tiled one otherwise).
+The timed outputs are checked against the CPU oracle in the same run (every
+row of the headline workload), and the line's `context.workloads` block gives
+the other four workloads (classifier_tiny, dense_hidden, wide_layer,
+encode_heavy_f32) a compact measurement each: rows/s, step time, HBM
+fraction, the accumulate's LDS fraction and a parity check on sampled rows.
+
+Other workloads (--workload) time the same step on their shapes as the main
+line; their tables are larger than LDS (the tiny classifier's aside), so a
+step is an encode launch plus an accumulate launch (the row-uniform kernel
+for tables at least 512 int8 or 256 fp32 columns wide, the column-tiled one
+otherwise).
 """
 from __future__ import annotations
 
@@ -89,37 +96,164 @@ def stored_traffic(workload: str, kh: str):
         return None
 
 
-def cpu_baseline(p, budget_s: float):
-    """The oracle as it stands, timed on whole passes over the workload's rows
-    (or a prefix of them, if one pass would exceed the budget) until about
-    `budget_s` seconds of host time have been spent."""
+def _oracle_path(p):
+    """The oracle's whole path for workload p: a function of rows of A."""
     import oracle
     o = oracle.get()
     if p.spec.quantized:
         lut, scale, offset = o.build_quantized_lut(p.P, p.B)
-        run = lambda A: o.matmul(A, p.split, p.thr, lut, scale, offset)
-        what = "int8"
-    else:
-        lut = o.build_lut_f32(p.P, p.B)
-        run = lambda A: o.matmul_f32(A, p.split, p.thr, lut)
-        what = "fp32"
+        return o, (lambda A: o.matmul(A, p.split, p.thr, lut, scale, offset)[2]), "int8"
+    lut = o.build_lut_f32(p.P, p.B)
+    return o, (lambda A: o.matmul_f32(A, p.split, p.thr, lut)[1]), "fp32"
+
+
+def _timed_passes(run, A, rows, budget_s):
+    done, passes = 0, 0
+    t = time.perf_counter()
+    while True:
+        run(A[:rows])
+        done += rows
+        passes += 1
+        if time.perf_counter() - t >= budget_s:
+            break
+    return done, passes, time.perf_counter() - t
+
+
+def cpu_baseline(p, budget_s: float, one_core_s: float):
+    """The oracle as it stands, timed on whole passes over the workload's rows
+    (or a prefix of them, if one pass would exceed the budget) until about
+    `budget_s` seconds of host time have been spent, on all the host threads
+    it uses; then on one thread over the first min(N, 8192) rows for about
+    `one_core_s` seconds."""
+    o, run, what = _oracle_path(p)
     probe = min(p.N, 256 if p.spec.C * p.spec.M > 100000 else 2048)
     t = time.perf_counter()
     run(p.A[:probe])
     per_row = max((time.perf_counter() - t) / probe, 1e-9)
     rows = int(min(p.N, max(probe, budget_s / per_row)))
-    done, passes = 0, 0
-    t = time.perf_counter()
-    while True:
-        run(p.A[:rows])
-        done += rows
-        passes += 1
-        if time.perf_counter() - t >= budget_s:
-            break
-    dt = time.perf_counter() - t
-    return {"value": done / dt, "unit": "rows/s", "cores": o.max_threads(), "kind": "oracle",
-            "sample": f"{passes} pass(es) over the first {rows} of {p.N} rows, full encode + "
-                      f"{what} lookup-accumulate, {dt:.1f} s wall"}
+    done, passes, dt = _timed_passes(run, p.A, rows, budget_s)
+    threads = o.max_threads()
+    out = {"value": done / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+           "sample": f"{passes} pass(es) over the first {rows} of {p.N} rows, full encode + "
+                     f"{what} lookup-accumulate, {dt:.1f} s wall"}
+    rows1 = min(p.N, 8192)
+    o.set_threads(1)
+    try:
+        d1, n1, t1 = _timed_passes(run, p.A, rows1, one_core_s)
+    finally:
+        o.set_threads(threads)
+    out["one_core"] = {"value": d1 / t1, "unit": "rows/s", "cores": 1,
+                       "sample": f"{n1} pass(es) over the first {rows1} rows, {t1:.1f} s wall"}
+    return out
+
+
+def parity_report(p, y_host, rows, run=None):
+    """The timed outputs of `rows` against the oracle's path on the same rows:
+    bit-identical outputs (the bar is 1e-6 relative) and the largest
+    relative difference."""
+    if run is None:
+        _, run, _ = _oracle_path(p)
+    ref = run(p.A[rows])
+    y = y_host[rows] if y_host.shape[0] != len(rows) else y_host
+    d = np.abs(y.astype(np.float64) - ref.astype(np.float64))
+    rel = d / np.maximum(np.abs(ref.astype(np.float64)), np.finfo(np.float32).tiny)
+    mx = float(rel.max(initial=0.0))
+    return {"rows_checked": int(len(rows)), "of_rows": int(p.N), "y_bit_identical": bool(np.array_equal(y, ref)),
+            "max_rel_err": mx, "ok": bool(mx <= 1e-6)}
+
+
+def sampled_rows(N, n=2048, seed=0):
+    """First and last n/4 rows and n/2 uniformly drawn rows."""
+    rng = np.random.default_rng(seed)
+    q = n // 4
+    rows = set(range(min(N, q))) | set(range(max(0, N - q), N)) | set(int(r) for r in rng.integers(0, N, size=n // 2))
+    return np.array(sorted(rows))
+
+
+def region_us(fn, stream, reps=20, warm=3):
+    """Average duration of one call of fn(i), from one event pair on the
+    launch stream around `reps` back-to-back calls (after `warm` calls)."""
+    import torch
+    for i in range(warm):
+        fn(i)
+    torch.cuda.synchronize()
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record(stream)
+    for i in range(reps):
+        fn(i)
+    r1.record(stream)
+    torch.cuda.synchronize()
+    return r0.elapsed_time(r1) / reps * 1e3
+
+
+def workload_block(name, steps, warmup, sample_n=2048):
+    """Compact measurement of one workload's step (the fused entry point over
+    all its rows, inputs resident): rows/s, step time, HBM fraction of the
+    algorithmic bytes, encode and accumulate alone, the accumulate's LDS
+    fraction (two-phase shapes), a dense fp32 GEMM of the same shape, and the
+    timed outputs against the oracle (every row of the tiny classifier, else
+    `sample_n` rows)."""
+    import torch
+    import paper_2207_05808_amd as mdn
+    from paper_2207_05808_amd import workloads as W
+    spec = W.SPECS[name]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    log(f"[bench] workload {name}: N={spec.N} D={spec.D} C={spec.C} M={spec.M}")
+    p = W.make(name)
+    N = p.N
+    A = torch.from_numpy(p.A).to(dev)
+    split, thr = torch.from_numpy(p.split).to(dev), torch.from_numpy(p.thr).to(dev)
+    Pd, Bd = torch.from_numpy(p.P).to(dev), torch.from_numpy(p.B).to(dev)
+    y = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
+    if spec.quantized:
+        lut, scale, offset = mdn.build_lut(Pd, Bd)
+        call = mdn.prepare_matmul(A, split, thr, lut, scale, offset, y_out=y)
+    else:
+        lut = mdn.build_lut_f32(Pd, Bd)
+        call = mdn.prepare_matmul_f32(A, split, thr, lut, y_out=y)
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    step_s = e0.elapsed_time(e1) / 1e3 / steps
+    y_host = y.cpu().numpy()
+    abytes = algorithmic_bytes(spec, N)
+    out = {"N": N, "D": spec.D, "C": spec.C, "M": spec.M, "table": "int8" if spec.quantized else "fp32",
+           "rows_per_s": round(N / wall, 1), "step_us": round(step_s * 1e6, 2),
+           "wall_us_per_step": round(wall * 1e6, 2), "algorithmic_bytes": abytes,
+           "hbm_frac": round(abytes / step_s / 1e9 / HBM_PEAK_GBS, 4), "steps": steps}
+    if mdn.matmul_index_bytes(A, spec.C, spec.M, f32=not spec.quantized) > 0:
+        idx = torch.empty((N, spec.C), dtype=torch.uint8, device=dev)
+        enc_us = region_us(lambda i: mdn.encode(A, split, thr, idx_out=idx), stream, reps=5, warm=1)
+        if spec.quantized:
+            acc_us = region_us(lambda i: mdn.lut_accumulate(idx, lut, scale, offset, y_out=y), stream, reps=5, warm=1)
+        else:
+            acc_us = region_us(lambda i: mdn.lut_accumulate_f32(idx, lut, y_out=y), stream, reps=5, warm=1)
+        lds_bytes = N * spec.C * spec.M * (2 if spec.quantized else 4)
+        out.update({"encode_us": round(enc_us, 2), "accumulate_us": round(acc_us, 2),
+                    "encode_hbm_frac": round((4 * spec.D + spec.C) * N / (enc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                    "accumulate_lds_frac": round(lds_bytes / (acc_us * 1e-6) / 1e12 / LDS_PEAK_TBS, 4),
+                    "accumulate_lds_read_bytes": lds_bytes})
+        del idx
+    torch.backends.cuda.matmul.allow_tf32 = False
+    gout = torch.empty((N, spec.M), dtype=torch.float32, device=dev)
+    gemm_us = region_us(lambda i: torch.mm(A, Bd, out=gout), stream, reps=5, warm=2)
+    out["dense_fp32_gemm_us"] = round(gemm_us, 2)
+    del gout, A, y, Pd, Bd, lut
+    torch.cuda.empty_cache()
+    rows = np.arange(N) if N <= 8192 else sampled_rows(N, sample_n)
+    out["parity"] = parity_report(p, y_host, rows)
+    if N > 8192:
+        out["parity"]["sample"] = f"first and last {sample_n // 4} rows and {sample_n // 2} random rows"
+    return out
 
 
 FIT_TRAIN_ROWS = 16384    # training rows for the table fit (the paper's layers use 10,000)
@@ -135,6 +269,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--one-core-seconds", type=float, default=3.0)
+    ap.add_argument("--workload-steps", type=int, default=10)
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the compact block for the other four workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-context", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -208,6 +346,12 @@ def main():
     value = N / (wall / K)
     log(f"[bench] wall {ms_per_step * 1e3:.1f} us/step, kernel avg {avg_kern_s * 1e6:.1f} us")
 
+    # the timed outputs against the oracle: every row of the tiny classifier
+    # and of the headline layer, a sample of the larger ones
+    y_host = y.cpu().numpy()
+    parity = parity_report(p, y_host, np.arange(N) if N <= 200000 else sampled_rows(N))
+    del y_host
+
     abytes = algorithmic_bytes(spec, N)
     achieved = abytes / avg_kern_s / 1e9
     kh = kernel_source_hash()
@@ -232,6 +376,7 @@ def main():
                    "table": "int8 block floating point" if spec.quantized else "fp32",
                    "parallelism": "single GPU"},
         "roofline": roofline,
+        "parity": parity,
     }
 
     if not args.no_context:
@@ -244,20 +389,11 @@ def main():
         else:
             acc_call = lambda: mdn.lut_accumulate_f32(idx, lut, y_out=y)
 
-        def region_us(fn, reps=20):
-            for i in range(3):
-                fn(i)
-            torch.cuda.synchronize()
-            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            r0.record(stream)
-            for i in range(reps):
-                fn(i)
-            r1.record(stream)
-            torch.cuda.synchronize()
-            return r0.elapsed_time(r1) / reps * 1e3
+        _region = region_us
+        region_us_ = lambda fn, reps=20: _region(fn, stream, reps=reps)   # noqa: E731
 
-        enc_us = region_us(lambda i: split_calls[i % 2]())
-        acc_us = region_us(lambda i: acc_call())
+        enc_us = region_us_(lambda i: split_calls[i % 2]())
+        acc_us = region_us_(lambda i: acc_call())
         result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
         if not headline:
             # the accumulate of the two-phase workloads is bound by LDS reads:
@@ -273,7 +409,7 @@ def main():
             # the rounded 8-bit averaging accumulate (approximate) over a
             # shared-exponent table of the same weights, on the same indices
             slut, sscale, soffset = mdn.build_lut_shared(Pd, Bd)
-            avg_us = region_us(lambda i: mdn.lut_accumulate_avg(idx, slut, sscale, soffset, y_out=y))
+            avg_us = region_us_(lambda i: mdn.lut_accumulate_avg(idx, slut, sscale, soffset, y_out=y))
             result["context"]["accumulate_avg8_us"] = round(avg_us, 2)
             # its accuracy cost: relative Frobenius distance to the exact sum
             # over the same shared-exponent table
@@ -295,7 +431,7 @@ def main():
                                                     act=a, y_out=y)
             else:
                 f = lambda i, a=act: mdn.matmul_act_f32(A_bufs[i % 2], split, thr, lut, col_bias=cb, act=a, y_out=y)
-            result["context"][f"step_with_{act}_us"] = round(region_us(f), 2)
+            result["context"][f"step_with_{act}_us"] = round(region_us_(f), 2)
 
         # the same step replayed from a captured HIP graph of 20 steps, as a
         # serving loop that captures its launches runs it (launch-bound
@@ -355,9 +491,9 @@ def main():
         # offline table construction on the GPU: T = P B in double, then the
         # 8-bit block floating point quantizer (or the fp32 rounding)
         if spec.quantized:
-            build_us = region_us(lambda i: mdn.build_lut(Pd, Bd), reps=3)
+            build_us = region_us_(lambda i: mdn.build_lut(Pd, Bd), reps=3)
         else:
-            build_us = region_us(lambda i: mdn.build_lut_f32(Pd, Bd), reps=3)
+            build_us = region_us_(lambda i: mdn.build_lut_f32(Pd, Bd), reps=3)
         result["context"]["build_lut_ms"] = round(build_us / 1e3, 3)
 
         # model-aware table fit (Eq. 3, affine output) on 16384 training rows
@@ -370,7 +506,7 @@ def main():
         idx_tr, idx_ho = mdn.encode(A_tr, split, thr), mdn.encode(A_ho, split, thr)
         T0 = mdn.build_lut_f32(Pd, Bd)
         ws = torch.empty((mdn.fit_lut_workspace_bytes(n_tr, spec.C) + 256,), dtype=torch.uint8, device=dev)
-        fit_us = region_us(lambda i: mdn.fit_lut_ridge(idx_tr, Y_tr, T0, FIT_LAMBDA, workspace=ws), reps=3)
+        fit_us = region_us_(lambda i: mdn.fit_lut_ridge(idx_tr, Y_tr, T0, FIT_LAMBDA, workspace=ws), reps=3)
         T_fit = mdn.fit_lut_ridge(idx_tr, Y_tr, T0, FIT_LAMBDA, workspace=ws).float()
 
         def rel_err(T):
@@ -387,7 +523,7 @@ def main():
         ws_gd = torch.empty((mdn.fit_lut_gd_workspace_bytes(n_tr, spec.C, spec.M) + 256,), dtype=torch.uint8,
                             device=dev)
         for act in ("relu", "softmax"):
-            us = region_us(lambda i, a=act: mdn.fit_lut_gd(idx_tr, Y_tr, T0, a, FIT_LAMBDA, eta, FIT_GD_STEPS,
+            us = region_us_(lambda i, a=act: mdn.fit_lut_gd(idx_tr, Y_tr, T0, a, FIT_LAMBDA, eta, FIT_GD_STEPS,
                                                             workspace=ws_gd), reps=2)
             result["context"][f"fit_gd_{act}_ms_per_step"] = round(us / 1e3 / FIT_GD_STEPS, 3)
         del ws_gd
@@ -408,9 +544,15 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] copy calibration: 3 x ({nb} bytes read + {nb} bytes written)")
 
+    if not args.no_context and not args.no_workloads and args.workload is None:
+        del A_bufs, y, calls, lut, scale, offset
+        torch.cuda.empty_cache()
+        result["context"]["workloads"] = {
+            w: workload_block(w, args.workload_steps, 3) for w in W.SPECS if w != W.HEADLINE}
+
     if not args.no_cpu_baseline:
-        log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s)")
-        result["cpu_baseline"] = cpu_baseline(p, args.cpu_seconds)
+        log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s + {args.one_core_seconds:.0f} s on one core)")
+        result["cpu_baseline"] = cpu_baseline(p, args.cpu_seconds, args.one_core_seconds)
 
     print(json.dumps(result), flush=True)
 

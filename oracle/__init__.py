@@ -79,6 +79,8 @@ class Oracle:
         lib.oracle_exponent_cap.argtypes = [i32]
         lib.oracle_block_exponent.argtypes = [ctypes.c_float, vp]
         lib.oracle_sigma.argtypes = [vp, i64, i32, vp, i32, vp]
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_threads.restype = None
         lib.oracle_quantize_table_shared.argtypes = [vp, i32, i32, vp, vp, vp]
         lib.oracle_lut_accumulate_avg.argtypes = [vp, i64, i32, vp, vp, vp, i32, vp, vp]
         lib.oracle_encoder_gram.argtypes = [vp, i64, i32, vp]
@@ -95,6 +97,10 @@ class Oracle:
 
     def max_threads(self) -> int:
         return int(self.lib.oracle_max_threads())
+
+    def set_threads(self, n: int) -> None:
+        """Host threads the row loops use from now on (timing only)."""
+        self.lib.oracle_set_threads(int(n))
 
     def encode(self, A, split, thr):
         A = np.asarray(A, dtype=np.float32)

@@ -91,6 +91,16 @@ int oracle_max_threads(void) {
 #endif
 }
 
+/* Host threads for the row loops of later calls (timing only; n >= 1). */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /*
  * Encoding function (§1: each subvector is mapped to the index of one of K
  * prototypes, a log2(K)-bit integer; §1 and §2.1: MADDNESS does it with a

@@ -93,10 +93,11 @@ def test_avg_workloads_with_shared_tables(orc, name):
 def test_avg_full_size_sampled(orc, name):
     """Full-size workload in the launch configuration the benchmark's context
     times (GPU encoder, GPU shared-exponent table, averaging accumulate over
-    every row); the oracle encodes and sums a sample of rows itself."""
-    from test_gpu_parity import sample_rows
+    every row); the oracle encodes and sums every row of the conv layer and
+    a sample of about 6000 rows of the larger ones itself."""
+    from test_gpu_parity import parity_rows
     p = W.make(name)
-    rows = sample_rows(p.N)
+    rows = parity_rows(name, p.N)
     idx = mdn.encode(dev(p.A), dev(p.split), dev(p.thr))
     lut, scale, offset = mdn.build_lut_shared(dev(p.P), dev(p.B))
     rl, rs, ro = orc.build_shared_lut(p.P, p.B)

@@ -317,27 +317,41 @@ def test_empty_inputs():
 
 
 # ------------------------------------------------------ full-size, sampled
-def sample_rows(N, RW=64, seed=0):
+# workloads whose every row the oracle recomputes in well under a second
+ALL_ROWS = ("classifier_tiny", "conv3x3_im2col")
+
+
+def sample_rows(N, RW=64, seed=0, edge=1000, random=4000, cuts=200):
+    """First and last `edge` rows, `random` rows drawn uniformly, and the two
+    rows around `cuts` evenly spaced boundaries (chunk, work-item and tile
+    edges fall among them)."""
     rng = np.random.default_rng(seed)
-    rows = set(range(min(N, 300))) | set(range(max(0, N - 300), N))
-    rows |= set(int(r) for r in rng.integers(0, N, size=1500))
-    for b in range(RW, N, max(RW, N // 50)):  # around chunk / tile boundaries
+    rows = set(range(min(N, edge))) | set(range(max(0, N - edge), N))
+    rows |= set(int(r) for r in rng.integers(0, N, size=random))
+    for b in range(RW, N, max(RW, N // cuts)):
         rows |= {b - 1, b}
     return np.array(sorted(r for r in rows if 0 <= r < N))
+
+
+def parity_rows(name, N):
+    return np.arange(N) if name in ALL_ROWS else sample_rows(N)
 
 
 @pytest.mark.slow
 @pytest.mark.parametrize("name", list(W.SPECS))
 def test_matmul_full_size_sampled(orc, name):
-    """Full-size workload in the launch configuration the benchmark times; the
-    oracle recomputes a sample of rows (first, last, random, chunk edges)."""
+    """Full-size workload in the launch configuration the benchmark times.
+    The oracle recomputes every row of the classifier and conv layers, and
+    about 6000 rows of the three large layers (first and last 1000, 4000
+    random, both sides of 200 evenly spaced boundaries)."""
     p = W.make(name)
-    rows = sample_rows(p.N)
+    rows = parity_rows(name, p.N)
     A = dev(p.A)
     split, thr = dev(p.split), dev(p.thr)
+    racc = acc = None
     if p.spec.quantized:
         lut, scale, offset = mdn.build_lut(dev(p.P), dev(p.B))
-        y, _, idx = mdn.matmul(A, split, thr, lut, scale, offset, want_idx=True)
+        y, acc, idx = mdn.matmul(A, split, thr, lut, scale, offset, want_acc=True, want_idx=True)
         rl, rs, ro = orc.build_quantized_lut(p.P, p.B)
         assert np.array_equal(host(lut), rl)
         ridx, racc, ry = orc.matmul(p.A[rows], p.split, p.thr, rl, rs, ro)
@@ -347,10 +361,12 @@ def test_matmul_full_size_sampled(orc, name):
         ridx, ry = orc.matmul_f32(p.A[rows], p.split, p.thr, orc.build_lut_f32(p.P, p.B))
     r = torch.from_numpy(rows).to(DEV)
     assert np.array_equal(host(idx[r]), ridx)
+    if acc is not None:
+        assert np.array_equal(host(acc[r]), racc)
     assert_y(host(y[r]), ry)
     # every index of every row is a valid leaf (a property at any size)
     assert int(idx.max()) < 16
-    del y, idx, A
+    del y, acc, idx, A
     torch.cuda.empty_cache()
 
 
