@@ -37,9 +37,11 @@
  *  - Output arrays must not overlap each other or any input array of the same
  *    call (kernels may read inputs, indices in particular, through the scalar
  *    cache while outputs are being written).  Inputs may overlap each other.
- *  - Thread safety: the only global state is a per-kernel cache of launch
- *    attributes, filled once under a mutex; concurrent calls on different
- *    streams are independent.
+ *  - Thread safety: the global state is a per-kernel cache of launch
+ *    attributes and the per-device address of maddness_matmul_noalloc's
+ *    scratch array, each filled once under a mutex; concurrent calls on
+ *    different streams are independent, except calls of
+ *    maddness_matmul_noalloc on one device (see there).
  */
 #ifndef MADDNESS_H
 #define MADDNESS_H
@@ -222,6 +224,31 @@ int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda,
                             int32_t C, const float* lut, int32_t M,
                             const float* col_bias, int32_t act, float* y_out,
                             uint8_t* idx_out, void* stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid allocation, even through
+ * a caching allocator): maddness_matmul with the same arguments and results,
+ * except that idx_out is optional for every shape.  When the table does not
+ * fit the single-launch kernels and idx_out is NULL, the indices go through
+ * a scratch array inside the library: a 32 MiB static device array on each
+ * device the library runs on, held until the process ends, whose address is
+ * resolved once per device on its first such call.  Rows are processed in
+ * chunks of (32 MiB / C) rounded down to a multiple of 256 rows (at least
+ * 65536), each encoded into the scratch array and accumulated from it, so no
+ * call size exceeds it.  Calls that take the scratch path share the device's
+ * array: two such calls on one device whose work overlaps (different
+ * streams, or different host threads without ordering) race on it and give
+ * unspecified results; calls on one stream are ordered and safe.  The array
+ * keeps the last call's indices; nothing is read before it is written, so
+ * nothing needs clearing.  Allocates nothing.  EHIP if the scratch address
+ * cannot be resolved; otherwise the errors of maddness_matmul.
+ */
+int maddness_matmul_noalloc(const float* A, int64_t N, int32_t D, int64_t lda,
+                            const int32_t* split_dims, const float* thresholds,
+                            int32_t C, const int8_t* lut, const float* scale,
+                            const float* offset, int32_t M, float* y_out,
+                            int32_t* acc_out, uint8_t* idx_out, void* stream);
 
 /*
  * Device bytes the fused entry points need in idx_out for this call: 0 when

@@ -10,7 +10,7 @@ seeded input generator) imports without torch or the HIP library.
 _BINDING = ("encode", "lut_accumulate", "lut_accumulate_f32", "matmul", "matmul_f32", "matmul_act",
             "matmul_act_f32", "lut_accumulate_avg", "build_lut_shared",
             "build_lut", "build_lut_f32", "quantize_lut", "encoder_gram", "encoder_scatter", "fit_lut_ridge", "fit_lut_gd",
-            "fit_lut_workspace_bytes", "fit_lut_gd_workspace_bytes", "matmul_index_bytes",
+            "fit_lut_workspace_bytes", "fit_lut_gd_workspace_bytes", "matmul_index_bytes", "matmul_noalloc",
             "version", "prepare_matmul", "prepare_matmul_f32", "PreparedCall")
 
 __all__ = list(_BINDING) + ["MaddnessError"]

@@ -61,6 +61,8 @@ def lib() -> ctypes.CDLL:
         L.maddness_fit_lut_workspace_bytes.argtypes = [i64, i32]
         L.maddness_fit_lut_workspace_bytes.restype = i64
         L.maddness_fit_lut_ridge.argtypes = [vp, i64, i32, vp, i32, vp, ctypes.c_double, vp, vp, i64, vp]
+        L.maddness_matmul_noalloc.argtypes = [vp, i64, i32, i64, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp]
+        L.maddness_matmul_noalloc.restype = ctypes.c_int
         L.maddness_matmul_index_bytes.argtypes = [vp, i64, i32, i64, i32, i32, i32, i32]
         L.maddness_matmul_index_bytes.restype = i64
         L.maddness_fit_lut_gd_workspace_bytes.argtypes = [i64, i32, i32]

@@ -211,6 +211,34 @@ def matmul(A, split_dims, thresholds, lut, scale, offset, y_out=None, acc_out=No
     return y_out, acc_out, idx_out
 
 
+def matmul_noalloc(A, split_dims, thresholds, lut, scale, offset, y_out, acc_out=None, idx_out=None,
+                   stream=None):
+    """maddness_matmul_noalloc: the fused int8 path with every buffer given
+    by the caller (y_out required) and, for large tables without idx_out,
+    the library's static scratch array in place of an index array; neither
+    this function nor the library allocates.  Returns y_out."""
+    N, D, lda = _rows(A)
+    C = _tree_args(split_dims, thresholds)
+    C2, M = _lut_i8(lut, scale, offset)
+    if C2 != C:
+        raise ValueError("lut codebooks differ from the trees'")
+    _need(y_out, "y_out", torch.float32, 2)
+    _dense(y_out, "y_out")
+    if tuple(y_out.shape) != (N, M):
+        raise ValueError("y_out must be [N, M]")
+    if acc_out is not None:
+        _need(acc_out, "acc_out", torch.int32, 2)
+        _dense(acc_out, "acc_out")
+        if tuple(acc_out.shape) != (N, M):
+            raise ValueError("acc_out must be [N, M]")
+    idx_out = _idx_out(idx_out, N, C)
+    st = _lib.lib().maddness_matmul_noalloc(_ptr(A), N, D, lda, _ptr(split_dims), _ptr(thresholds), C,
+                                            _ptr(lut), _ptr(scale), _ptr(offset), M, _ptr(y_out),
+                                            _ptr(acc_out), _ptr(idx_out), _stream(stream))
+    _lib.check("maddness_matmul_noalloc", st)
+    return y_out
+
+
 def matmul_f32(A, split_dims, thresholds, lut, y_out=None, idx_out=None, want_idx=False, stream=None,
                validate=False):
     """Fused encode + fp32 lookup-accumulate; returns (y, idx or None)."""

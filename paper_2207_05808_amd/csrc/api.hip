@@ -5,6 +5,14 @@
 
 #include <stdint.h>
 #include <cmath>
+#include <mutex>
+
+// Index array of maddness_matmul_noalloc's two-phase path, for callers that
+// cannot allocate device memory: kScratchBytes on each device the library
+// runs on, held until the process ends.  Host code never uses this name as
+// an address: scratch_base() resolves it per device.
+constexpr int64_t kScratchBytes = int64_t(32) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 namespace mdn {
 namespace {
@@ -486,6 +494,30 @@ int fused(const Shape& s, hipStream_t st) {
   return two_phase(s, s.idx_out, st);
 }
 
+// Device address of `scratch` on the current device, resolved once per device
+// (hipGetSymbolAddress with that device current) and cached; nullptr with
+// *rc = EHIP when the device or the symbol cannot be queried.
+uint8_t* scratch_base(int* rc) {
+  constexpr int kDevs = 64;
+  static std::mutex mu;
+  static uint8_t* base[kDevs] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevs) {
+    *rc = MADDNESS_EHIP;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!base[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      *rc = MADDNESS_EHIP;
+      return nullptr;
+    }
+    base[dev] = static_cast<uint8_t*>(p);
+  }
+  return base[dev];
+}
+
 }  // namespace
 }  // namespace mdn
 
@@ -626,6 +658,41 @@ int maddness_matmul_act_f32(const float* A, int64_t N, int32_t D, int64_t lda, c
   s.lut = lut; s.M = M; s.y = y_out;
   s.col_bias = col_bias; s.act = act; s.idx_out = idx_out;
   return fused(s, static_cast<hipStream_t>(stream));
+}
+
+int maddness_matmul_noalloc(const float* A, int64_t N, int32_t D, int64_t lda, const int32_t* split_dims,
+                            const float* thresholds, int32_t C, const int8_t* lut, const float* scale,
+                            const float* offset, int32_t M, float* y_out, int32_t* acc_out, uint8_t* idx_out,
+                            void* stream) {
+  int rc = check_encode_args(A, N, D, lda, split_dims, thresholds, C);
+  if (rc != MADDNESS_OK) return rc;
+  rc = check_accum_args(N, C, lut, M);
+  if (rc != MADDNESS_OK || N == 0) return rc;
+  if (!scale || !offset || !y_out || !aligned(scale, 4) || !aligned(offset, 4) || !aligned(y_out, 4) ||
+      (acc_out && !aligned(acc_out, 4)))
+    return MADDNESS_EINVAL;
+  Shape s = shape(kFused, kI8);
+  s.A = A; s.N = N; s.D = D; s.lda = lda; s.split = split_dims; s.thr = thresholds; s.C = C;
+  s.lut = lut; s.scale = scale; s.offset = offset; s.M = M; s.y = y_out; s.acc = acc_out;
+  s.idx_out = idx_out;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (idx_out || single_launch(s)) return fused(s, st);
+  uint8_t* idx = scratch_base(&rc);
+  if (!idx) return rc;
+  // rows per chunk: as many whole 256-row groups as the scratch holds (C <=
+  // 512, so at least 65536 rows); each chunk is encoded into the scratch and
+  // accumulated from it before the next chunk's encode, in stream order
+  const int64_t chunk = (kScratchBytes / C) / 256 * 256;
+  for (int64_t r0 = 0; r0 < N; r0 += chunk) {
+    Shape c = s;
+    c.N = (N - r0 < chunk) ? N - r0 : chunk;
+    c.A = A + r0 * lda;
+    c.y = y_out + r0 * M;
+    c.acc = acc_out ? acc_out + r0 * M : nullptr;
+    rc = two_phase(c, idx, st);
+    if (rc != MADDNESS_OK) return rc;
+  }
+  return MADDNESS_OK;
 }
 
 int64_t maddness_matmul_index_bytes(const float* A, int64_t N, int32_t D, int64_t lda, int32_t C, int32_t M,
