@@ -22,8 +22,9 @@
 //    (128 * sum_c 2^(e_c - e_min) <= 32768) are staged in LDS as int16
 //    values q << (e_c - e_min) and summed with packed 16-bit adds: the
 //    arithmetic is modular and the exact total fits, so the sum is exact;
-//  * other int8 tables are staged as int8 and summed with v_dot4c_i32_i8
-//    against per-codebook weights 2^sh << 8b (exact int32);
+//  * other int8 tables are staged as int8; each code is sign-extended from
+//    its byte (v_bfe_i32), shifted by its codebook's e_c - e_min and added
+//    in int32 (exact under the accumulator's precondition);
 //  * fp32 tables are summed with ordered fp32 adds, codebooks ascending.
 // Codebooks are padded to a multiple of 4 with offsets of an all-zero row.
 #include "internal.hpp"
