@@ -314,11 +314,14 @@ bool plan_tacc(const Shape& s, TArgs* t, int* nj_out, int* nw_out) {
 // tile wide (512 int8 or 256 fp32 columns): scalar loads of 4-byte index words
 // (C % 4 == 0), table rows in whole 16-byte units (int8: M % 16 == 0, fp32:
 // M % 4 == 0 and a 16-byte aligned table), 16-byte output stores, and enough
-// 256-row work items to occupy a quarter of the CUs.
-bool plan_trow(const Shape& s, TArgs* t) {
+// 256-row work items to occupy a quarter of the CUs.  `companion`: the launch
+// after the row-streaming fused kernel (int8, any M % 16 == 0 up to one tile,
+// index rows `idx_stride` bytes apart), which sums only when that kernel could
+// not.
+bool plan_trow(const Shape& s, TArgs* t, bool companion = false, int64_t idx_stride = 0) {
   const bool f32 = s.elem == kF32;
   const int cols = f32 ? kRowTileColsF32 : kRowTileCols;
-  if (s.M < cols || s.M % (f32 ? 4 : 16) != 0 || s.C % 4 != 0) return false;
+  if ((!companion && s.M < cols) || s.M % (f32 ? 4 : 16) != 0 || s.C % 4 != 0) return false;
   if (!aligned(s.idx_in, 4) || !aligned(s.lut, f32 ? 16 : 4)) return false;
   if ((s.y && !aligned(s.y, 16)) || (s.acc && !aligned(s.acc, 16))) return false;
   if ((int64_t)s.C * kK * s.M * (f32 ? 4 : 1) >= (1ll << 31)) return false;   // 32-bit buffer offsets
@@ -329,7 +332,9 @@ bool plan_trow(const Shape& s, TArgs* t) {
   a.RB = 256;
   a.ntm = (s.M + cols - 1) / cols;
   a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
-  if (a.nwork * 4 < device_cus()) return false;
+  if (!companion && a.nwork * 4 < device_cus()) return false;
+  a.idx_stride = companion ? idx_stride : s.C;
+  a.only_wide = companion ? 1 : 0;
   a.col_bias = s.col_bias;
   a.act = (s.act == 3 && a.ntm > 1) ? 1 : s.act;   // rows over several tiles: softmax as a second pass
   int off = 0;
@@ -352,6 +357,49 @@ int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   const int rc = plan(s, &p, single_tile_only);
   if (rc != MADDNESS_OK) return rc;
   return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, stream));
+}
+
+// Row-streaming fused kernel (fused_rows.hip): int8 tables of 64 codebooks,
+// 16 <= M <= 512 with M % 16 == 0, at least kFencMinRows rows (each of the at
+// least 64 workgroups gets a few hundred), 16-byte aligned table and outputs,
+// row blocks whose byte offsets fit 32 bits.  With `cus` = 0 (the index-bytes
+// query, which makes no HIP call) only the shape is checked.  The companion
+// launch (row-uniform accumulate, 32-bit sums when the 16-bit fields do not
+// fit) reads the indices from idx_out, else from the first 64 bytes of each
+// output row.
+constexpr int64_t kFencMinRows = 98304;
+bool plan_fenc(const Shape& s, FArgs* f, int* blocks_out, TArgs* companion, int cus) {
+  if (s.mode != kFused || s.elem != kI8 || s.C != 64) return false;
+  if (s.M < 16 || s.M > kRowTileCols || s.M % 16 != 0 || s.N < kFencMinRows) return false;
+  if (!aligned(s.lut, 16) || !aligned(s.y, 16) || (s.acc && !aligned(s.acc, 16))) return false;
+  // rows per workgroup with at least 64 workgroups; the kernel's gathers run
+  // up to 12 x 36 rows past its block (those offsets must stay below 2^31)
+  const int64_t max_block = (s.N + 63) / 64;
+  if ((max_block + 512) * s.lda * 4 >= (1ll << 31)) return false;
+  if (cus <= 0) return true;
+  const int blocks = cus > 64 ? cus : 64;
+  FArgs a{};
+  a.A = s.A; a.split = s.split; a.thr = s.thr; a.lut = static_cast<const int8_t*>(s.lut);
+  a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc; a.idx_out = s.idx_out;
+  a.col_bias = s.col_bias; a.act = s.act;
+  a.N = s.N; a.lda = s.lda; a.D = s.D; a.M = s.M;
+  a.rows_per_block = (s.N + blocks - 1) / blocks;
+  a.bias_lds = (s.act != 0 && s.col_bias) ? 1 : 0;
+  int off = 2 * 4 * kK * 2 * kRowTileCols;   // two tile buffers of 4 codebooks x 16 rows x 1 KB
+  a.off_ring = off;
+  off += kFRing * (12 * 64 + 4);
+  a.off_bias = off;
+  off += a.bias_lds ? round_up(s.M * 4, 16) : 0;
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  Shape q = s;
+  q.mode = kAccum;
+  q.idx_in = s.idx_out ? s.idx_out : reinterpret_cast<const uint8_t*>(s.y);
+  q.idx_out = nullptr;
+  if (!plan_trow(q, companion, true, s.idx_out ? (int64_t)s.C : (int64_t)s.M * 4)) return false;
+  *f = a;
+  *blocks_out = blocks;
+  return true;
 }
 
 // Rounded 8-bit averaging accumulate (tiled_accum.hip): 8 wavefronts, the
@@ -476,6 +524,9 @@ bool single_launch(const Shape& s) {
   GArgs g;
   int ng, uq, nw;
   if (plan_gfused(s, &g, &ng, &uq, &nw)) return true;
+  FArgs f;
+  int blocks;
+  if (plan_fenc(s, &f, &blocks, nullptr, 0)) return true;   // (needs no index array)
   Plan p;
   return s.act == 0 && plan(s, &p, true) == MADDNESS_OK;
 }
@@ -487,6 +538,14 @@ int fused(const Shape& s, hipStream_t st) {
   int ng, uq, nw;
   if (plan_gfused(s, &g, &ng, &uq, &nw))
     return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
+  FArgs f;
+  TArgs t;
+  int blocks;
+  if (plan_fenc(s, &f, &blocks, &t, device_cus())) {
+    const int rc = status_from(launch_fenc(f, blocks, st));
+    if (rc != MADDNESS_OK) return rc;
+    return status_from(launch_trow(kI8, t, device_cus(), st));
+  }
   Plan p;
   if (s.act == 0 && plan(s, &p, true) == MADDNESS_OK)
     return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, st));

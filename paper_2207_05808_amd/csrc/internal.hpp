@@ -117,6 +117,9 @@ struct TArgs {
   int act;                // 0 none, 1 bias, 2 bias + ReLU, 3 bias + row softmax (one column tile only)
   int off_tab, off_idx, off_sh, off_misc, lds_total;  // LDS byte offsets
   int bias_lds, off_bias; // row-uniform kernels: column biases staged in LDS at off_bias (else read from memory)
+  int64_t idx_stride;     // row-uniform kernels: bytes between index rows (C, or another layout's row pitch)
+  int only_wide;          // row-uniform int8 kernel: do nothing when the 16-bit field sums fit (the
+                          // fused row-streaming kernel has already written every output then)
 };
 
 // Row softmax in place over y [N][M] (layer outputs whose rows span several
@@ -131,6 +134,28 @@ hipError_t launch_tacc(int elem, int nj, const TArgs& t, int nw, int cus, hipStr
 constexpr int kRowTileCols = 512;
 constexpr int kRowTileColsF32 = 256;
 hipError_t launch_trow(int elem, const TArgs& t, int cus, hipStream_t stream);
+
+// Fused encode + accumulate streaming rows (fused_rows.hip): int8 tables of
+// exactly 64 codebooks and M <= 512 columns (M % 16 == 0), one 1024-thread
+// workgroup per CU over a contiguous block of rows_per_block rows.
+constexpr int kFRing = 20;   // steps of index rows the row-streaming kernel keeps in LDS
+struct FArgs {
+  const float* A;         // [N][lda]
+  const int32_t* split;   // [64][4]
+  const float* thr;       // [64][15]
+  const int8_t* lut;      // [64][16][M]
+  const float* scale;     // [64]
+  const float* offset;    // [64]
+  float* y;               // [N][M]
+  int32_t* acc;           // [N][M] or null
+  uint8_t* idx_out;       // [N][64] or null
+  const float* col_bias;  // [M] or null
+  int64_t N, lda, rows_per_block;
+  int D, M, act;
+  int bias_lds;           // column biases staged in LDS (act != 0 and col_bias given)
+  int off_ring, off_bias, lds_total;   // LDS byte offsets (the two table tile buffers at 0)
+};
+hipError_t launch_fenc(const FArgs& f, int blocks, hipStream_t stream);
 
 // Rounded 8-bit summation over codebooks: the whole [C][16][Mt] column slice
 // (one byte per entry) staged once per workgroup, Mt = 16 * lanes per row.

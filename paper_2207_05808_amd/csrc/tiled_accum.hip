@@ -438,6 +438,25 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
   tlds_i32* s_sh = reinterpret_cast<tlds_i32*>(smem + a.off_sh);
   tlds_i32* s_misc = reinterpret_cast<tlds_i32*>(smem + a.off_misc);   // bias32, e_min, sum of 2^sh, max shift
 
+  if (a.only_wide) {
+    // the launch after the row-streaming kernel: leave at once unless the
+    // 16-bit field sums did not fit (every wavefront decides alone, from the
+    // scales: the same test as below)
+    const uint32_t* sb0 = reinterpret_cast<const uint32_t*>(a.scale);
+    int e = INT_MAX;
+    for (int c = lane; c < C; c += 64) e = min(e, (int)((sb0[c] >> 23) & 0xffu) - 127);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) e = min(e, __shfl_xor(e, o));
+    int S0 = 0;
+    for (int c = lane; c < C; c += 64) {
+      const int sh = min((int)((sb0[c] >> 23) & 0xffu) - 127 - e, 30);
+      S0 += sh <= 14 ? (1 << sh) : (1 << 15);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) S0 += __shfl_xor(S0, o);
+    if (tuni(S0) <= 257) return;   // uniform over the workgroup
+  }
+
   // ---------------- block exponents, shifts and bias32
   if (tid == 0) { s_misc[1] = INT_MAX; s_misc[2] = 0; s_misc[3] = 0; }
   __syncthreads();
@@ -570,7 +589,7 @@ __global__ void __launch_bounds__(1024) trow_kernel(const TArgs a, const uint8_t
         uint32_t d[NJ];   // index bytes of codebooks c0..c0+3 (uniform)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
-          d[j] = *reinterpret_cast<const uint32_t*>(idx + min(r0 + j, N - 1) * C + c0);   // rows past N: any valid row
+          d[j] = *reinterpret_cast<const uint32_t*>(idx + min(r0 + j, N - 1) * a.idx_stride + c0);   // rows past N: any valid row
         const uint32_t lane_buf = lane_slot + (t & 1) * kRowTileBytes;
         auto slot_of = [&](int cb, int k) -> const tlds_t* {
           uint32_t adr;
@@ -786,7 +805,7 @@ __global__ void __launch_bounds__(1024) trow_f32_kernel(const TArgs a, const uin
       uint32_t d[NJ];   // index bytes of codebooks c0..c0+3 (uniform)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        d[j] = *reinterpret_cast<const uint32_t*>(idx + min(r0 + j, N - 1) * C + c0);   // rows past N: any valid row
+        d[j] = *reinterpret_cast<const uint32_t*>(idx + min(r0 + j, N - 1) * a.idx_stride + c0);   // rows past N: any valid row
       const uint32_t lane_buf = lane_slot + gb * kRowTileBytes;
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb) {

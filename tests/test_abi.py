@@ -89,14 +89,20 @@ def test_matmul_rejects(L):
 
 def test_matmul_index_bytes(L):
     """The fused entry points need a caller index array exactly when their
-    single-launch kernels cannot take the table: 0 for the im2col conv layer
-    (C = 32, M = 64) and the tiny classifier, N * C for the dense hidden
-    layer, the wide layer and the fp32 search-tree layer."""
+    own kernels cannot take the table: 0 for the im2col conv layer (C = 32,
+    M = 64), the tiny classifier and the dense hidden layer (C = 64, M = 512:
+    the row-streaming kernel, from 98304 rows on), N * C for the dense hidden
+    layer's shape below that, the wide layer and the fp32 search-tree layer."""
     Q = L.maddness_matmul_index_bytes
     assert Q(FAKE, 131072, 576, 576, 32, 64, 0, 0) == 0
     assert Q(FAKE, 131072, 576, 576, 32, 64, 0, 3) == 0
     assert Q(FAKE, 1024, 64, 64, 4, 10, 0, 3) == 0
-    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 0) == (1 << 20) * 64
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 0) == 0
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 3) == 0
+    assert Q(FAKE, 98304, 512, 512, 64, 512, 0, 0) == 0
+    assert Q(FAKE, 98303, 512, 512, 64, 512, 0, 0) == 98303 * 64
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 520, 0, 0) == (1 << 20) * 64     # M % 16 != 0
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 1, 0) == (1 << 20) * 64     # fp32 table
     assert Q(FAKE, 262144, 1024, 1024, 128, 4096, 0, 2) == 262144 * 128
     assert Q(FAKE, 524288, 256, 256, 256, 1024, 1, 0) == 524288 * 256
     assert Q(NULL, 0, 512, 512, 64, 512, 0, 0) == 0          # N == 0: nothing to do
