@@ -532,12 +532,20 @@ bool single_launch(const Shape& s) {
 }
 
 // Every fused entry point: one launch when the shape allows it, else the
-// two-phase path through the caller's index array (required there).
+// two-phase path through the caller's index array (required there).  When
+// the table's rows are not whole 16-byte units the gather-fused kernel stages
+// them element by element, and the general kernel (rows of A staged with
+// 16-byte loads, no dependent gather) is faster on such layers (the tiny
+// classifier, M = 10: 6.9 against 10.5 us per call, at 256 to 16384 rows);
+// it has no layer-output epilogue, so it takes act == 0 only.
 int fused(const Shape& s, hipStream_t st) {
   GArgs g;
   int ng, uq, nw;
-  if (plan_gfused(s, &g, &ng, &uq, &nw))
-    return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
+  Plan p;
+  const bool gf = plan_gfused(s, &g, &ng, &uq, &nw);
+  if (gf && !g.vec16 && s.act == 0 && plan(s, &p, true) == MADDNESS_OK)
+    return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, st));
+  if (gf) return status_from(launch_gfused(s.elem, ng, uq, g, nw, device_cus(), st));
   FArgs f;
   TArgs t;
   int blocks;
@@ -546,7 +554,6 @@ int fused(const Shape& s, hipStream_t st) {
     if (rc != MADDNESS_OK) return rc;
     return status_from(launch_trow(kI8, t, device_cus(), st));
   }
-  Plan p;
   if (s.act == 0 && plan(s, &p, true) == MADDNESS_OK)
     return status_from(launch_path(s.mode, s.elem, p.pf, p.uq, p.a, p.grid, p.block, st));
   if (!s.idx_out) return MADDNESS_EINVAL;

@@ -247,8 +247,9 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   if (!vec_all) {
     // general staging (tables larger than the up-front units, or rows that are
     // not whole 16-byte units): 8 LDS dwords per thread per round, all global
-    // loads of a round issued first; columns padded to octets with zeros
-    __syncthreads();   // shifts visible
+    // loads of a round issued first; columns padded to octets with zeros.  A
+    // codebook's shift comes from the lane that holds it (no barrier: the
+    // rounds are uniform, so every lane takes part in each shuffle)
     const int wpr = (ELEM == kF32) ? 8 * no : (narrow ? 4 * no : 2 * no);  // dwords per LDS row
     int wlog = 0;
     while ((1 << wlog) < wpr) ++wlog;
@@ -256,7 +257,8 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
     const int8_t* q8 = reinterpret_cast<const int8_t*>(g.lut);
     const float* qf = reinterpret_cast<const float*>(g.lut);
     const int64_t last = (int64_t)rows * M - 1;
-    for (int base = tid; base < total; base += 8 * blockDim.x) {
+    for (int base0 = 0; base0 < total; base0 += 8 * blockDim.x) {
+      const int base = base0 + tid;
       uint32_t v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -279,13 +281,13 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
       for (int j = 0; j < 8; ++j) {
         const int u = base + j * blockDim.x;
         const int row = u >> wlog, w = u & ((1 << wlog) - 1);
+        const int shr = __shfl(sh, min(row >> 4, C - 1));   // lane row / 16 holds that codebook's shift
         if (u >= total || w >= wpr) continue;
         uint32_t xx = 0;
         if (row < rows) {
           if (ELEM == kF32) {
             xx = w < M ? v[j] : 0u;
           } else if (narrow) {
-            const int shr = s_shc[row >> 4];
             const int m = 2 * w;
             const int lo = m < M ? ((int)(int8_t)(v[j] & 0xffu) << shr) : 0;
             const int hi = m + 1 < M ? ((int)(int8_t)(v[j] >> 8) << shr) : 0;
