@@ -352,6 +352,40 @@ bool plan_trow(const Shape& s, TArgs* t, bool companion = false, int64_t idx_str
   return true;
 }
 
+// One output row per lane (row_lanes.hip): fp32 tables of at least 256
+// columns (M % 4 == 0) and C % 16 == 0, 16-byte aligned table, outputs and
+// index rows, the column biases in LDS when there are any, enough work items
+// for the CUs.  A row softmax takes the row-uniform kernel when the row is one
+// of its column tiles (fused there), else it is a second pass here too.
+bool plan_rlane(const Shape& s, TArgs* t) {
+  if (s.elem != kF32 || s.M < kRowTileColsF32 || s.M % 4 != 0 || s.C % kRowLaneCT != 0) return false;
+  if (s.act == 3 && s.M <= kRowTileColsF32) return false;
+  if (!aligned(s.idx_in, 16) || !aligned(s.lut, 16) || (s.y && !aligned(s.y, 16))) return false;
+  if (!s.y || s.acc) return false;
+  if ((int64_t)s.C * kK * s.M * 4 + 1024 >= (1ll << 31)) return false;   // 32-bit buffer offsets
+  TArgs a{};
+  a.idx = s.idx_in; a.lut = s.lut; a.y = s.y;
+  a.N = s.N; a.C = s.C; a.M = s.M;
+  a.Mt = kRowLaneCols;
+  a.RB = 1024;
+  a.ntm = (s.M + kRowLaneCols - 1) / kRowLaneCols;
+  a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
+  if (a.nwork * 4 < device_cus()) return false;
+  a.idx_stride = s.C;
+  a.col_bias = s.col_bias;
+  a.act = s.act == 3 ? 1 : s.act;   // (rows over several tiles) softmax as a second pass
+  int off = kRowLaneLds;
+  if (a.act != 0 && a.col_bias) {
+    a.bias_lds = 1;
+    a.off_bias = off;
+    off += a.ntm * kRowLaneCols * 4;   // zero-padded to whole column tiles
+  }
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  *t = a;
+  return true;
+}
+
 int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   Plan p;
   const int rc = plan(s, &p, single_tile_only);
@@ -451,6 +485,11 @@ bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
 int accumulate(const Shape& s, hipStream_t stream) {
   TArgs t;
   int nj, nw;
+  if (plan_rlane(s, &t)) {
+    const int rc = status_from(launch_rlane_f32(t, device_cus(), stream));
+    if (rc != MADDNESS_OK || t.act == s.act) return rc;
+    return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
+  }
   if (plan_trow(s, &t)) {
     const int rc = status_from(launch_trow(s.elem, t, device_cus(), stream));
     if (rc != MADDNESS_OK || t.act == s.act) return rc;

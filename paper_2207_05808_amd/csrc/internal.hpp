@@ -135,6 +135,16 @@ constexpr int kRowTileCols = 512;
 constexpr int kRowTileColsF32 = 256;
 hipError_t launch_trow(int elem, const TArgs& t, int cus, hipStream_t stream);
 
+// Accumulate with one output row per lane (row_lanes.hip), fp32 tables with C
+// % 16 == 0 and M % 4 == 0: one 1024-thread workgroup per CU, work items of
+// 1024 rows x kRowLaneCols columns, the table staged kRowLaneCT codebooks at a
+// time; idx rows (idx_stride bytes apart, a multiple of 16) must not overlap
+// the outputs.
+constexpr int kRowLaneCols = 64;
+constexpr int kRowLaneCT = 16;
+constexpr int kRowLaneLds = 2 * kRowLaneCT * 16 * (kRowLaneCols * 4 + 16);   // two tile buffers
+hipError_t launch_rlane_f32(const TArgs& t, int cus, hipStream_t stream);
+
 // Fused encode + accumulate streaming rows (fused_rows.hip): int8 tables of
 // exactly 64 codebooks and M <= 512 columns (M % 16 == 0), one 1024-thread
 // workgroup per CU over a contiguous block of rows_per_block rows.

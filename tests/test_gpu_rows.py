@@ -203,6 +203,51 @@ def test_row_layer_output_f32(orc, M, act):
     assert np.all(np.abs(y.astype(np.float64) - ref) <= tol)
 
 
+# --------------------------------------- fp32 tables, one output row per lane
+# The dispatcher takes that kernel for fp32 tables with C % 16 == 0 and at
+# least 256 columns (work items of 1024 rows x 64 columns, 16 codebooks per
+# staged tile), unless the row softmax fits the row-uniform kernel's epilogue
+# (M = 256).  Cases: several work items per workgroup (more items than CUs),
+# a grid that is not a multiple of 8, one codebook tile (C = 16), a ragged
+# last column tile (M % 64 != 0) with the layer outputs, and a last row block
+# of a few rows.
+LANE_CASES = [(32, 1000, 20485), (16, 384, 10241), (256, 1024, 16389), (48, 4100, 2051)]
+
+
+@pytest.mark.parametrize("C,M,N", LANE_CASES)
+def test_lane_accumulate_f32(orc, C, M, N):
+    idx = W.random_indices(N, C, seed=C + M + N)
+    tab = W.random_fp32_table(C, M, seed=7 * C + M)
+    y = host(mdn.lut_accumulate_f32(dev(idx), dev(tab), validate=True))
+    rows = np.unique(np.r_[0:300, N - 300:N, np.random.default_rng(N).integers(0, N, size=700)])
+    assert np.array_equal(y[rows], orc.lut_accumulate_f32(idx[rows], tab))
+
+
+@pytest.mark.parametrize("act", ["bias", "relu", "softmax"])
+def test_lane_layer_output_f32(orc, act):
+    """Bias and ReLU in the epilogue (bias row zero-padded in LDS to whole
+    column tiles: M = 1000), softmax as a second pass."""
+    C, D, M, N = 32, 72, 1000, 20485
+    rng = np.random.default_rng(len(act) + 11)
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
+    thr = rng.standard_normal((C, 15), dtype=np.float32)
+    tab = W.random_fp32_table(C, M, seed=M + 9)
+    bias = rng.standard_normal(M).astype(np.float32)
+    code = {"bias": 1, "relu": 2, "softmax": 3}[act]
+    y = host(mdn.matmul_act_f32(dev(A), dev(split), dev(thr), dev(tab), col_bias=dev(bias), act=act))
+    rows = np.unique(np.r_[0:200, N - 200:N, rng.integers(0, N, size=500)])
+    _, yref = orc.matmul_f32(A[rows], split, thr, tab)
+    ref = orc.sigma(yref, bias, code)
+    got = y[rows].astype(np.float64)
+    if act != "softmax":
+        assert np.array_equal(got, ref)
+        return
+    z = orc.sigma(yref, bias, 1)
+    tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + M + 5) * 2.0 ** -24 * ref + 2.0 ** -120
+    assert np.all(np.abs(got - ref) <= tol)
+
+
 # ------------------------------------------- rounded 8-bit summation (R20)
 # The averaging accumulate at the row counts of the cases above (its kernel
 # keeps one column slice of the table per workgroup and streams row batches):
