@@ -386,6 +386,45 @@ bool plan_rlane(const Shape& s, TArgs* t) {
   return true;
 }
 
+// One output row per lane for int8 tables (row_lanes.hip): y only (no int32
+// sums), the row-uniform kernel's shapes (it is the companion launch, for
+// 32-bit sums) with C % 16 == 0, C >= 32 and 16-byte aligned index rows and
+// table; a row softmax the row-uniform kernel would fuse (M <= 512) stays
+// with that kernel alone.
+bool plan_rlane_i8(const Shape& s, TArgs* t, TArgs* companion) {
+  if (s.elem != kI8 || s.C % kRowLaneCT != 0 || s.C < 2 * kRowLaneCT) return false;
+  if (!s.y || s.acc) return false;   // y only: with the int32 sums too, the row-uniform kernel's stores win
+  if (s.act == 3 && s.M <= kRowTileCols) return false;
+  if (!aligned(s.idx_in, 16) || !aligned(s.lut, 16)) return false;
+  TArgs r;
+  if (!plan_trow(s, &r)) return false;
+  TArgs a{};
+  a.idx = s.idx_in; a.lut = s.lut; a.scale = s.scale; a.offset = s.offset; a.y = s.y; a.acc = s.acc;
+  a.N = s.N; a.C = s.C; a.M = s.M;
+  a.Mt = kRowLaneColsI8;
+  a.RB = 1024;
+  a.ntm = (s.M + kRowLaneColsI8 - 1) / kRowLaneColsI8;
+  a.nwork = (int64_t)a.ntm * ((s.N + a.RB - 1) / a.RB);
+  if (a.nwork * 4 < device_cus()) return false;
+  a.idx_stride = s.C;
+  a.col_bias = s.col_bias;
+  a.act = r.act;   // 1 for a softmax over rows of several tiles (then a second pass), as there
+  int off = kRowLaneLds;
+  auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
+  a.off_sh = take(s.C * 4);
+  a.off_misc = take(16);
+  if (a.act != 0 && a.col_bias) {
+    a.bias_lds = 1;
+    a.off_bias = take(a.ntm * kRowLaneColsI8 * 4);   // zero-padded to whole column tiles
+  }
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  r.only_wide = 1;   // does the call only when the 16-bit field sums do not fit
+  *t = a;
+  *companion = r;
+  return true;
+}
+
 int run(const Shape& s, bool single_tile_only, hipStream_t stream) {
   Plan p;
   const int rc = plan(s, &p, single_tile_only);
@@ -487,6 +526,13 @@ int accumulate(const Shape& s, hipStream_t stream) {
   int nj, nw;
   if (plan_rlane(s, &t)) {
     const int rc = status_from(launch_rlane_f32(t, device_cus(), stream));
+    if (rc != MADDNESS_OK || t.act == s.act) return rc;
+    return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
+  }
+  TArgs wide;
+  if (plan_rlane_i8(s, &t, &wide)) {
+    int rc = status_from(launch_rlane_i8(t, device_cus(), stream));
+    if (rc == MADDNESS_OK) rc = status_from(launch_trow(kI8, wide, device_cus(), stream));
     if (rc != MADDNESS_OK || t.act == s.act) return rc;
     return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
   }

@@ -144,6 +144,11 @@ constexpr int kRowLaneCols = 64;
 constexpr int kRowLaneCT = 16;
 constexpr int kRowLaneLds = 2 * kRowLaneCT * 16 * (kRowLaneCols * 4 + 16);   // two tile buffers
 hipError_t launch_rlane_f32(const TArgs& t, int cus, hipStream_t stream);
+// int8 tables with C % 16 == 0, C >= 32, M % 16 == 0: work items of 1024 rows x
+// kRowLaneColsI8 columns; the launch does nothing unless the 16-bit field sums
+// fit (the row-uniform kernel with only_wide set then does the other case).
+constexpr int kRowLaneColsI8 = 128;
+hipError_t launch_rlane_i8(const TArgs& t, int cus, hipStream_t stream);
 
 // Fused encode + accumulate streaming rows (fused_rows.hip): int8 tables of
 // exactly 64 codebooks and M <= 512 columns (M % 16 == 0), one 1024-thread

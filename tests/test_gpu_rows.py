@@ -149,6 +149,79 @@ def test_row_layer_output_bias_placement(orc, M, act, bias_off):
     assert np.array_equal(y.astype(np.float64), orc.sigma(yref, bias, code))
 
 
+# ---------------------------------- int8 tables, one output row per lane (y)
+# Calls that want y only (no int32 sums) take that kernel when C % 16 == 0
+# and C >= 32 within the row-uniform kernel's shapes; it does nothing when
+# the 16-bit field sums do not fit, and the row-uniform kernel launched after
+# it (which otherwise does nothing) then sums in int32.  Each workgroup keeps
+# one 128-column tile and streams row blocks; from 4 row blocks per workgroup
+# on, its wavefronts start at different codebook tiles.  Below 128 codebooks
+# the outputs go through a quad transpose before the stores.  Cases: both
+# store forms with and without the phases, C = 32 (two tiles per cycle), a
+# ragged last row block and last column tile, the field bound exactly, sums
+# that need int32, and the layer outputs.
+def check_y(orc, idx, lut, scale, offset, rows=None):
+    _, y = mdn.lut_accumulate(dev(idx), dev(lut), dev(scale), dev(offset), want_acc=False, validate=True)
+    N = idx.shape[0]
+    if rows is None:
+        rows = np.unique(np.r_[0:300, N - 300:N, np.random.default_rng(N).integers(0, N, size=600)])
+    got = y[torch.from_numpy(rows).to(DEV)]
+    _, ry = orc.lut_accumulate(idx[rows], lut, scale, offset)
+    assert np.array_equal(host(got), ry)
+
+
+# (C, M, N, max_shift): phases need N >= 4 row blocks of 1024 x the workgroups per column tile
+LANE_I8_CASES = [(64, 512, 262144 + 333, 1), (64, 512, 20485, 2), (128, 4096, 32768 + 1500, 1), (256, 1024, 131072 + 7, 0),
+                 (32, 1008, 131072 + 65, 3), (48, 2048, 40961, 1)]
+
+
+@pytest.mark.parametrize("C,M,N,max_shift", LANE_I8_CASES)
+def test_lane_accumulate_i8(orc, C, M, N, max_shift):
+    idx = W.random_indices(N, C, seed=C + M + N)
+    lut, scale, offset = W.random_codes(C, M, seed=3 * C + M, max_shift=max_shift)
+    check_y(orc, idx, lut, scale, offset)
+
+
+@pytest.mark.parametrize("code", [127, -128])
+@pytest.mark.parametrize("shifts", [(7, 6, 1, 1, 1), (7, 6, 1, 1, 2)])
+def test_lane_accumulate_i8_field_bound(orc, code, shifts):
+    """sum 2^sh = 257 exactly (every field at 65535 or 0), and 258, the
+    first sum that takes the row-uniform kernel's int32 sums."""
+    C, M, N = 64, 512, 262144 + 5
+    sh = np.array(list(shifts) + [0] * (C - len(shifts)), dtype=np.int32)
+    idx = W.random_indices(N, C, seed=int(sh.sum()) + code + 300)
+    lut = np.full((C, 16, M), code, dtype=np.int8)
+    lut[:, 5, ::3] = -code if code != -128 else 127
+    scale = np.ldexp(np.float32(1.0), sh - 9).astype(np.float32)
+    offset = np.random.default_rng(5).standard_normal(C).astype(np.float32)
+    check_y(orc, idx, lut, scale, offset)
+
+
+@pytest.mark.parametrize("act", ["bias", "relu", "softmax"])
+def test_lane_layer_output_i8(orc, act):
+    """Bias and ReLU in the epilogue (the workgroup's 128 column biases in
+    LDS, M = 1008: a ragged last column tile), softmax as a second pass."""
+    C, D, M, N = 64, 72, 1008, 65536 + 123
+    rng = np.random.default_rng(len(act) + 21)
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
+    thr = rng.standard_normal((C, 15), dtype=np.float32)
+    lut, scale, offset = W.random_codes(C, M, seed=M + 3, max_shift=1)
+    bias = rng.standard_normal(M).astype(np.float32)
+    code = {"bias": 1, "relu": 2, "softmax": 3}[act]
+    y = mdn.matmul_act(dev(A), dev(split), dev(thr), dev(lut), dev(scale), dev(offset), col_bias=dev(bias), act=act)
+    rows = np.unique(np.r_[0:200, N - 200:N, rng.integers(0, N, size=500)])
+    got = host(y[torch.from_numpy(rows).to(DEV)]).astype(np.float64)
+    _, _, yref = orc.matmul(A[rows], split, thr, lut, scale, offset)
+    ref = orc.sigma(yref, bias, code)
+    if act != "softmax":
+        assert np.array_equal(got, ref)
+        return
+    z = orc.sigma(yref, bias, 1)
+    tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + M + 5) * 2.0 ** -24 * ref + 2.0 ** -120
+    assert np.all(np.abs(got - ref) <= tol)
+
+
 # ------------------------------------------------------------- fp32 tables
 def rows_for_f32(M):
     """Rows that reach the fp32 row-uniform kernel: 64 work items of 256 rows
