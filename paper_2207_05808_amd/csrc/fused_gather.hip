@@ -247,9 +247,8 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
   if (!vec_all) {
     // general staging (tables larger than the up-front units, or rows that are
     // not whole 16-byte units): 8 LDS dwords per thread per round, all global
-    // loads of a round issued first; columns padded to octets with zeros.  A
-    // codebook's shift comes from the lane that holds it (no barrier: the
-    // rounds are uniform, so every lane takes part in each shuffle)
+    // loads of a round issued first; columns padded to octets with zeros
+    __syncthreads();   // shifts visible
     const int wpr = (ELEM == kF32) ? 8 * no : (narrow ? 4 * no : 2 * no);  // dwords per LDS row
     int wlog = 0;
     while ((1 << wlog) < wpr) ++wlog;
@@ -257,8 +256,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
     const int8_t* q8 = reinterpret_cast<const int8_t*>(g.lut);
     const float* qf = reinterpret_cast<const float*>(g.lut);
     const int64_t last = (int64_t)rows * M - 1;
-    for (int base0 = 0; base0 < total; base0 += 8 * blockDim.x) {
-      const int base = base0 + tid;
+    for (int base = tid; base < total; base += 8 * blockDim.x) {
       uint32_t v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -281,13 +279,13 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
       for (int j = 0; j < 8; ++j) {
         const int u = base + j * blockDim.x;
         const int row = u >> wlog, w = u & ((1 << wlog) - 1);
-        const int shr = __shfl(sh, min(row >> 4, C - 1));   // lane row / 16 holds that codebook's shift
         if (u >= total || w >= wpr) continue;
         uint32_t xx = 0;
         if (row < rows) {
           if (ELEM == kF32) {
             xx = w < M ? v[j] : 0u;
           } else if (narrow) {
+            const int shr = s_shc[row >> 4];
             const int m = 2 * w;
             const int lo = m < M ? ((int)(int8_t)(v[j] & 0xffu) << shr) : 0;
             const int hi = m + 1 < M ? ((int)(int8_t)(v[j] >> 8) << shr) : 0;
@@ -482,7 +480,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
           if (qd >= nq4) continue;
           const int mh = 4 * qd;
           if (g.vec_out && mh + 4 <= M) {
-            if (g.y)
+            if (!IDX || g.y)   // (y is required unless the indices are given)
               __builtin_nontemporal_store((f32x4g){o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]},
                                           reinterpret_cast<f32x4g*>(yrow + mh));
             if (arow)
@@ -493,7 +491,7 @@ __global__ void __launch_bounds__(1024) gfused_kernel(const GArgs g) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               if (mh + e < M) {
-                if (g.y) yrow[mh + e] = o[4 * h + e];
+                if (!IDX || g.y) yrow[mh + e] = o[4 * h + e];
                 if (arow) arow[mh + e] = iacc[u][4 * h + e];
               }
           }
