@@ -25,6 +25,8 @@
 //      with 16-byte non-temporal stores.
 #include "internal.hpp"
 
+#include <climits>
+
 #include <atomic>
 #include <mutex>
 
@@ -46,6 +48,25 @@ __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirs
 
 // Exponent of a normal fp32 power of two: scale = 2^e.
 __device__ __forceinline__ int exp_of_bits(uint32_t bits) { return (int)((bits >> 23) & 0xffu) - 127; }
+
+// Minimum and maximum over the 64 lanes of a wavefront (the same value in
+// every lane): DPP exchanges within each row of 16 lanes (quad butterflies,
+// then rotations by 4 and 8), then the four row results through readlane.
+// (__shfl_xor compiles to ds_bpermute with a wait on each step.)
+__device__ __forceinline__ void wave_minmax(int& lo, int& hi) {
+#define MDN_MINMAX_STEP(CTRL)                                              \
+  lo = min(lo, __builtin_amdgcn_update_dpp(lo, lo, CTRL, 0xf, 0xf, false)); \
+  hi = max(hi, __builtin_amdgcn_update_dpp(hi, hi, CTRL, 0xf, 0xf, false));
+  MDN_MINMAX_STEP(0xB1)    // quad_perm [1, 0, 3, 2]
+  MDN_MINMAX_STEP(0x4E)    // quad_perm [2, 3, 0, 1]
+  MDN_MINMAX_STEP(0x124)   // row_ror 4
+  MDN_MINMAX_STEP(0x128)   // row_ror 8
+#undef MDN_MINMAX_STEP
+  lo = min(min(__builtin_amdgcn_readlane(lo, 0), __builtin_amdgcn_readlane(lo, 16)),
+           min(__builtin_amdgcn_readlane(lo, 32), __builtin_amdgcn_readlane(lo, 48)));
+  hi = max(max(__builtin_amdgcn_readlane(hi, 0), __builtin_amdgcn_readlane(hi, 16)),
+           max(__builtin_amdgcn_readlane(hi, 32), __builtin_amdgcn_readlane(hi, 48)));
+}
 
 __device__ __forceinline__ uint32_t bfe(uint32_t v, int off, int width) {
   return __builtin_amdgcn_ubfe(v, off, width);
@@ -252,104 +273,7 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   lds_i32* s_sh = reinterpret_cast<lds_i32*>(smem + a.L.sh);
   lds_t* s_shp = smem + a.L.shp;
 
-  // ---------------- workgroup prologue ----------------
-  // Table staging: 8 LDS dwords per thread per round with every global load
-  // issued first (clamped addresses, masked afterwards), so a round costs one
-  // memory latency instead of eight.
-  if (kAcc) {
-    const int rows = C * kK;
-    const int wpr = (ELEM == kI8) ? nq : 4 * nq;   // LDS dwords per table row
-    int wlog = 0;
-    while ((1 << wlog) < wpr) ++wlog;
-    const int total = rows << wlog;
-    const int8_t* q8 = reinterpret_cast<const int8_t*>(a.lut);
-    const float* qf = reinterpret_cast<const float*>(a.lut);
-    const int64_t last = (int64_t)rows * a.M - 1;
-    for (int base = tid; base < total; base += 8 * blockDim.x) {
-      uint32_t v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int u = base + j * blockDim.x;
-        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
-        const int64_t e0 = (int64_t)row * a.M + m0;
-        if (ELEM == kF32) {
-          v[j] = __float_as_uint(qf[min(e0 + w, last)]);
-        } else if (a.vec_out) {   // M % 4 == 0, aligned: whole dwords
-          v[j] = *reinterpret_cast<const uint32_t*>(q8 + min(e0 + 4 * w, last - 3));
-        } else {
-          uint32_t x = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) x |= (uint32_t)(uint8_t)q8[min(e0 + 4 * w + e, last)] << (8 * e);
-          v[j] = x;
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int u = base + j * blockDim.x;
-        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
-        if (u >= total || w >= wpr) continue;
-        uint32_t x;
-        if (ELEM == kF32) {
-          x = w < mt ? v[j] : 0u;
-        } else {
-          x = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (4 * w + e < mt) x |= v[j] & (0xffu << (8 * e));
-        }
-        *reinterpret_cast<lds_u32*>(s_lut + row * a.lut_rs + 4 * w) = x;
-      }
-    }
-  }
-  if (kEnc) {
-    // node-major [16][C] thresholds and level-major [4][C] split columns:
-    // lanes walking consecutive codebooks read consecutive banks at any node
-    for (int u = tid; u < C * 16; u += blockDim.x) {
-      const int c = u >> 4, j = u & 15;
-      s_thr[j * C + c] = (j < kNodes) ? a.thr[c * kNodes + j] : 0.0f;
-    }
-    for (int u = tid; u < C * kLevels; u += blockDim.x) {
-      const unsigned sp = (unsigned)a.split[u];
-      s_split[(u & 3) * C + (u >> 2)] = (int)min(sp, (unsigned)(a.D - 1));  // memory safety only
-    }
-  }
-  if (kAcc && ELEM == kI8) {
-    if (tid == 0) { s_misc[0] = 1 << 30; s_misc[1] = 0; }
-    __syncthreads();
-    const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
-    for (int c = tid; c < C; c += blockDim.x) atomicMin((int*)&s_misc[0], exp_of_bits(sb[c]));
-    __syncthreads();
-    const int emin = s_misc[0];
-    for (int c = tid; c < C; c += blockDim.x) {
-      const int sh = exp_of_bits(sb[c]) - emin;
-      s_sh[c] = sh;
-      atomicMax((int*)&s_misc[1], sh);
-    }
-    if (wave == 0) {
-      // bias32: double sum over codebooks in ascending order, 64 offsets per
-      // coalesced load, summed in order through readlane (all lanes alike)
-      double sum = 0.0;
-      for (int j0 = 0; j0 < C; j0 += 64) {
-        const float ov = a.offset[min(j0 + lane, C - 1)];
-        const int n = min(64, C - j0);
-        for (int l = 0; l < n; ++l) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), l));
-      }
-      if (lane == 0) {
-        s_misc[2] = __float_as_int((float)sum);
-        s_misc[3] = __float_as_int(__builtin_ldexpf(1.0f, emin));
-      }
-    }
-    __syncthreads();
-    // shifts packed as nibbles, 8 codebooks per dword (used while every shift <= 6)
-    for (int g = tid; g < (C + 7) / 8; g += blockDim.x) {
-      uint32_t w = 0;
-      for (int b = 0; b < 8 && 8 * g + b < C; ++b) w |= (uint32_t)(min(s_sh[8 * g + b], 15)) << (4 * b);
-      *reinterpret_cast<lds_u32*>(s_shp + 4 * g) = w;
-    }
-  }
-  __syncthreads();
-
-  // ---------------- per-wavefront chunk loop ----------------
+  // ---------------- the first chunk's rows, in flight during the prologue
   const int RW = a.RW;
   lds_t* sA = smem + a.L.a + wave * a.L.a_wave;
   lds_t* sI = smem + a.L.idx + wave * a.L.idx_wave;
@@ -369,6 +293,160 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     }
   }
 
+  // the first round of the parameter loads below, issued before anything waits
+  const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
+  float thr0 = 0.0f, off0 = 0.0f;
+  int split0 = 0;
+  uint32_t sb0 = 0u;
+  if (kEnc) {
+    if (tid < C * 16 && (tid & 15) < kNodes) thr0 = a.thr[(tid >> 4) * kNodes + (tid & 15)];
+    if (tid < C * kLevels) split0 = a.split[tid];
+  }
+  if (kAcc && ELEM == kI8) {
+    sb0 = sb[min(lane, C - 1)];
+    if (wave == 0) off0 = a.offset[min(lane, C - 1)];
+  }
+
+  // ---------------- workgroup prologue ----------------
+  // Table staging: 8 LDS dwords per thread per round with every global load
+  // issued first (clamped addresses, masked afterwards), so a round costs one
+  // memory latency instead of eight.
+  if (kAcc) {
+    const int rows = C * kK;
+    const int wpr = (ELEM == kI8) ? nq : 4 * nq;   // LDS dwords per table row
+    int wlog = 0;
+    while ((1 << wlog) < wpr) ++wlog;
+    const int total = rows << wlog;
+    const int8_t* q8 = reinterpret_cast<const int8_t*>(a.lut);
+    const float* qf = reinterpret_cast<const float*>(a.lut);
+    const int64_t last = (int64_t)rows * a.M - 1;
+    // one round: 8 LDS dwords per thread, starting at element `base`
+    auto stage_round = [&](int base) {
+      uint32_t v[8];
+      // (one branch around each whole round, so that its loads are issued back
+      // to back: a branch per element made the compiler wait after each one)
+      auto e0_of = [&](int j, int& w) {
+        const int u = base + j * blockDim.x;
+        const int row = u >> wlog;
+        w = u & ((1 << wlog) - 1);
+        return (int64_t)row * a.M + m0;
+      };
+      if (ELEM == kF32) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          int w;
+          const int64_t e0 = e0_of(j, w);
+          v[j] = __float_as_uint(qf[min(e0 + w, last)]);
+        }
+      } else if (a.vec_out) {   // M % 4 == 0, aligned: whole dwords
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          int w;
+          const int64_t e0 = e0_of(j, w);
+          v[j] = *reinterpret_cast<const uint32_t*>(q8 + min(e0 + 4 * w, last - 3));
+        }
+      } else {
+        uint32_t b[8][4];   // every byte of the round requested before any is used
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          int w;
+          const int64_t e0 = e0_of(j, w);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) b[j][e] = (uint8_t)q8[min(e0 + 4 * w + e, last)];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = b[j][0] | (b[j][1] << 8) | (b[j][2] << 16) | (b[j][3] << 24);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int u = base + j * blockDim.x;
+        const int row = u >> wlog, w = u & ((1 << wlog) - 1);
+        if (u >= total || w >= wpr) continue;
+        uint32_t x;
+        if (ELEM == kF32) {
+          x = w < mt ? v[j] : 0u;
+        } else {
+          x = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (4 * w + e < mt) x |= v[j] & (0xffu << (8 * e));
+        }
+        *reinterpret_cast<lds_u32*>(s_lut + row * a.lut_rs + 4 * w) = x;
+      }
+    };
+    // (the first round outside the loop, as straight-line code: at a loop
+    // header the compiler's wait analysis waited for every load in flight,
+    // the first chunk's rows included, before the table's loads were issued)
+    if (tid < total) stage_round(tid);
+    for (int base = tid + 8 * blockDim.x; base < total; base += 8 * blockDim.x) stage_round(base);
+  }
+  if (kEnc) {
+    // node-major [16][C] thresholds and level-major [4][C] split columns:
+    // lanes walking consecutive codebooks read consecutive banks at any node
+    // (the first round from the registers loaded at entry, the rest from memory)
+    if (tid < C * 16) s_thr[(tid & 15) * C + (tid >> 4)] = thr0;
+    for (int u = tid + blockDim.x; u < C * 16; u += blockDim.x) {
+      const int c = u >> 4, j = u & 15;
+      s_thr[j * C + c] = (j < kNodes) ? a.thr[c * kNodes + j] : 0.0f;
+    }
+    if (tid < C * kLevels) s_split[(tid & 3) * C + (tid >> 2)] = (int)min((unsigned)split0, (unsigned)(a.D - 1));
+    for (int u = tid + blockDim.x; u < C * kLevels; u += blockDim.x) {
+      const unsigned sp = (unsigned)a.split[u];
+      s_split[(u & 3) * C + (u >> 2)] = (int)min(sp, (unsigned)(a.D - 1));  // memory safety only
+    }
+  }
+  // block exponents: every wavefront reduces e_min and the largest shift over
+  // the scales itself (no barrier); wave 0 also sums the offsets
+  int emin = 0, maxsh = 0;
+  if (kAcc && ELEM == kI8) {
+    int lo = INT_MAX, hi = INT_MIN;
+    if (lane < C) lo = hi = exp_of_bits(sb0);
+    for (int c = lane + 64; c < C; c += 64) {
+      const int e = exp_of_bits(sb[c]);
+      lo = min(lo, e);
+      hi = max(hi, e);
+    }
+    wave_minmax(lo, hi);
+    emin = lo;
+    maxsh = hi - emin;
+    if (wave == 0 && lane < C) s_sh[lane] = exp_of_bits(sb0) - emin;
+    for (int c = tid + 64; c < C; c += blockDim.x) s_sh[c] = exp_of_bits(sb[c]) - emin;
+    // shifts packed as nibbles, 8 codebooks per dword (used while every shift
+    // <= 6): up to 64 codebooks from wave 0's registers (an OR over each 8
+    // lanes, every lane taking part), more from memory
+    if (C <= 64) {
+      if (wave == 0) {
+        // (DPP: quad butterflies, then lane 8k + 4 takes lane 8k's quad by a
+        // row shift, so it holds the OR of lanes 8k .. 8k + 7)
+        uint32_t w = lane < C ? (uint32_t)min(exp_of_bits(sb0) - emin, 15) << (4 * (lane & 7)) : 0u;
+        w |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, 0xB1, 0xf, 0xf, true);
+        w |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, 0x4E, 0xf, 0xf, true);
+        w |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, 0x114, 0xf, 0xf, true);   // row_shr 4
+        if ((lane & 7) == 4 && lane - 4 < C) *reinterpret_cast<lds_u32*>(s_shp + 4 * (lane >> 3)) = w;
+      }
+    } else {
+      for (int g = tid; g < (C + 7) / 8; g += blockDim.x) {
+        uint32_t w = 0;
+        for (int b = 0; b < 8 && 8 * g + b < C; ++b) w |= (uint32_t)min(exp_of_bits(sb[8 * g + b]) - emin, 15) << (4 * b);
+        *reinterpret_cast<lds_u32*>(s_shp + 4 * g) = w;
+      }
+    }
+    if (wave == 0) {
+      // bias32: double sum over codebooks in ascending order, 64 offsets per
+      // coalesced load, summed in order through readlane (all lanes alike)
+      double sum = 0.0;
+      for (int j0 = 0; j0 < C; j0 += 64) {
+        const float ov = j0 == 0 ? off0 : a.offset[min(j0 + lane, C - 1)];
+        const int n = min(64, C - j0);
+        for (int l = 0; l < n; ++l) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), l));
+      }
+      if (lane == 0) s_misc[2] = __float_as_int((float)sum);
+    }
+  }
+  __syncthreads();
+
+  // ---------------- per-wavefront chunk loop ----------------
   // accumulate-phase lane mapping
   const int lpr_log2 = 6 - a.rw_log2;
   const int ar = lane >> lpr_log2;                  // row of the chunk
@@ -397,12 +475,10 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     sc2 = s_split[2 * C + cl];
     sc3 = s_split[3 * C + cl];
   }
-  int maxsh = 0;
   float step = 1.0f, bias = 0.0f;
   if (kAcc && ELEM == kI8) {
-    maxsh = uniform(s_misc[1]);
     bias = __int_as_float(uniform(s_misc[2]));
-    step = __int_as_float(uniform(s_misc[3]));
+    step = __builtin_ldexpf(1.0f, emin);
   }
 
   for (; ch < a.nchunks; ch += tw) {
