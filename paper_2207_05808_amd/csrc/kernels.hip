@@ -26,6 +26,7 @@
 #include "internal.hpp"
 
 #include <climits>
+#include <type_traits>
 
 #include <atomic>
 #include <mutex>
@@ -34,6 +35,7 @@ namespace mdn {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32_ua __attribute__((aligned(1)));   // a dword at any byte address
 #define MDN_CONST __attribute__((address_space(4)))
 typedef __attribute__((address_space(3))) char lds_t;           // 32-bit LDS addresses
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
@@ -86,11 +88,15 @@ struct Prefetch {
   int rrow[PF > 0 ? PF : 1];   // row within the chunk (0 when idle)
 
   __device__ __forceinline__ void init(int lane, int rw, int upr, int64_t src_rs, int lds_rs, int dummy) {
+    // u / upr as (u + 1/2) * rcp(upr), truncated: the product is within
+    // (u + 1/2) * 2^-21 of (u + 1/2) / upr, which lies at least 1/(2 upr) from
+    // every integer, so the truncation is exact for u < 2^20
+    const float rcp = __builtin_amdgcn_rcpf((float)upr);
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
       const int u = lane + 64 * j;
       const bool live = u < rw * upr;
-      const int r = live ? u / upr : 0;
+      const int r = live ? (int)(((float)u + 0.5f) * rcp) : 0;
       const int col = live ? u - r * upr : 0;
       goff[j] = (int)(r * src_rs) + col * 16;
       loff[j] = live ? r * lds_rs + col * 16 : dummy;
@@ -257,6 +263,21 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   lds_t* smem = (lds_t*)smem_raw;
 
+  // The argument block lives in memory; read where first used, its fields
+  // arrive in several dependent scalar-load rounds ahead of the first data
+  // load.  Pinning them all here issues every scalar load at once and waits
+  // once.
+#define MDN_PIN(x) asm volatile("" ::"s"(x))
+  MDN_PIN(a.A); MDN_PIN(a.idx_in); MDN_PIN(a.split); MDN_PIN(a.thr); MDN_PIN(a.lut);
+  MDN_PIN(a.scale); MDN_PIN(a.offset); MDN_PIN(a.y); MDN_PIN(a.acc); MDN_PIN(a.idx_out);
+  MDN_PIN(a.N); MDN_PIN(a.lda); MDN_PIN(a.D); MDN_PIN(a.C); MDN_PIN(a.M); MDN_PIN(a.Mt);
+  MDN_PIN(a.lut_rs); MDN_PIN(a.Dp); MDN_PIN(a.Cp); MDN_PIN(a.RW); MDN_PIN(a.rw_log2);
+  MDN_PIN(a.nchunks); MDN_PIN(a.c_magic); MDN_PIN(a.vec_out); MDN_PIN(a.enc_reg); MDN_PIN(a.c_log2);
+  MDN_PIN(a.L.lut); MDN_PIN(a.L.thr); MDN_PIN(a.L.split); MDN_PIN(a.L.misc); MDN_PIN(a.L.sh);
+  MDN_PIN(a.L.shp); MDN_PIN(a.L.a); MDN_PIN(a.L.a_wave); MDN_PIN(a.L.idx); MDN_PIN(a.L.idx_wave);
+  MDN_PIN(blockDim.x); MDN_PIN(gridDim.x);
+#undef MDN_PIN
+
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);   // wavefront-uniform: loop control stays scalar
@@ -320,9 +341,10 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
     const int8_t* q8 = reinterpret_cast<const int8_t*>(a.lut);
     const float* qf = reinterpret_cast<const float*>(a.lut);
     const int64_t last = (int64_t)rows * a.M - 1;
-    // one round: 8 LDS dwords per thread, starting at element `base`
-    auto stage_round = [&](int base) {
-      uint32_t v[8];
+    // one round: NJ LDS dwords per thread, starting at element `base`
+    auto stage_round = [&](int base, auto nj_tag) {
+      constexpr int NJ = decltype(nj_tag)::value;
+      uint32_t v[NJ];
       // (one branch around each whole round, so that its loads are issued back
       // to back: a branch per element made the compiler wait after each one)
       auto e0_of = [&](int j, int& w) {
@@ -333,33 +355,26 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
       };
       if (ELEM == kF32) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < NJ; ++j) {
           int w;
           const int64_t e0 = e0_of(j, w);
           v[j] = __float_as_uint(qf[min(e0 + w, last)]);
         }
-      } else if (a.vec_out) {   // M % 4 == 0, aligned: whole dwords
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          int w;
-          const int64_t e0 = e0_of(j, w);
-          v[j] = *reinterpret_cast<const uint32_t*>(q8 + min(e0 + 4 * w, last - 3));
-        }
       } else {
-        uint32_t b[8][4];   // every byte of the round requested before any is used
+        // four columns per load, unaligned when M % 4 != 0 (the memory system
+        // serves unaligned dwords); a dword that would run past the table is
+        // read from its last four bytes and shifted down
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < NJ; ++j) {
           int w;
-          const int64_t e0 = e0_of(j, w);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) b[j][e] = (uint8_t)q8[min(e0 + 4 * w + e, last)];
+          const int64_t e = e0_of(j, w) + 4 * w;
+          const int64_t p = min(e, last - 3);
+          const int sh = (int)min<int64_t>(e - p, 3);
+          v[j] = *reinterpret_cast<const u32_ua*>(q8 + p) >> (8 * sh);
         }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = b[j][0] | (b[j][1] << 8) | (b[j][2] << 16) | (b[j][3] << 24);
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < NJ; ++j) {
         const int u = base + j * blockDim.x;
         const int row = u >> wlog, w = u & ((1 << wlog) - 1);
         if (u >= total || w >= wpr) continue;
@@ -367,19 +382,23 @@ __global__ void __launch_bounds__(512) path_kernel(const KArgs a) {
         if (ELEM == kF32) {
           x = w < mt ? v[j] : 0u;
         } else {
-          x = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (4 * w + e < mt) x |= v[j] & (0xffu << (8 * e));
+          const int live = min(mt - 4 * w, 4);   // columns of this dword inside the tile
+          x = live >= 4 ? v[j] : v[j] & ((1u << (8 * live)) - 1u);
         }
         *reinterpret_cast<lds_u32*>(s_lut + row * a.lut_rs + 4 * w) = x;
       }
     };
     // (the first round outside the loop, as straight-line code: at a loop
     // header the compiler's wait analysis waited for every load in flight,
-    // the first chunk's rows included, before the table's loads were issued)
-    if (tid < total) stage_round(tid);
-    for (int base = tid + 8 * blockDim.x; base < total; base += 8 * blockDim.x) stage_round(base);
+    // the first chunk's rows included, before the table's loads were issued;
+    // a table of at most one dword per thread takes a one-load round)
+    if (total <= (int)blockDim.x) {
+      if (tid < total) stage_round(tid, std::integral_constant<int, 1>());
+    } else {
+      if (tid < total) stage_round(tid, std::integral_constant<int, 8>());
+      for (int base = tid + 8 * blockDim.x; base < total; base += 8 * blockDim.x)
+        stage_round(base, std::integral_constant<int, 8>());
+    }
   }
   if (kEnc) {
     // node-major [16][C] thresholds and level-major [4][C] split columns:
