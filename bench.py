@@ -186,6 +186,40 @@ def region_us(fn, stream, reps=20, warm=3):
     return r0.elapsed_time(r1) / reps * 1e3
 
 
+def repeat_us(fn, stream, reps, blocks=5):
+    """Minimum and median over `blocks` repeats of the average duration of one
+    call of fn(i) in `reps` back-to-back calls (one event pair per repeat: an
+    event pair around every call would add its own overhead to each)."""
+    import torch
+    d = []
+    for _ in range(blocks):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(reps):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        d.append(a.elapsed_time(b) * 1e3 / reps)
+    d.sort()
+    return d[0], float(np.median(d))
+
+
+def copy_peak_gbs(dev, mb=512, reps=10):
+    """Device-to-device copy rate of an mb-MiB buffer (bytes read + written per
+    second): a measured practical peak of the HBM beside the published one."""
+    import torch
+    src = torch.ones((mb << 20) // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream()
+    us = region_us(lambda i: dst.copy_(src), stream, reps=reps, warm=3)
+    del src, dst
+    return 2.0 * (mb << 20) / (us * 1e-6) / 1e9
+
+
+WARM_SECONDS = 0.2   # minimum warm-up of each workload block
+
+
 def workload_block(name, steps, warmup, sample_n=2048):
     """Compact measurement of one workload's step (the fused entry point over
     all its rows, inputs resident): rows/s, step time, HBM fraction of the
@@ -212,8 +246,14 @@ def workload_block(name, steps, warmup, sample_n=2048):
     else:
         lut = mdn.build_lut_f32(Pd, Bd)
         call = mdn.prepare_matmul_f32(A, split, thr, lut, y_out=y)
-    for _ in range(warmup):
+    # warm-up by time as well as by count: a millisecond-long step runs ~10%
+    # slower for the first ~50 ms of sustained work
+    n_warm, tw0 = 0, time.perf_counter()
+    while n_warm < warmup or time.perf_counter() - tw0 < WARM_SECONDS:
         call()
+        n_warm += 1
+        if n_warm % 8 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -229,7 +269,7 @@ def workload_block(name, steps, warmup, sample_n=2048):
     out = {"N": N, "D": spec.D, "C": spec.C, "M": spec.M, "table": "int8" if spec.quantized else "fp32",
            "rows_per_s": round(N / wall, 1), "step_us": round(step_s * 1e6, 2),
            "wall_us_per_step": round(wall * 1e6, 2), "algorithmic_bytes": abytes,
-           "hbm_frac": round(abytes / step_s / 1e9 / HBM_PEAK_GBS, 4), "steps": steps}
+           "hbm_frac": round(abytes / step_s / 1e9 / HBM_PEAK_GBS, 4), "steps": steps, "warmup": n_warm}
     if mdn.matmul_index_bytes(A, spec.C, spec.M, f32=not spec.quantized) > 0:
         idx = torch.empty((N, spec.C), dtype=torch.uint8, device=dev)
         enc_us = region_us(lambda i: mdn.encode(A, split, thr, idx_out=idx), stream, reps=5, warm=1)
@@ -352,6 +392,11 @@ def main():
     parity = parity_report(p, y_host, np.arange(N) if N <= 200000 else sampled_rows(N))
     del y_host
 
+    # after the timed region: minimum and median over five more repeats of the
+    # K launches, and the copy-rate peak
+    k_min, k_med = repeat_us(step, stream, K)
+    copy_gbs = copy_peak_gbs(dev)
+
     abytes = algorithmic_bytes(spec, N)
     achieved = abytes / avg_kern_s / 1e9
     kh = kernel_source_hash()
@@ -360,6 +405,8 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes": abytes, "kernel_us": round(avg_kern_s * 1e6, 2),
+                "kernel_us_min": round(k_min, 2), "kernel_us_median": round(k_med, 2),
+                "copy_peak": round(copy_gbs, 1), "frac_of_copy_peak": round(achieved / copy_gbs, 4),
                 "kernel": ("gfused_kernel<int8> (maddness_matmul, one launch per step)" if headline else
                            "whole step (maddness_matmul%s: encode + accumulate launches)"
                            % ("" if spec.quantized else "_f32")),
