@@ -163,3 +163,29 @@ def test_sweep_misaligned(orc, seed):
     tab = W.random_fp32_table(C, M, seed=9500 + seed)
     y = mdn.lut_accumulate_f32(idxd, shifted(tab, torch.float32), y_out=y_out)
     assert np.array_equal(host(y), orc.lut_accumulate_f32(idx, tab))
+
+
+@pytest.mark.parametrize("M", [1, 3, 10, 12, 33])
+@pytest.mark.parametrize("off", [0, 1, 2, 3])
+def test_general_kernel_table_at_any_byte_offset(orc, M, off):
+    """Small layers whose table rows are not whole 16-byte units run the
+    general single-launch kernel, which reads the int8 table one dword per
+    four columns at any byte alignment (the table's last dword shifted down
+    from its last four bytes).  Tables placed 0-3 bytes past an allocation,
+    ragged N over several chunks: indices, accumulators and outputs
+    bit-exact."""
+    rng = np.random.default_rng(7100 + 10 * M + off)
+    C, D, N = 4, 64, 4100 + M
+    A = rng.standard_normal((N, D), dtype=np.float32)
+    split = rng.integers(0, D, size=(C, 4)).astype(np.int32)
+    thr = rng.standard_normal((C, 15), dtype=np.float32)
+    lut, scale, offset = W.random_codes(C, M, seed=7200 + M, max_shift=3)
+    flat = torch.empty(lut.size + off, dtype=torch.int8, device=DEV)
+    lutd = flat[off:].view(lut.shape)
+    lutd.copy_(dev(lut))
+    y, acc, idx = mdn.matmul(dev(A), dev(split), dev(thr), lutd, dev(scale), dev(offset),
+                             want_acc=True, want_idx=True)
+    ridx, racc, ry = orc.matmul(A, split, thr, lut, scale, offset)
+    assert np.array_equal(host(idx), ridx)
+    assert np.array_equal(host(acc), racc)
+    assert np.array_equal(host(y), ry)
