@@ -323,7 +323,9 @@ _default = None
 
 
 def get() -> Oracle:
+    """The default build, or the library MADDNESS_ORACLE_LIB names (a
+    sanitizer build of the same source, for the tests)."""
     global _default
     if _default is None:
-        _default = Oracle()
+        _default = Oracle(os.environ.get("MADDNESS_ORACLE_LIB", _LIB))
     return _default
