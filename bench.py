@@ -77,6 +77,23 @@ def algorithmic_bytes(spec, N) -> int:
     return N * per_row + fixed
 
 
+def a_coverage(split, D, lda, rows=256):
+    """Share of the 32-byte sectors, 64-byte segments and 128-byte lines
+    spanned by a row of A that the split columns touch (over the first rows,
+    each at its own offset lda * 4 bytes in): how much of every row the
+    encode must fetch from HBM whatever it does."""
+    cols = np.unique(np.minimum(np.asarray(split).ravel(), D - 1)).astype(np.int64)
+    out = {}
+    for size, key in ((32, "sector32"), (64, "segment64"), (128, "line128")):
+        touched = spanned = 0
+        for r in range(rows):
+            base = r * lda * 4
+            touched += len(np.unique((base + 4 * cols) // size))
+            spanned += (base + 4 * D - 1) // size - base // size + 1
+        out[key] = round(touched / spanned, 4)
+    return out
+
+
 def stored_traffic(workload: str, kh: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
     None when it is missing or was taken on a different kernel source."""
@@ -295,7 +312,8 @@ def workload_block(name, steps, warmup, sample_n=2048):
     out = {"N": N, "D": spec.D, "C": spec.C, "M": spec.M, "table": "int8" if spec.quantized else "fp32",
            "rows_per_s": round(N / wall, 1), "step_us": round(step_s * 1e6, 2),
            "wall_us_per_step": round(wall * 1e6, 2), "algorithmic_bytes": abytes,
-           "hbm_frac": round(abytes / step_s / 1e9 / HBM_PEAK_GBS, 4), "steps": steps, "warmup": n_warm}
+           "hbm_frac": round(abytes / step_s / 1e9 / HBM_PEAK_GBS, 4), "steps": steps, "warmup": n_warm,
+           "a_coverage": a_coverage(p.split, spec.D, spec.D)}
     if graph_us is not None:
         out["graph_step_us"] = graph_us
     if mdn.matmul_index_bytes(A, spec.C, spec.M, f32=not spec.quantized) > 0:
@@ -435,6 +453,7 @@ def main():
                 "algorithmic_bytes": abytes, "kernel_us": round(avg_kern_s * 1e6, 2),
                 "kernel_us_min": round(k_min, 2), "kernel_us_median": round(k_med, 2),
                 "copy_peak": round(copy_gbs, 1), "frac_of_copy_peak": round(achieved / copy_gbs, 4),
+                "a_coverage": a_coverage(p.split, spec.D, spec.D),
                 "kernel": ("gfused_kernel<int8> (maddness_matmul, one launch per step)" if headline else
                            "whole step (maddness_matmul%s: encode + accumulate launches)"
                            % ("" if spec.quantized else "_f32")),
