@@ -88,9 +88,10 @@ struct Prefetch {
   int rrow[PF > 0 ? PF : 1];   // row within the chunk (0 when idle)
 
   __device__ __forceinline__ void init(int lane, int rw, int upr, int64_t src_rs, int lds_rs, int dummy) {
-    // u / upr as (u + 1/2) * rcp(upr), truncated: the product is within
-    // (u + 1/2) * 2^-21 of (u + 1/2) / upr, which lies at least 1/(2 upr) from
-    // every integer, so the truncation is exact for u < 2^20
+    // u / upr as (u + 1/2) * rcp(upr), truncated: with rcp within 1 ulp and
+    // one more rounding, the product is within 2^-21 (u + 1/2) / upr of
+    // (u + 1/2) / upr, which lies at least 1/(2 upr) from every integer, so
+    // the truncation is exact for u < 2^20 (and upr < 2^24, exact in fp32)
     const float rcp = __builtin_amdgcn_rcpf((float)upr);
 #pragma unroll
     for (int j = 0; j < PF; ++j) {
