@@ -368,8 +368,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "the path shards by rows with no exchange, so a multi-GPU run is not part of this "
-              "build", file=sys.stderr)
+              "the path would shard by rows with the tables replicated and no exchange (each GPU "
+              "running this step on its share); no multi-GPU path is implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -7,7 +7,7 @@ each entry's rows in ascending order in double on both sides; the solve
 takes the same correctly rounded operations (fma, division, square root) in
 the same order per entry on both sides (blocked on the GPU, unblocked in the
 oracle), so the fitted tables agree to the bit.  The quantizer applied to a
-given table is the build's quantizer: codes, scales and offsets bit-exact.
+given table is the table builder's quantizer: codes, scales and offsets bit-exact.
 """
 import numpy as np
 import pytest
