@@ -231,3 +231,14 @@ def test_fit_gd_rejects(L):
     assert G(FAKE, 10, 4, FAKE, 5, NULL, 2, FAKE, 0.1, float("inf"), 3, FAKE, FAKE, ws, NULL) == 1
     assert G(FAKE, 10, 4, FAKE, 5, NULL, 2, FAKE, 0.1, 0.01, 3, FAKE, FAKE, ws - 1, NULL) == 1
     assert G(FAKE, 10, 300, FAKE, 5, NULL, 2, FAKE, 0.1, 0.01, 3, FAKE, FAKE, 1 << 40, NULL) == 3
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU is present: valid-looking calls would launch kernels")
+def test_no_device_gives_ehip(L):
+    """On a machine without a GPU, calls whose arguments pass validation fail
+    in the HIP runtime and return EHIP (2) instead of crashing."""
+    assert L.maddness_encode(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, NULL) == 2
+    assert L.maddness_lut_accumulate(FAKE, 10, 4, FAKE, FAKE, FAKE, 10, NULL, FAKE, NULL) == 2
+    assert L.maddness_lut_accumulate_f32(FAKE, 10, 4, FAKE, 12, FAKE, NULL) == 2
+    assert L.maddness_matmul(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, FAKE, NULL, NULL, NULL) == 2
+    assert L.maddness_matmul_f32(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 12, FAKE, NULL, NULL) == 2
