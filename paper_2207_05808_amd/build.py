@@ -16,7 +16,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = ["csrc/kernels.hip", "csrc/fused_gather.hip", "csrc/fused_rows.hip", "csrc/tiled_accum.hip",
-           "csrc/row_lanes.hip", "csrc/lut_build.hip", "csrc/lut_fit.hip", "csrc/api.hip"]
+           "csrc/row_lanes.hip", "csrc/onehot_mfma.hip", "csrc/lut_build.hip", "csrc/lut_fit.hip", "csrc/api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

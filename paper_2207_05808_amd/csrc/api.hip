@@ -520,10 +520,57 @@ bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
   return true;
 }
 
+// One-hot product on the matrix cores (onehot_mfma.hip): int8 tables with
+// C % 16 == 0 and C <= 128, M % 4 == 0, a 4-byte aligned table, 8-byte
+// aligned index rows and 16-byte aligned outputs, at row counts where each of
+// the workgroups (one per CU) gets whole tiles of rows to stream.
+constexpr int64_t kMaccMinRows = 16384;
+bool plan_macc(const Shape& s, MArgs* m, int* blocks_out) {
+  if (s.elem != kI8 || s.C % 16 != 0 || s.C > 128 || s.M % 4 != 0 || s.N < kMaccMinRows) return false;
+  if (!aligned(s.lut, 4) || !aligned(s.idx_in, 8)) return false;
+  if ((s.y && !aligned(s.y, 16)) || (s.acc && !aligned(s.acc, 16))) return false;
+  if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;
+  const int W = macc_width(s.C);
+  MArgs a{};
+  a.idx = s.idx_in; a.lut = static_cast<const int8_t*>(s.lut); a.scale = s.scale; a.offset = s.offset;
+  a.y = s.y; a.acc = s.acc; a.col_bias = s.col_bias;
+  a.N = s.N; a.C = s.C; a.M = s.M;
+  a.act = s.act == 3 ? 1 : s.act;   // the softmax as a second pass
+  a.bias_lds = (a.act != 0 && s.col_bias) ? 1 : 0;
+  a.nslices = (s.M + W - 1) / W;
+  int groups = device_cus() / a.nslices;
+  if (groups < 1) groups = 1;
+  if (groups >= 8) {
+    groups -= groups % 8;
+    a.xcd_map = 1;
+  }
+  a.rows_per_group = round_up64((s.N + groups - 1) / groups, 64);
+  int off = (s.C <= 64 ? 64 : 128) * W * 16;   // the transposed table slice
+  auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
+  const int cp = s.C <= 64 ? 64 : 128;
+  a.off_val = take(kMaccGroups * cp);
+  a.off_sh = take(4 * cp);
+  a.off_misc = take(16);
+  a.off_bias = take(4 * W);
+  a.off_oh = take(8 * 16 * 16);   // one-hot operands: 8 rows of 16 entries
+  a.lds_total = off;
+  if (off > kLdsBytes) return false;
+  *m = a;
+  *blocks_out = groups * a.nslices;
+  return true;
+}
+
 // Accumulate-only work: the column-tiled kernel, else the general path.
 int accumulate(const Shape& s, hipStream_t stream) {
   TArgs t;
   int nj, nw;
+  MArgs m;
+  int mb;
+  if (plan_macc(s, &m, &mb)) {
+    const int rc = status_from(launch_macc(m, mb, stream));
+    if (rc != MADDNESS_OK || m.act == s.act) return rc;
+    return status_from(launch_softmax_rows(s.y, s.N, s.M, device_cus(), stream));
+  }
   if (plan_rlane(s, &t)) {
     const int rc = status_from(launch_rlane_f32(t, device_cus(), stream));
     if (rc != MADDNESS_OK || t.act == s.act) return rc;

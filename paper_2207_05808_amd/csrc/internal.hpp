@@ -172,6 +172,30 @@ struct FArgs {
 };
 hipError_t launch_fenc(const FArgs& f, int blocks, hipStream_t stream);
 
+// Lookup-accumulate as a one-hot int8 product on the matrix cores
+// (onehot_mfma.hip): int8 tables with C % 16 == 0 and C <= 128, M % 4 == 0.
+// Workgroups of 8 wavefronts each own one column slice (macc_width(C)
+// columns) of one row group; block b takes slice (b / 8) % nslices of group
+// (b / 8 / nslices) * 8 + b % 8 when xcd_map (groups a multiple of 8), else
+// slice b % nslices of group b / nslices.
+struct MArgs {
+  const uint8_t* idx;     // [N][C], 8-byte aligned
+  const int8_t* lut;      // [C][16][M], 4-byte aligned
+  const float* scale;     // [C]
+  const float* offset;    // [C]
+  float* y;               // [N][M] or null, 16-byte aligned
+  int32_t* acc;           // [N][M] or null, 16-byte aligned
+  const float* col_bias;  // [M] or null
+  int64_t N, rows_per_group;   // rows_per_group: a multiple of 64
+  int C, M, act;          // act: 0 none, 1 bias, 2 bias + ReLU (a softmax runs as a second pass)
+  int bias_lds;           // column biases staged in LDS (act != 0 and col_bias given)
+  int nslices, xcd_map;
+  int off_val, off_sh, off_misc, off_bias, off_oh, lds_total;   // LDS byte offsets (the table slice at 0)
+};
+constexpr int kMaccGroups = 5;   // one-hot shift groups of 7 for shifts up to 30
+int macc_width(int C);
+hipError_t launch_macc(const MArgs& m, int blocks, hipStream_t stream);
+
 // Rounded 8-bit summation over codebooks: the whole [C][16][Mt] column slice
 // (one byte per entry) staged once per workgroup, Mt = 16 * lanes per row.
 hipError_t launch_tavg(const TArgs& t, int nw, int cus, hipStream_t stream);

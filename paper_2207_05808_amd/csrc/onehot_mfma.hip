@@ -1,0 +1,348 @@
+// Lookup-accumulate as an int8 matrix product on the matrix cores.
+//
+// The encoder's output for a row is the concatenation of C one-hot vectors of
+// length 16 (§2.2 of McCarter & Dronen), and the lookup-accumulate is the
+// product of that 0/1 row with the stacked tables (§1: the sum over codebooks
+// of the selected table rows).  For int8 tables in block floating point the
+// exact integer sum is acc = sum_c 2^sh_c q_c[idx_c] with sh_c = e_c - e_min;
+// with the one-hot entry of codebook c set to 2^sh_c instead of 1, acc is one
+// int8 x int8 -> int32 product over K = 16 C, which v_mfma_i32_32x32x32_i8
+// computes exactly (int32 wraps only past the documented bound, and every
+// partial sum obeys the same bound).  One-hot entries must fit int8, so the
+// codebooks are taken in shift groups of width 7 (2^0 .. 2^6), the highest
+// group first, with the sums shifted left by 7 between groups: a table whose
+// shifts are all below 7 (the common case) takes one pass.
+//
+// Why the matrix cores: summed by gathers, each lookup reads 2 bytes of LDS
+// (a 16-bit field per column), and on layers with hundreds of output columns
+// the LDS, not HBM, sets the time.  The product does 16 times the arithmetic
+// of the gathers but on units that are otherwise idle, and reads the table
+// from LDS once per 64 rows: the kernel is left bound by its output stores.
+//
+// Layout.  A workgroup (8 wavefronts) owns one column slice of W = 32 WB
+// columns for its lifetime, staged once into LDS transposed, as [codebook]
+// [column][16 prototypes] bytes: the 16 bytes a lane passes as the table
+// operand of one product (32 columns x 32 K values: two codebooks, one per
+// half-wavefront) are one 16-byte read.  Each wavefront then takes tiles of
+// 64 rows (two 32-row blocks) of the workgroup's row range independently (no
+// barrier after the prologue): per pair of codebooks it builds the one-hot
+// operand of its rows in registers from their index bytes (loaded a tile
+// ahead), reads WB table operands, and issues 2 WB products.  The product's
+// K order inside an operand is the hardware's, but the same for both
+// operands, so the byte a lane places at a position of the table operand and
+// the byte it places at that position of the one-hot operand always belong
+// to the same (codebook, prototype).  Results come out with the rows across
+// the lanes and 4 consecutive columns per group of 4 registers: 16-byte
+// stores, y = fmaf(float(acc), 2^e_min, bias32) (the offsets' double sum,
+// codebooks ascending, rounded once), then the layer output's bias and ReLU.
+//
+// Workgroups are numbered so that the slices of one row group run on one XCD
+// (block b runs on XCD b % 8): the index rows of a group are read into one L2.
+#include "internal.hpp"
+
+#include <climits>
+#include <utility>
+
+namespace mdn {
+
+namespace {
+
+typedef int32_t mi32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t mi32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t mu32x2 __attribute__((ext_vector_type(2)));
+typedef float mf32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char mlds_t;
+typedef __attribute__((address_space(3))) mi32x4 mlds_i32x4;
+typedef __attribute__((address_space(3))) mu32x2 mlds_u32x2;
+typedef __attribute__((address_space(3))) uint32_t mlds_u32;
+typedef __attribute__((address_space(3))) uint8_t mlds_u8;
+typedef __attribute__((address_space(3))) int32_t mlds_i32;
+typedef __attribute__((address_space(3))) float mlds_f32;
+typedef __attribute__((address_space(3))) mf32x4 mlds_f32x4;
+
+constexpr int kMWaves = 8;      // wavefronts per workgroup
+constexpr int kMTileRows = 64;  // rows per wavefront tile: two blocks of 32
+constexpr int kMGroupBits = 7;  // one-hot entries 2^0 .. 2^6 fit int8
+static_assert(30 / 7 + 1 <= kMaccGroups, "shifts up to 30 (clamped, as everywhere) in whole groups of 7");
+
+__device__ __forceinline__ int muni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// f(integral_constant<int, I>) for I = 0, 1, ..., in order, unrolled
+template <typename F, int... I>
+__device__ __forceinline__ void mfor(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+
+}  // namespace
+
+// C16: codebooks in units of 16 (padded codebooks have one-hot entries 0);
+// WB: 32-column blocks per wavefront (W = 32 WB columns per slice)
+template <int C16, int WB>
+__global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
+  constexpr int W = 32 * WB;
+  constexpr int CP = 16 * C16;                 // staged codebooks
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  mlds_t* s_tab = (mlds_t*)smem_raw;           // [CP][W][16] bytes (off 0)
+  mlds_u8* s_val = reinterpret_cast<mlds_u8*>(s_tab + a.off_val);      // [kMaccGroups][CP] one-hot entries
+  mlds_i32* s_sh = reinterpret_cast<mlds_i32*>(s_tab + a.off_sh);      // [CP] shifts (-1: padding)
+  mlds_i32* s_misc = reinterpret_cast<mlds_i32*>(s_tab + a.off_misc);  // bias32 bits, e_min, max shift
+  mlds_f32* s_bias = reinterpret_cast<mlds_f32*>(s_tab + a.off_bias);  // [W] column biases of the slice
+  mlds_u32* s_oh = reinterpret_cast<mlds_u32*>(s_tab + a.off_oh);      // [8][16][16 bytes] one-hot operands
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = muni(tid >> 6);
+  const int C = a.C, M = a.M;
+  const int64_t N = a.N;
+
+  // ---------------- this workgroup's slice and rows
+  const int b = blockIdx.x;
+  int slice, group;
+  if (a.xcd_map) {   // the slices of a row group on one XCD
+    const int k = b >> 3;
+    slice = k % a.nslices;
+    group = (k / a.nslices) * 8 + (b & 7);
+  } else {
+    slice = b % a.nslices;
+    group = b / a.nslices;
+  }
+  const int col0 = slice * W;
+  const int64_t r0 = (int64_t)group * a.rows_per_group;
+  if (r0 >= N) return;   // uniform: no rows for this workgroup
+  const int64_t r1 = min(N, r0 + a.rows_per_group);
+
+  // ---------------- block exponents, shifts, the offsets' sum
+  if (tid == 0) { s_misc[1] = INT_MAX; s_misc[2] = 0; }
+  __syncthreads();
+  const uint32_t* sb = reinterpret_cast<const uint32_t*>(a.scale);
+  for (int c = tid; c < C; c += kMWaves * 64) atomicMin((int*)&s_misc[1], (int)((sb[c] >> 23) & 0xffu) - 127);
+  __syncthreads();
+  const int emin = muni(s_misc[1]);
+  for (int c = tid; c < CP; c += kMWaves * 64) {
+    const int sh = c < C ? min((int)((sb[c] >> 23) & 0xffu) - 127 - emin, 30) : -1;
+    s_sh[c] = sh;
+    atomicMax((int*)&s_misc[2], sh);
+  }
+  if (wave == 0) {   // double sum over codebooks in ascending order, rounded once
+    double sum = 0.0;
+    for (int c0 = 0; c0 < C; c0 += 64) {
+      const float ov = a.offset[min(c0 + lane, C - 1)];
+      const int n = min(64, C - c0);
+      for (int j = 0; j < n; ++j) sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(ov), j));
+    }
+    if (lane == 0) s_misc[0] = __float_as_int((float)sum);
+  }
+  if (a.bias_lds)   // zeros past the last column
+    for (int m = tid; m < W; m += kMWaves * 64) s_bias[m] = col0 + m < M ? a.col_bias[col0 + m] : 0.0f;
+
+  // ---------------- the table slice, transposed: LDS byte (c W + m) 16 + p =
+  // q[c][p][col0 + m].  A unit is 4 prototypes x 4 columns of one codebook:
+  // four dword loads (one per prototype row) and a 4 x 4 byte transpose.
+  {
+    constexpr int units = CP * 4 * (W / 4);
+    for (int u = tid; u < units; u += kMWaves * 64) {
+      const int m4 = u % (W / 4);
+      const int pg = (u / (W / 4)) & 3;
+      const int c = u / (W / 4) / 4;
+      const int col = col0 + 4 * m4;
+      uint32_t d[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t e = ((int64_t)c * 16 + 4 * pg + r) * M + col;
+        d[r] = (c < C && col < M) ? *reinterpret_cast<const uint32_t*>(a.lut + e) : 0u;
+      }
+      const uint32_t lo01 = __builtin_amdgcn_perm(d[1], d[0], 0x05010400u);   // d0.0 d1.0 d0.1 d1.1
+      const uint32_t hi01 = __builtin_amdgcn_perm(d[1], d[0], 0x07030602u);   // d0.2 d1.2 d0.3 d1.3
+      const uint32_t lo23 = __builtin_amdgcn_perm(d[3], d[2], 0x05010400u);
+      const uint32_t hi23 = __builtin_amdgcn_perm(d[3], d[2], 0x07030602u);
+      mlds_u32* dst = reinterpret_cast<mlds_u32*>(s_tab + ((c * W + 4 * m4) * 16 + 4 * pg));
+      dst[0] = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);    // column + 0: d0.0 d1.0 d2.0 d3.0
+      dst[4] = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u);    // column + 1
+      dst[8] = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);    // column + 2
+      dst[12] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);   // column + 3
+    }
+  }
+  __syncthreads();
+  const int maxsh = muni(s_misc[2]);
+  const int ngroups = maxsh / kMGroupBits + 1;
+  // the one-hot operands: row r < 7, entry x has byte x = 2^r (the others
+  // 0); row 7 is all zero.  Per shift group g, codebook c takes row sh_c - 7 g
+  // when its shift is in the group, else row 7.
+  for (int u = tid; u < 8 * 16 * 4; u += kMWaves * 64) {
+    const int r = u >> 6, x = (u >> 2) & 15, dw = u & 3;
+    s_oh[u] = (r < kMGroupBits && (x >> 2) == dw) ? (1u << r) << (8 * (x & 3)) : 0u;
+  }
+  for (int u = tid; u < ngroups * CP; u += kMWaves * 64) {
+    const int g = u / CP, c = u % CP;
+    const int sh = s_sh[c];
+    s_val[u] = (sh >= 0 && sh / kMGroupBits == g) ? (uint8_t)(sh - kMGroupBits * g) : (uint8_t)kMGroupBits;
+  }
+  __syncthreads();
+  const float step = __builtin_ldexpf(1.0f, emin);
+  const float bias32 = __int_as_float(muni(s_misc[0]));
+
+  // ---------------- row tiles
+  const int h = lane >> 5;    // half-wavefront: codebook 16 j + 8 h + i of the pair
+  const int ml = lane & 31;   // table operand: column; one-hot operand and results: row
+  const uint32_t lane_tab = (uint32_t)(uintptr_t)(s_tab + (8 * h * W + ml) * 16);
+  const int cvalid = (C + 15) >> 4;   // index chunks of 16 codebooks that exist
+  const int64_t ntiles = (r1 - r0 + kMTileRows - 1) / kMTileRows;
+
+  // index bytes of codebooks 16 j + 8 h .. + 7 of the lane's two rows
+  auto load_idx = [&](int64_t t, mu32x2 (&ix)[2][C16]) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      int64_t row = r0 + t * kMTileRows + 32 * rb + ml;
+      row = row < N ? row : N - 1;
+      const uint8_t* src = a.idx + row * C + 8 * h;
+#pragma unroll
+      for (int j = 0; j < C16; ++j)
+        ix[rb][j] = j < cvalid ? *reinterpret_cast<const mu32x2*>(src + 16 * j) : (mu32x2){0u, 0u};
+    }
+  };
+
+  // index chunks of the current tile; chunk j is reloaded with the next
+  // tile's as soon as the last product step that reads it has been issued
+  mu32x2 ixc[2][C16];
+  const uint32_t oh_base = (uint32_t)(uintptr_t)s_oh;
+  const bool plain = a.y && !a.acc && a.act == 0 && col0 + W <= M;   // uniform
+  int64_t t = wave;
+  if (t < ntiles) load_idx(t, ixc);
+  for (; t < ntiles; t += kMWaves) {
+    const bool more = t + kMWaves < ntiles;   // uniform
+    mi32x16 acc[2][WB];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < WB; ++cb) acc[rb][cb] = (mi32x16){};
+    for (int g = ngroups - 1; g >= 0; --g) {
+      if (g != ngroups - 1) {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < WB; ++cb) acc[rb][cb] <<= kMGroupBits;
+      }
+      const mlds_t* vrow = reinterpret_cast<const mlds_t*>(s_val) + g * CP + 8 * h;
+      mu32x2 vv[C16];   // one-hot rows of the lane's codebooks in this group
+#pragma unroll
+      for (int j = 0; j < C16; ++j) vv[j] = *reinterpret_cast<const mlds_u32x2*>(vrow + 16 * j);
+      // (the index bytes opaque here: their extraction stays inside the group
+      // loop instead of being hoisted out of it into more registers)
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int j = 0; j < C16; ++j) asm volatile("" : "+v"(ixc[rb][j]));
+      // operands of product step s (codebooks 16 j + i and + 8: j = s / 8,
+      // i = s % 8), read one step ahead of the products that use them
+      auto load_ops = [&](auto sc, mi32x4 (&At)[WB], mi32x4 (&Bt)[2]) {
+        constexpr int st = decltype(sc)::value;
+        constexpr int j = st / 8, i = st % 8;
+#pragma unroll
+        for (int cb = 0; cb < WB; ++cb)
+          At[cb] = *reinterpret_cast<const mlds_i32x4*>((const mlds_t*)(uintptr_t)lane_tab +
+                                                        ((16 * j + i) * W + 32 * cb) * 16);
+        const uint32_t vb = oh_base + (((vv[j][i >> 2] >> (8 * (i & 3))) & 0xffu) << 8);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          const uint32_t x = (ixc[rb][j][i >> 2] >> (8 * (i & 3))) & 15u;
+          Bt[rb] = *reinterpret_cast<const mlds_i32x4*>((const mlds_t*)(uintptr_t)(vb + (x << 4)));
+        }
+      };
+      mi32x4 Ta[WB], Tb[WB], Ba[2], Bb[2];
+      load_ops(std::integral_constant<int, 0>{}, Ta, Ba);
+      mfor([&](auto sc) {
+        constexpr int st = decltype(sc)::value;
+        mi32x4(&cur)[WB] = (st & 1) ? Tb : Ta;
+        mi32x4(&nxt)[WB] = (st & 1) ? Ta : Tb;
+        mi32x4(&bcur)[2] = (st & 1) ? Bb : Ba;
+        mi32x4(&bnxt)[2] = (st & 1) ? Ba : Bb;
+        if constexpr (st + 1 < 8 * C16) load_ops(std::integral_constant<int, st + 1>{}, nxt, bnxt);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < WB; ++cb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(cur[cb], bcur[rb], acc[rb][cb], 0, 0, 0);
+        if constexpr (st % 8 == 7) {
+          // chunk st / 8 has been read for the last time in this pass: in
+          // the last pass, start loading the next tile's
+          constexpr int j = st / 8;
+          if (g == 0 && more && j < cvalid) {
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+              int64_t row = r0 + (t + kMWaves) * kMTileRows + 32 * rb + ml;
+              row = row < N ? row : N - 1;
+              ixc[rb][j] = *reinterpret_cast<const mu32x2*>(a.idx + row * C + 8 * h + 16 * j);
+            }
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }, std::make_integer_sequence<int, 8 * C16>{});
+    }
+
+    // ---------------- epilogue: lane (ml, h) holds row ml of each block and,
+    // in registers 4 q .. 4 q + 3, columns 8 q + 4 h .. + 3 of each 32-column block
+    if (plain) {   // y only, no layer output, every column of the slice exists
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const int64_t row = r0 + t * kMTileRows + 32 * rb + ml;
+        if (row >= r1) continue;
+        mf32x4* yr = reinterpret_cast<mf32x4*>(a.y + row * M + col0 + 4 * h);
+#pragma unroll
+        for (int cb = 0; cb < WB; ++cb)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            mf32x4 z;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) z[e] = __builtin_fmaf((float)acc[rb][cb][4 * q + e], step, bias32);
+            yr[(32 * cb + 8 * q) / 4] = z;
+          }
+      }
+      continue;
+    }
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const int64_t row = r0 + t * kMTileRows + 32 * rb + ml;
+      if (row >= r1) continue;
+#pragma unroll
+      for (int cb = 0; cb < WB; ++cb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int lc = 32 * cb + 8 * q + 4 * h;   // column within the slice
+          if (col0 + lc >= M) continue;             // (M % 4 == 0: groups of 4 are whole)
+          const int s0 = acc[rb][cb][4 * q], s1 = acc[rb][cb][4 * q + 1];
+          const int s2 = acc[rb][cb][4 * q + 2], s3 = acc[rb][cb][4 * q + 3];
+          if (a.y) {
+            mf32x4 z = {__builtin_fmaf((float)s0, step, bias32), __builtin_fmaf((float)s1, step, bias32),
+                        __builtin_fmaf((float)s2, step, bias32), __builtin_fmaf((float)s3, step, bias32)};
+            if (a.act != 0) {
+              const mf32x4 bb = a.bias_lds ? *reinterpret_cast<const mlds_f32x4*>(s_bias + lc)
+                                           : (mf32x4){0.0f, 0.0f, 0.0f, 0.0f};
+              z = z + bb;
+              if (a.act == 2)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) z[e] = z[e] > 0.0f ? z[e] : 0.0f;
+            }
+            *reinterpret_cast<mf32x4*>(a.y + row * M + col0 + lc) = z;
+          }
+          if (a.acc) *reinterpret_cast<mi32x4*>(a.acc + row * M + col0 + lc) = (mi32x4){s0, s1, s2, s3};
+        }
+    }
+  }
+}
+
+int macc_width(int C) { return C <= 64 ? 128 : 64; }
+
+hipError_t launch_macc(const MArgs& m, int blocks, hipStream_t stream) {
+  const void* fn = m.C <= 64 ? reinterpret_cast<const void*>(&macc_kernel<4, 4>)
+                             : reinterpret_cast<const void*>(&macc_kernel<8, 2>);
+  hipError_t err = hipSuccess;
+  launch_prepare(fn, kMWaves * 64, m.lds_total, &err);
+  if (err != hipSuccess) return err;
+  if (m.C <= 64)
+    hipLaunchKernelGGL((macc_kernel<4, 4>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total, stream, m);
+  else
+    hipLaunchKernelGGL((macc_kernel<8, 2>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total, stream, m);
+  return hipGetLastError();
+}
+
+}  // namespace mdn

@@ -73,12 +73,13 @@ def test_row_streaming_vs_encode_then_accumulate():
 
 
 def test_one_row_per_lane_vs_row_uniform_int8():
-    """Accumulate-only, int8 table of 64 codebooks and 512 columns: outputs
-    alone take the one-row-per-lane kernel, outputs plus int32 sums the
-    row-uniform kernel."""
-    N, C, M = 20485, 64, 512
+    """Accumulate-only, int8 table of 256 codebooks (past the one-hot
+    product's 128) and 512 columns, one shared block exponent (so the 16-bit
+    field sums fit): outputs alone take the one-row-per-lane kernel, outputs
+    plus int32 sums the row-uniform kernel."""
+    N, C, M = 20485, 256, 512
     idx = dev(W.random_indices(N, C, seed=13))
-    lut, scale, offset = W.random_codes(C, M, seed=14, max_shift=2)
+    lut, scale, offset = W.random_codes(C, M, seed=14, max_shift=0)
     _, y0 = mdn.lut_accumulate(idx, dev(lut), dev(scale), dev(offset))
     a1, y1 = mdn.lut_accumulate(idx, dev(lut), dev(scale), dev(offset), want_acc=True)
     assert np.array_equal(host(y0), host(y1))
@@ -104,5 +105,20 @@ def test_gather_fused_encode_vs_indices():
     ld, scd, od = dev(lut), dev(scale), dev(offset)
     y0, a0, idx = mdn.matmul(dev(A), dev(split), dev(thr), ld, scd, od, want_acc=True, want_idx=True)
     a1, y1 = mdn.lut_accumulate(idx, ld, scd, od, want_acc=True)
+    assert np.array_equal(host(a0), host(a1))
+    assert np.array_equal(host(y0), host(y1))
+
+
+def test_one_hot_product_vs_row_uniform():
+    """Accumulate-only, int8 table of 64 codebooks and 512 columns, outputs
+    and int32 sums: 8-byte aligned index rows take the one-hot product on the
+    matrix cores, index rows 4 bytes off that alignment the row-uniform
+    kernel."""
+    N, C, M = 20485, 64, 512
+    idx = W.random_indices(N, C, seed=20)
+    lut, scale, offset = W.random_codes(C, M, seed=21, max_shift=9)
+    ld, scd, od = dev(lut), dev(scale), dev(offset)
+    a0, y0 = mdn.lut_accumulate(dev(idx), ld, scd, od, want_acc=True)
+    a1, y1 = mdn.lut_accumulate(shifted(idx, torch.uint8, 4), ld, scd, od, want_acc=True)
     assert np.array_equal(host(a0), host(a1))
     assert np.array_equal(host(y0), host(y1))

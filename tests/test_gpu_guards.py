@@ -101,18 +101,19 @@ def test_fused_guards(orc, name, N, D, C, M, outs):
         assert np.array_equal(first[-1][r], ridx)
 
 
-ACCUM = [  # (kernel family, N, C, M, table, with int32 sums)
-    ("one-row-per-lane-int8", 20485, 64, 512, "i8", False),
-    ("row-uniform", 20485, 64, 512, "i8", True),
-    ("column-tiled", 5001, 96, 200, "i8", True),
-    ("gather-fused-indices", 5003, 32, 64, "i8", True),
-    ("one-row-per-lane-fp32", 20485, 32, 1000, "f32", False),
-    ("averaging", 5001, 64, 512, "avg", False),
+ACCUM = [  # (kernel family, N, C, M, table, with int32 sums, spread of the block exponents)
+    ("one-hot-product", 20485, 64, 512, "i8", True, 1),
+    ("one-row-per-lane-int8", 20485, 256, 512, "i8", False, 0),   # (past the one-hot product's 128 codebooks)
+    ("row-uniform", 20485, 256, 512, "i8", True, 1),
+    ("column-tiled", 5001, 96, 200, "i8", True, 1),
+    ("gather-fused-indices", 5003, 32, 64, "i8", True, 1),
+    ("one-row-per-lane-fp32", 20485, 32, 1000, "f32", False, 0),
+    ("averaging", 5001, 64, 512, "avg", False, 0),
 ]
 
 
-@pytest.mark.parametrize("name,N,C,M,table,with_acc", ACCUM, ids=[c[0] for c in ACCUM])
-def test_accumulate_guards(orc, name, N, C, M, table, with_acc):
+@pytest.mark.parametrize("name,N,C,M,table,with_acc,max_shift", ACCUM, ids=[c[0] for c in ACCUM])
+def test_accumulate_guards(orc, name, N, C, M, table, with_acc, max_shift):
     idx = W.random_indices(N, C, seed=N + M)
     y = Guarded((N, M), torch.float32, 12345.0)
     acc = Guarded((N, M), torch.int32, -7) if with_acc else None
@@ -123,7 +124,7 @@ def test_accumulate_guards(orc, name, N, C, M, table, with_acc):
         first = run_twice(lambda: mdn.lut_accumulate_f32(dev(idx), dev(tab), y_out=y.view), present)
         assert np.array_equal(first[0][r], orc.lut_accumulate_f32(idx[r], tab))
         return
-    lut, scale, offset = W.random_codes(C, M, seed=N + 1, max_shift=0 if table == "avg" else 1)
+    lut, scale, offset = W.random_codes(C, M, seed=N + 1, max_shift=max_shift)
     if table == "avg":   # (max_shift 0: one block exponent shared by every codebook)
         first = run_twice(lambda: mdn.lut_accumulate_avg(dev(idx), dev(lut), dev(scale), dev(offset),
                                                          y_out=y.view), present)
