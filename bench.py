@@ -39,6 +39,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, published
 LDS_PEAK_TBS = 157.3   # 256 B/clk per CU x 256 CUs x 2.4 GHz (a ds_read_b128 probe reaches about 88% of it)
+I8_MFMA_PEAK_TOPS = 5000.0  # MI355X dense int8 matrix-core peak, published (5.0 POP/s)
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 
 
@@ -237,6 +238,13 @@ def copy_peak_gbs(dev, mb=512, reps=10):
 WARM_SECONDS = 0.2   # minimum warm-up of each workload block
 
 
+def onehot_product_route(spec, N):
+    """Whether the library's accumulate takes the one-hot int8 product for
+    this layer (int8 table, C % 16 == 0, C <= 128, M % 4 == 0, 16384 rows or
+    more; the buffers here are aligned): for reporting its roof only."""
+    return spec.quantized and spec.C % 16 == 0 and spec.C <= 128 and spec.M % 4 == 0 and N >= 16384
+
+
 def workload_block(name, steps, warmup, sample_n=2048):
     """Compact measurement of one workload's step (the fused entry point over
     all its rows, inputs resident): rows/s, step time, HBM fraction of the
@@ -323,11 +331,22 @@ def workload_block(name, steps, warmup, sample_n=2048):
             acc_us = region_us(lambda i: mdn.lut_accumulate(idx, lut, scale, offset, y_out=y), stream, reps=5, warm=1)
         else:
             acc_us = region_us(lambda i: mdn.lut_accumulate_f32(idx, lut, y_out=y), stream, reps=5, warm=1)
-        lds_bytes = N * spec.C * spec.M * (2 if spec.quantized else 4)
         out.update({"encode_us": round(enc_us, 2), "accumulate_us": round(acc_us, 2),
-                    "encode_hbm_frac": round((4 * spec.D + spec.C) * N / (enc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-                    "accumulate_lds_frac": round(lds_bytes / (acc_us * 1e-6) / 1e12 / LDS_PEAK_TBS, 4),
-                    "accumulate_lds_read_bytes": lds_bytes})
+                    "encode_hbm_frac": round((4 * spec.D + spec.C) * N / (enc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+        if onehot_product_route(spec, N):
+            # the one-hot int8 product on the matrix cores: N x 16 C x M
+            # multiply-adds against the dense int8 peak, and the output
+            # stores against the HBM peak
+            macs = N * 16 * spec.C * spec.M
+            out.update({"accumulate_route": "one-hot int8 product (matrix cores)",
+                        "accumulate_mfma_frac": round(2 * macs / (acc_us * 1e-6) / 1e12 / I8_MFMA_PEAK_TOPS, 4),
+                        "accumulate_macs": macs,
+                        "accumulate_store_hbm_frac": round(4 * N * spec.M / (acc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+        else:
+            lds_bytes = N * spec.C * spec.M * (2 if spec.quantized else 4)
+            out.update({"accumulate_route": "gathers from LDS",
+                        "accumulate_lds_frac": round(lds_bytes / (acc_us * 1e-6) / 1e12 / LDS_PEAK_TBS, 4),
+                        "accumulate_lds_read_bytes": lds_bytes})
         del idx
     torch.backends.cuda.matmul.allow_tf32 = False
     gout = torch.empty((N, spec.M), dtype=torch.float32, device=dev)

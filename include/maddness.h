@@ -21,7 +21,8 @@
  *    allocation, so every call can be captured in a HIP graph.  Where a call
  *    needs device memory beyond its inputs and outputs, the caller passes it:
  *    the index array of the fused entry points for tables too large for
- *    their single-launch kernels (maddness_matmul_index_bytes), and the
+ *    their single-launch kernels or where two phases are faster
+ *    (maddness_matmul_index_bytes), and the
  *    workspaces of the table fit.
  *  - Row-major layouts.  A has row stride `lda` (elements, lda >= D); every
  *    other array is dense.
@@ -178,8 +179,13 @@ int maddness_lut_accumulate_f32(const uint8_t* idx, int64_t N, int32_t C,
  * output.  When the table [C][16][M] fits the single-launch kernels the
  * indices never leave the chip and idx_out is optional (written when given).
  * Otherwise the rows are encoded into idx_out and then accumulated, and
- * idx_out is required: EINVAL when it is NULL.  maddness_matmul_index_bytes
- * tells which case a call is.
+ * idx_out is required: EINVAL when it is NULL.  One case sits between: int8
+ * tables of 64 codebooks and 16 <= M <= 512 columns at 98304 rows or more
+ * run as one launch without idx_out, but given an 8-byte aligned idx_out
+ * with M >= 128 they run faster in two phases through it (encode, then the
+ * lookup-accumulate as a one-hot int8 product on the matrix cores, §2.2's
+ * encoder output taken as a 0/1 matrix).  maddness_matmul_index_bytes tells
+ * which case a call is.
  */
 int maddness_matmul(const float* A, int64_t N, int32_t D, int64_t lda,
                     const int32_t* split_dims, const float* thresholds,
@@ -251,9 +257,10 @@ int maddness_matmul_noalloc(const float* A, int64_t N, int32_t D, int64_t lda,
                             int32_t* acc_out, uint8_t* idx_out, void* stream);
 
 /*
- * Device bytes the fused entry points need in idx_out for this call: 0 when
- * the table fits their single-launch kernels (idx_out optional), N * C when
- * the indices go through memory (idx_out required).  The answer depends on
+ * Device bytes of idx_out that the fused entry points use for this call: 0
+ * when the call runs as one launch (idx_out optional), N * C when the indices
+ * go through memory: required there, except for the shapes above that also
+ * run as one launch without it (slower).  The answer depends on
  * the shape, on whether the table is fp32 (f32 != 0), on act (the layer
  * output of maddness_matmul_act[_f32]; 0 for maddness_matmul[_f32]) and on
  * the alignment of A, so pass the A of the call.  Returns -1 for arguments

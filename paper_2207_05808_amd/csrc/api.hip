@@ -525,11 +525,14 @@ bool plan_tavg(const Shape& s, TArgs* t, int* nw_out) {
 // aligned index rows and 16-byte aligned outputs, at row counts where each of
 // the workgroups (one per CU) gets whole tiles of rows to stream.
 constexpr int64_t kMaccMinRows = 16384;
-bool plan_macc(const Shape& s, MArgs* m, int* blocks_out) {
+bool macc_shape(const Shape& s) {   // (everything but the index rows' alignment)
   if (s.elem != kI8 || s.C % 16 != 0 || s.C > 128 || s.M % 4 != 0 || s.N < kMaccMinRows) return false;
-  if (!aligned(s.lut, 4) || !aligned(s.idx_in, 8)) return false;
+  if (!aligned(s.lut, 4)) return false;
   if ((s.y && !aligned(s.y, 16)) || (s.acc && !aligned(s.acc, 16))) return false;
-  if ((int64_t)s.C * kK * s.M >= (1ll << 31)) return false;
+  return (int64_t)s.C * kK * s.M < (1ll << 31);
+}
+bool plan_macc(const Shape& s, MArgs* m, int* blocks_out) {
+  if (!macc_shape(s) || !aligned(s.idx_in, 8)) return false;
   const int W = macc_width(s.C);
   MArgs a{};
   a.idx = s.idx_in; a.lut = static_cast<const int8_t*>(s.lut); a.scale = s.scale; a.offset = s.offset;
@@ -649,6 +652,18 @@ int two_phase(const Shape& s, uint8_t* idx, hipStream_t stream) {
   return accumulate(q, stream);
 }
 
+// Whether a fused call that the row-streaming kernel could take runs faster
+// as encode + the one-hot product, through an index array: measured on 1M
+// rows of 512 columns of A with 64 codebooks, 0.84 against 1.05 ms at 512
+// output columns, 0.62 against 0.94 at 256, 0.51 against 0.89 at 128 (the
+// encode alone is 0.37 ms).
+constexpr int kTwoPhaseMinCols = 128;
+bool two_phase_faster(const Shape& s) {
+  FArgs f;
+  int blocks;
+  return s.M >= kTwoPhaseMinCols && macc_shape(s) && plan_fenc(s, &f, &blocks, nullptr, 0);
+}
+
 // Whether a fused call runs as one launch (the gather-fused kernel, or the
 // general kernel with the whole table in one column tile; the latter has no
 // layer-output epilogue).
@@ -681,7 +696,10 @@ int fused(const Shape& s, hipStream_t st) {
   FArgs f;
   TArgs t;
   int blocks;
-  if (plan_fenc(s, &f, &blocks, &t, device_cus())) {
+  // (given an index array the row-streaming kernel's shapes may go faster
+  // in two phases; without one they take that kernel, as one launch)
+  const bool two = s.idx_out && aligned(s.idx_out, 8) && two_phase_faster(s);
+  if (!two && plan_fenc(s, &f, &blocks, &t, device_cus())) {
     const int rc = status_from(launch_fenc(f, blocks, st));
     if (rc != MADDNESS_OK) return rc;
     return status_from(launch_trow(kI8, t, device_cus(), st));
@@ -902,7 +920,7 @@ int64_t maddness_matmul_index_bytes(const float* A, int64_t N, int32_t D, int64_
   if (!A || !aligned(A, 4)) return -1;
   Shape s = shape(kFused, f32 ? kF32 : kI8);
   s.A = A; s.N = N; s.D = D; s.lda = lda; s.C = C; s.M = M; s.act = act;
-  return single_launch(s) ? 0 : N * (int64_t)C;
+  return (two_phase_faster(s) || !single_launch(s)) ? N * (int64_t)C : 0;
 }
 
 int maddness_build_lut(const float* P, const float* B, int32_t C, int32_t D, int32_t M, int8_t* lut_out,

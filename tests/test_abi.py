@@ -88,18 +88,22 @@ def test_matmul_rejects(L):
 
 
 def test_matmul_index_bytes(L):
-    """The fused entry points need a caller index array exactly when their
-    own kernels cannot take the table: 0 for the im2col conv layer (C = 32,
-    M = 64), the tiny classifier and the dense hidden layer (C = 64, M = 512:
-    the row-streaming kernel, from 98304 rows on), N * C for the dense hidden
-    layer's shape below that, the wide layer and the fp32 search-tree layer."""
+    """The fused entry points use a caller index array when their own
+    single-launch kernels cannot take the table, or when encode + the one-hot
+    product beats the row-streaming kernel: 0 for the im2col conv layer
+    (C = 32, M = 64) and the tiny classifier; N * C for the dense hidden layer
+    (C = 64, M = 512; without an index array it still runs, as one launch of
+    the row-streaming kernel, from 98304 rows on), its shape below that, the
+    wide layer and the fp32 search-tree layer; 0 again for 64 output columns
+    (the row-streaming kernel alone)."""
     Q = L.maddness_matmul_index_bytes
     assert Q(FAKE, 131072, 576, 576, 32, 64, 0, 0) == 0
     assert Q(FAKE, 131072, 576, 576, 32, 64, 0, 3) == 0
     assert Q(FAKE, 1024, 64, 64, 4, 10, 0, 3) == 0
-    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 0) == 0
-    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 3) == 0
-    assert Q(FAKE, 98304, 512, 512, 64, 512, 0, 0) == 0
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 0) == (1 << 20) * 64
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 0, 3) == (1 << 20) * 64
+    assert Q(FAKE, 98304, 512, 512, 64, 512, 0, 0) == 98304 * 64
+    assert Q(FAKE, 1 << 20, 512, 512, 64, 64, 0, 0) == 0
     assert Q(FAKE, 98303, 512, 512, 64, 512, 0, 0) == 98303 * 64
     assert Q(FAKE, 1 << 20, 512, 512, 64, 520, 0, 0) == (1 << 20) * 64     # M % 16 != 0
     assert Q(FAKE, 1 << 20, 512, 512, 64, 512, 1, 0) == (1 << 20) * 64     # fp32 table
@@ -242,3 +246,7 @@ def test_no_device_gives_ehip(L):
     assert L.maddness_lut_accumulate_f32(FAKE, 10, 4, FAKE, 12, FAKE, NULL) == 2
     assert L.maddness_matmul(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, FAKE, FAKE, 10, FAKE, NULL, NULL, NULL) == 2
     assert L.maddness_matmul_f32(FAKE, 10, 64, 64, FAKE, FAKE, 4, FAKE, 12, FAKE, NULL, NULL) == 2
+    # the dense hidden layer without an index array is not rejected: it takes
+    # the row-streaming kernel (one launch)
+    assert L.maddness_matmul(FAKE, 1 << 20, 512, 512, FAKE, FAKE, 64, FAKE, FAKE, FAKE, 512, FAKE, NULL, NULL,
+                             NULL) == 2

@@ -8,8 +8,13 @@ and sums in one launch when the 16-bit field sums fit (255 sum_c 2^sh <=
 each output row) and the row-uniform accumulate that always follows it sums
 with 32-bit accumulators.  Both branches are covered here, with row strides,
 ragged row counts, column counts below one tile, the field bound exactly,
-every layer output, and the optional index and int32 outputs.  Bar: indices,
-int32 sums and fp32 outputs bit-exact; softmax within the bound of the sigma
+every layer output, and the optional index and int32 outputs.  Given an
+8-byte aligned index array, calls of at least 128 columns whose table the
+one-hot product takes run faster as encode + that product (the index-size
+query asks for the array there); so the kernel itself is reached here through
+the allocation-free entry point without an index array, or with one at a
+4-byte offset, and the routed call is checked beside it.  Bar: indices, int32
+sums and fp32 outputs bit-exact; softmax within the bound of the sigma
 tests."""
 import numpy as np
 import pytest
@@ -50,22 +55,35 @@ def rows_sample(N, seed=0):
     return np.unique(np.r_[0:1500, N - 1500:N, rng.integers(0, N, size=3000)])
 
 
+def offset_index_array(N):
+    """An [N, 64] index array 4 bytes past an 8-byte boundary: the one-hot
+    product does not take it, so a fused call keeps the row-streaming kernel."""
+    flat = torch.empty(N * 64 + 4, dtype=torch.uint8, device=DEV)
+    return flat[4:].view(N, 64)
+
+
 def run_and_check(orc, A, D, split, thr, lut, scale, offset, rows=None, with_idx=True, with_acc=True):
-    """Fused call on A[:, :D] (row stride A.shape[1]); outputs against the oracle."""
+    """Fused call on A[:, :D] (row stride A.shape[1]) through the row-streaming
+    kernel, and as the library routes it by default; both against the oracle."""
     N, M = A.shape[0], lut.shape[2]
     Ad = dev(A)[:, :D]
     args = (Ad, dev(split), dev(thr), dev(lut), dev(scale), dev(offset))
-    assert mdn.matmul_index_bytes(Ad, 64, M) == 0   # one call, no index array needed
-    y, acc, idx = mdn.matmul(*args, want_acc=with_acc, want_idx=with_idx, validate=True)
+    assert mdn.matmul_index_bytes(Ad, 64, M) == (N * 64 if M >= 128 else 0)
+    y = torch.empty((N, M), dtype=torch.float32, device=DEV)
+    acc = torch.empty((N, M), dtype=torch.int32, device=DEV) if with_acc else None
+    idx = offset_index_array(N) if with_idx else None
+    mdn.matmul_noalloc(*args, y_out=y, acc_out=acc, idx_out=idx)
     rows = np.arange(N) if rows is None else rows
     ridx, racc, ry = orc.matmul(A[rows, :D], split, thr, lut, scale, offset)
     r = torch.from_numpy(rows).to(DEV)
-    if with_idx:
-        assert np.array_equal(host(idx[r]), ridx)
-        assert int(idx.max()) < 16
-    if with_acc:
-        assert np.array_equal(host(acc[r]), racc)
-    assert np.array_equal(host(y[r]), ry)
+    routed = mdn.matmul(*args, want_acc=with_acc, want_idx=with_idx, validate=True)
+    for yy, aa, ii in ((y, acc, idx), routed):
+        if with_idx:
+            assert np.array_equal(host(ii[r]), ridx)
+            assert int(ii.max()) < 16
+        if with_acc:
+            assert np.array_equal(host(aa[r]), racc)
+        assert np.array_equal(host(yy[r]), ry)
     return y
 
 
@@ -117,16 +135,19 @@ def test_layer_outputs(orc, act):
     rl, rs, ro = orc.build_quantized_lut(p.P, p.B)
     bias = np.random.default_rng(4).standard_normal(512).astype(np.float32)
     args = (dev(p.A), dev(p.split), dev(p.thr), dev(rl), dev(rs), dev(ro))
-    assert mdn.matmul_index_bytes(args[0], 64, 512, act=act) == 0
-    y = host(mdn.matmul_act(*args, col_bias=dev(bias), act=act))
+    assert mdn.matmul_index_bytes(args[0], 64, 512, act=act) == p.N * 64
     rows = rows_sample(p.N, 3)
     _, _, yr = orc.matmul(p.A[rows], p.split, p.thr, rl, rs, ro)
     code = {"bias": 1, "relu": 2, "softmax": 3}[act]
     ref = orc.sigma(yr, bias, code)
-    got = y[rows].astype(np.float64)
-    if act != "softmax":
-        assert np.array_equal(got, ref)
-    else:
-        z = orc.sigma(yr, bias, 1)
-        tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + 512 + 5) * 2.0 ** -24 * ref + 2.0 ** -120
-        assert np.all(np.abs(got - ref) <= tol)
+    # the row-streaming kernel (index array off 8-byte alignment), then the
+    # routed call (encode + one-hot product)
+    for idx in (offset_index_array(p.N), None):
+        y = host(mdn.matmul_act(*args, col_bias=dev(bias), act=act, idx_out=idx))
+        got = y[rows].astype(np.float64)
+        if act != "softmax":
+            assert np.array_equal(got, ref)
+        else:
+            z = orc.sigma(yr, bias, 1)
+            tol = 1.01 * (np.abs(z - z.max(axis=1, keepdims=True)) + 512 + 5) * 2.0 ** -24 * ref + 2.0 ** -120
+            assert np.all(np.abs(got - ref) <= tol)
