@@ -543,10 +543,7 @@ bool plan_macc(const Shape& s, MArgs* m, int* blocks_out) {
   a.nslices = (s.M + W - 1) / W;
   int groups = device_cus() / a.nslices;
   if (groups < 1) groups = 1;
-  if (groups >= 8) {
-    groups -= groups % 8;
-    a.xcd_map = 1;
-  }
+  a.xcd_map = (groups * a.nslices) % 8 == 0;
   a.rows_per_group = round_up64((s.N + groups - 1) / groups, 64);
   int off = (s.C <= 64 ? 64 : 128) * W * 16;   // the transposed table slice
   auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };

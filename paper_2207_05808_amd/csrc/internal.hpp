@@ -175,9 +175,9 @@ hipError_t launch_fenc(const FArgs& f, int blocks, hipStream_t stream);
 // Lookup-accumulate as a one-hot int8 product on the matrix cores
 // (onehot_mfma.hip): int8 tables with C % 16 == 0 and C <= 128, M % 4 == 0.
 // Workgroups of 8 wavefronts each own one column slice (macc_width(C)
-// columns) of one row group; block b takes slice (b / 8) % nslices of group
-// (b / 8 / nslices) * 8 + b % 8 when xcd_map (groups a multiple of 8), else
-// slice b % nslices of group b / nslices.
+// columns) of one row group; with xcd_map (a grid of whole multiples of 8)
+// block b takes pair gi = (b % 8) (grid / 8) + b / 8 of the (group, slice)
+// pairs in group-major order, else slice b % nslices of group b / nslices.
 struct MArgs {
   const uint8_t* idx;     // [N][C], 8-byte aligned
   const int8_t* lut;      // [C][16][M], 4-byte aligned

@@ -36,8 +36,9 @@
 // stores, y = fmaf(float(acc), 2^e_min, bias32) (the offsets' double sum,
 // codebooks ascending, rounded once), then the layer output's bias and ReLU.
 //
-// Workgroups are numbered so that the slices of one row group run on one XCD
-// (block b runs on XCD b % 8): the index rows of a group are read into one L2.
+// Workgroups are numbered so that the slices of one row group run on one XCD,
+// or on as few as the group's slices fill (block b runs on XCD b % 8): the
+// index rows of a group are read into one or two L2s, not eight.
 #include "internal.hpp"
 
 #include <climits>
@@ -121,10 +122,12 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   // ---------------- this workgroup's slice and rows
   const int b = blockIdx.x;
   int slice, group;
-  if (a.xcd_map) {   // the slices of a row group on one XCD
-    const int k = b >> 3;
-    slice = k % a.nslices;
-    group = (k / a.nslices) * 8 + (b & 7);
+  if (a.xcd_map) {
+    // (group, slice) pairs in group-major order, a contiguous run of them per
+    // XCD (block b runs on XCD b % 8): the slices of a row group share an L2
+    const int gi = (b & 7) * (int)(gridDim.x >> 3) + (b >> 3);
+    slice = gi % a.nslices;
+    group = gi / a.nslices;
   } else {
     slice = b % a.nslices;
     group = b / a.nslices;
