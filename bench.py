@@ -326,11 +326,11 @@ def workload_block(name, steps, warmup, sample_n=2048):
         out["graph_step_us"] = graph_us
     if mdn.matmul_index_bytes(A, spec.C, spec.M, f32=not spec.quantized) > 0:
         idx = torch.empty((N, spec.C), dtype=torch.uint8, device=dev)
-        enc_us = region_us(lambda i: mdn.encode(A, split, thr, idx_out=idx), stream, reps=5, warm=1)
+        enc_us = region_us(lambda i: mdn.encode(A, split, thr, idx_out=idx), stream, reps=10, warm=3)
         if spec.quantized:
-            acc_us = region_us(lambda i: mdn.lut_accumulate(idx, lut, scale, offset, y_out=y), stream, reps=5, warm=1)
+            acc_us = region_us(lambda i: mdn.lut_accumulate(idx, lut, scale, offset, y_out=y), stream, reps=10, warm=3)
         else:
-            acc_us = region_us(lambda i: mdn.lut_accumulate_f32(idx, lut, y_out=y), stream, reps=5, warm=1)
+            acc_us = region_us(lambda i: mdn.lut_accumulate_f32(idx, lut, y_out=y), stream, reps=10, warm=3)
         out.update({"encode_us": round(enc_us, 2), "accumulate_us": round(acc_us, 2),
                     "encode_hbm_frac": round((4 * spec.D + spec.C) * N / (enc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
         if onehot_product_route(spec, N):

@@ -1,5 +1,5 @@
-"""The one-hot product accumulate (int8 tables, C % 16 == 0, C <= 128, M % 4
-== 0, 16,384 rows and more) against the oracle: int32 sums and outputs
+"""The one-hot product accumulate (int8 tables, C % 16 == 0, 48 <= C <= 128,
+M % 4 == 0, M >= 128, 16,384 rows and more) against the oracle: int32 sums and outputs
 bit-exact.  The cases cover the two instantiations (64 and 128 staged
 codebooks), codebook counts that leave padded codebooks, column counts that
 leave a ragged last slice, row counts with a ragged last tile, codes of
@@ -45,11 +45,11 @@ def sample_rows(N, seed, n=512):
 CASES = [  # (N, C, M, max_shift, want_acc, -128 codes)
     (16384, 64, 512, 1, False, False),        # dense_hidden's table shape
     (16384 + 37, 64, 512, 6, True, True),     # one group at its widest, ragged last tile
-    (16500, 16, 100, 3, True, False),         # 48 padded codebooks, ragged last slice
-    (17000, 48, 12, 0, False, True),          # one slice narrower than a column block
+    (16500, 48, 160, 3, True, False),         # 16 padded codebooks, ragged last slice
+    (17000, 48, 128, 0, False, True),         # one slice exactly
     (16411, 80, 132, 7, True, False),         # 128 staged codebooks (48 padded), two shift groups
-    (16384, 128, 64, 13, True, True),         # two groups, the second at its widest
-    (16390, 32, 4, 2, True, False),           # four columns
+    (16384, 128, 128, 13, True, True),        # two groups, the second at its widest
+    (16390, 64, 132, 2, True, False),         # a last slice of four columns
     (18000, 96, 200, 16, False, False),       # three shift groups
     (40000, 128, 1000, 1, True, False),       # wide_layer's codebooks, sampled rows
 ]
