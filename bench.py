@@ -508,9 +508,17 @@ def main():
         enc_us = region_us_(lambda i: split_calls[i % 2]())
         acc_us = region_us_(lambda i: acc_call())
         result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
-        if not headline:
-            # the accumulate of the two-phase workloads is bound by LDS reads:
-            # N C M lookups of 2 bytes (int8 tables, staged as 16-bit
+        if not headline and onehot_product_route(spec, N):
+            # the one-hot int8 product on the matrix cores: N x 16 C x M
+            # multiply-adds against the dense int8 peak
+            macs = N * 16 * spec.C * spec.M
+            tops = 2 * macs / (acc_us * 1e-6) / 1e12
+            result["context"]["accumulate_mfma_roofline"] = {
+                "bound": "mfma", "achieved": round(tops, 1), "peak": I8_MFMA_PEAK_TOPS, "unit": "TOP/s",
+                "frac": round(tops / I8_MFMA_PEAK_TOPS, 4), "macs": macs}
+        elif not headline:
+            # the accumulate of the other two-phase workloads is bound by LDS
+            # reads: N C M lookups of 2 bytes (int8 tables, staged as 16-bit
             # entries) or 4 bytes (fp32), against 256 B/clk/CU x 256 CUs x
             # 2.4 GHz
             lds_bytes = N * spec.C * spec.M * (2 if spec.quantized else 4)

@@ -657,12 +657,13 @@ int two_phase(const Shape& s, uint8_t* idx, hipStream_t stream) {
 // as encode + the one-hot product, through an index array: measured on 1M
 // rows of 512 columns of A with 64 codebooks, 0.84 against 1.05 ms at 512
 // output columns, 0.62 against 0.94 at 256, 0.51 against 0.89 at 128 (the
-// encode alone is 0.37 ms).
+// encode alone is 0.37 ms).  Not for a row softmax, which the row-streaming
+// kernel fuses and the two-phase path runs as a pass of its own.
 constexpr int kTwoPhaseMinCols = 128;
 bool two_phase_faster(const Shape& s) {
   FArgs f;
   int blocks;
-  return s.M >= kTwoPhaseMinCols && macc_shape(s) && plan_fenc(s, &f, &blocks, nullptr, 0);
+  return s.act != 3 && s.M >= kTwoPhaseMinCols && macc_shape(s) && plan_fenc(s, &f, &blocks, nullptr, 0);
 }
 
 // Whether a fused call runs as one launch (the gather-fused kernel, or the

@@ -231,7 +231,20 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   // tile's as soon as the last product step that reads it has been issued
   mu32x2 ixc[2][C16];
   const uint32_t oh_base = (uint32_t)(uintptr_t)s_oh;
-  const bool plain = a.y && !a.acc && a.act == 0 && col0 + W <= M;   // uniform
+  const bool plain = a.y && !a.acc && col0 + W <= M;   // uniform
+  // the layer output of 4 consecutive columns from slice column lc: bias,
+  // then ReLU (act 2)
+  auto layer_out = [&](mf32x4 z, int lc) -> mf32x4 {
+    if (a.act != 0) {
+      const mf32x4 bb = a.bias_lds ? *reinterpret_cast<const mlds_f32x4*>(s_bias + lc)
+                                   : (mf32x4){0.0f, 0.0f, 0.0f, 0.0f};
+      z = z + bb;
+      if (a.act == 2)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) z[e] = z[e] > 0.0f ? z[e] : 0.0f;
+    }
+    return z;
+  };
   int64_t t = wave;
   if (t < ntiles) load_idx(t, ixc);
   for (; t < ntiles; t += kMWaves) {
@@ -308,7 +321,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
     // ---------------- epilogue: lane (ml, h) holds row ml of each block and,
     // in registers 4 q .. 4 q + 3, columns 8 q + 4 h .. + 3 of each 32-column block
     if (plain && WB == 4) {
-      // y only, no layer output, every column of the slice exists, and 128
+      // y only (any layer output), every column of the slice exists, and 128
       // columns: a quad transpose first gives lane 4 a + u of the quad the
       // 16 bytes at columns 8 u + 4 h of rows 4 a .. 4 a + 3, so a store
       // instruction writes 8 whole 128-byte row segments (16 bytes per lane),
@@ -327,16 +340,17 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
             for (int e = 0; e < 4; ++e)
               x[q][e] = __float_as_int(__builtin_fmaf((float)acc[rb][cb][4 * q + e], step, bias32));
           mquad_transpose(x, lane);   // x[k]: columns 8 (ml % 4) + 4 h .. + 3 of row rowq + k
+          const int lc = 32 * cb + 8 * (ml & 3) + 4 * h;
 #pragma unroll
           for (int k = 0; k < 4; ++k)
             if (rowq + k < r1)
-              __builtin_nontemporal_store(
-                  x[k], reinterpret_cast<mi32x4*>(a.y + (rowq + k) * M + col0 + 32 * cb + 8 * (ml & 3) + 4 * h));
+              __builtin_nontemporal_store(layer_out(__builtin_bit_cast(mf32x4, x[k]), lc),
+                                          reinterpret_cast<mf32x4*>(a.y + (rowq + k) * M + col0 + lc));
         }
       }
       continue;
     }
-    if (plain) {   // y only, no layer output, every column of the slice exists
+    if (plain) {   // y only (any layer output), every column of the slice exists
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
         const int64_t row = r0 + t * kMTileRows + 32 * rb + ml;
@@ -349,7 +363,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
             mf32x4 z;
 #pragma unroll
             for (int e = 0; e < 4; ++e) z[e] = __builtin_fmaf((float)acc[rb][cb][4 * q + e], step, bias32);
-            yr[(32 * cb + 8 * q) / 4] = z;
+            yr[(32 * cb + 8 * q) / 4] = layer_out(z, 32 * cb + 8 * q + 4 * h);
           }
       }
       continue;

@@ -123,8 +123,9 @@ def test_accumulate_avg_replays(orc):
 
 @pytest.mark.parametrize("name,N", [("dense_hidden", 16411), ("encode_heavy_f32", 4173)])
 def test_two_phase_row_kernels_replay(orc, name, N):
-    """Row counts large enough for the row-uniform accumulate (int8 table:
-    dense_hidden; fp32 table: encode_heavy_f32), captured with a caller index
+    """Row counts large enough for the large-table accumulates (int8 table:
+    dense_hidden, the one-hot product on the matrix cores; fp32 table:
+    encode_heavy_f32, the row-uniform kernel), captured with a caller index
     buffer and replayed with new inputs."""
     p = W.make(name, N=N)
     rng = np.random.default_rng(N + 3)
