@@ -25,16 +25,21 @@
 // operand of one product (32 columns x 32 K values: two codebooks, one per
 // half-wavefront) are one 16-byte read.  Each wavefront then takes tiles of
 // 64 rows (two 32-row blocks) of the workgroup's row range independently (no
-// barrier after the prologue): per pair of codebooks it builds the one-hot
-// operand of its rows in registers from their index bytes (loaded a tile
-// ahead), reads WB table operands, and issues 2 WB products.  The product's
-// K order inside an operand is the hardware's, but the same for both
-// operands, so the byte a lane places at a position of the table operand and
-// the byte it places at that position of the one-hot operand always belong
-// to the same (codebook, prototype).  Results come out with the rows across
-// the lanes and 4 consecutive columns per group of 4 registers: 16-byte
-// stores, y = fmaf(float(acc), 2^e_min, bias32) (the offsets' double sum,
-// codebooks ascending, rounded once), then the layer output's bias and ReLU.
+// barrier after the prologue): per pair of codebooks it reads the one-hot
+// operands of its two row blocks from a 2 KB LDS table of the 8 possible
+// one-hot rows (entries 2^0 .. 2^6, and zero), at the entry of each row's
+// index byte, reads WB table operands, all one step ahead, and issues 2 WB
+// products.  Index rows come in 8-byte chunks, each reloaded with the next
+// tile's as soon as its last product step has been issued.  The product's K
+// order inside an operand is the hardware's, but the same for both operands,
+// so the byte a lane places at a position of the table operand and the byte
+// it places at that position of the one-hot operand always belong to the same
+// (codebook, prototype).  Results come out with the rows across the lanes and
+// 4 consecutive columns per group of 4 registers; y = fmaf(float(acc),
+// 2^e_min, bias32) (the offsets' double sum, codebooks ascending, rounded
+// once), then the layer output's bias and ReLU, and 16-byte stores (for
+// 128-column slices after a quad transpose, so that each store instruction
+// writes whole 128-byte row segments).
 //
 // Workgroups are numbered so that the slices of one row group run on one XCD,
 // or on as few as the group's slices fill (block b runs on XCD b % 8): the
