@@ -13,6 +13,15 @@
 // group first, with the sums shifted left by 7 between groups: a table whose
 // shifts are all below 7 (the common case) takes one pass.
 //
+// Sparse products.  A one-hot operand has at most one nonzero in every group
+// of 4 consecutive K values, so it is 2:4 sparse, and the sparse product
+// v_smfmac_i32_32x32x64_i8 covers 64 K values (4 codebooks) in about the time
+// of one 32-value dense product: the one-hot operand goes as the compressed
+// sparse operand (two stored values and their 2-bit positions per group,
+// built in registers from the index bytes), the table as the dense one.  The
+// dense form (one-hot entries read from a small LDS table) stays as the
+// instantiation with SP = false.
+//
 // Why the matrix cores: summed by gathers, each lookup reads 2 bytes of LDS
 // (a 16-bit field per column), and on layers with hundreds of output columns
 // the LDS, not HBM, sets the time.  The product does 16 times the arithmetic
@@ -54,6 +63,7 @@ namespace mdn {
 namespace {
 
 typedef int32_t mi32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t mi32x8 __attribute__((ext_vector_type(8)));
 typedef int32_t mi32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t mu32x2 __attribute__((ext_vector_type(2)));
 typedef float mf32x4 __attribute__((ext_vector_type(4)));
@@ -102,11 +112,44 @@ __device__ __forceinline__ void mquad_transpose(mi32x4 (&x)[4], int lane) {
     }
 }
 
+// 4 x 4 transpose of dwords over the four lanes of every quad: dword e of
+// lane u on entry is dword u of lane e on return (the same two stages)
+__device__ __forceinline__ void mquad_transpose_dw(mi32x4& x, int lane) {
+  const int b0 = lane & 1, b1 = (lane >> 1) & 1;
+  mi32x4 z;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int v = __builtin_amdgcn_mov_dpp(x[e ^ 1], 0xB1, 0xf, 0xf, false);
+    z[e] = b0 == (e & 1) ? x[e] : v;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int v = __builtin_amdgcn_mov_dpp(z[e ^ 2], 0x4E, 0xf, 0xf, false);
+    x[e] = b1 == ((e >> 1) & 1) ? z[e] : v;
+  }
+}
+
+// One codebook's half of a 2:4-compressed one-hot operand: 16 prototypes in
+// groups of 4, two stored values per group, each with a 2-bit position.  The
+// group x / 4 holding prototype x stores (v, 0) at positions (x % 4, x % 4 +
+// 1 mod 4); the other groups store (0, 0) at positions (0, 1).  Writes the
+// codebook's two dwords of compressed values and xors its 16 position bits
+// (starting from 0x4 per group) into ix, at bit 16 k.
+__device__ __forceinline__ void msparse_half(uint32_t x, uint32_t v, int k, int& lo, int& hi, int& ix) {
+  x &= 15u;
+  const uint32_t b = x >> 2;
+  const uint64_t p = (uint64_t)v << (16 * b);
+  lo = (int)(uint32_t)p;
+  hi = (int)(uint32_t)(p >> 32);
+  const uint32_t d = (0x070A0D00u >> (8 * (x & 3u))) & 0xffu;   // position bits ^ 0x4 for x % 4 = 0..3
+  ix ^= (int)(d << (16 * k + 4 * b));
+}
+
 }  // namespace
 
 // C16: codebooks in units of 16 (padded codebooks have one-hot entries 0);
 // WB: 32-column blocks per wavefront (W = 32 WB columns per slice)
-template <int C16, int WB>
+template <int C16, int WB, bool SP>
 __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   constexpr int W = 32 * WB;
   constexpr int CP = 16 * C16;                 // staged codebooks
@@ -206,7 +249,11 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   for (int u = tid; u < ngroups * CP; u += kMWaves * 64) {
     const int g = u / CP, c = u % CP;
     const int sh = s_sh[c];
-    s_val[u] = (sh >= 0 && sh / kMGroupBits == g) ? (uint8_t)(sh - kMGroupBits * g) : (uint8_t)kMGroupBits;
+    const bool in = sh >= 0 && sh / kMGroupBits == g;
+    if (SP)   // the one-hot entry itself
+      s_val[u] = in ? (uint8_t)(1u << (sh - kMGroupBits * g)) : (uint8_t)0;
+    else      // the row of the one-hot table
+      s_val[u] = in ? (uint8_t)(sh - kMGroupBits * g) : (uint8_t)kMGroupBits;
   }
   __syncthreads();
   const float step = __builtin_ldexpf(1.0f, emin);
@@ -215,7 +262,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   // ---------------- row tiles
   const int h = lane >> 5;    // half-wavefront: codebook 16 j + 8 h + i of the pair
   const int ml = lane & 31;   // table operand: column; one-hot operand and results: row
-  const uint32_t lane_tab = (uint32_t)(uintptr_t)(s_tab + (8 * h * W + ml) * 16);
+  const uint32_t lane_tab = (uint32_t)(uintptr_t)(s_tab + ((SP ? h : 8 * h) * W + ml) * 16);
   const int cvalid = (C + 15) >> 4;   // index chunks of 16 codebooks that exist
   const int64_t ntiles = (r1 - r0 + kMTileRows - 1) / kMTileRows;
 
@@ -276,6 +323,60 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int j = 0; j < C16; ++j) asm volatile("" : "+v"(ixc[rb][j]));
+      if constexpr (SP) {
+        // sparse product step s (j = s / 4, i = s % 4) covers codebooks
+        // 16 j + 2 i + {0, 1, 8, 9}: the lane's one-hot operand (row ml)
+        // holds 16 j + 8 h + 2 i + k in groups 4 k .. 4 k + 3 (k = 0, 1);
+        // its table operand (column ml) holds 16 j + 2 i + h in bytes 0-15
+        // and 16 j + 8 + 2 i + h in bytes 16-31.  Table operands are read one
+        // step ahead; the compressed one-hot operands are built in registers.
+        auto load_tab = [&](auto sc, mi32x8 (&Bt)[WB]) {
+          constexpr int st = decltype(sc)::value;
+          constexpr int j = st / 4, i = st % 4;
+#pragma unroll
+          for (int cb = 0; cb < WB; ++cb) {
+            const mi32x4 lo = *reinterpret_cast<const mlds_i32x4*>((const mlds_t*)(uintptr_t)lane_tab +
+                                                                   ((16 * j + 2 * i) * W + 32 * cb) * 16);
+            const mi32x4 hi = *reinterpret_cast<const mlds_i32x4*>((const mlds_t*)(uintptr_t)lane_tab +
+                                                                   ((16 * j + 8 + 2 * i) * W + 32 * cb) * 16);
+            Bt[cb] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          }
+        };
+        mi32x8 Ta[WB], Tb[WB];
+        load_tab(std::integral_constant<int, 0>{}, Ta);
+        mfor([&](auto sc) {
+          constexpr int st = decltype(sc)::value;
+          constexpr int j = st / 4, i = st % 4;
+          mi32x8(&cur)[WB] = (st & 1) ? Tb : Ta;
+          mi32x8(&nxt)[WB] = (st & 1) ? Ta : Tb;
+          if constexpr (st + 1 < 4 * C16) load_tab(std::integral_constant<int, st + 1>{}, nxt);
+          // bytes 2 i, 2 i + 1 of the chunk: dword i / 2, bits 16 (i % 2) ..
+          const uint32_t vw = vv[j][i >> 1] >> (16 * (i & 1));
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb) {
+            const uint32_t xw = ixc[rb][j][i >> 1] >> (16 * (i & 1));
+            int a0, a1, a2, a3, ix = 0x44444444;
+            msparse_half(xw, vw & 0xffu, 0, a0, a1, ix);
+            msparse_half(xw >> 8, (vw >> 8) & 0xffu, 1, a2, a3, ix);
+            const mi32x4 A = {a0, a1, a2, a3};
+#pragma unroll
+            for (int cb = 0; cb < WB; ++cb)
+              acc[rb][cb] = __builtin_amdgcn_smfmac_i32_32x32x64_i8(A, cur[cb], acc[rb][cb], ix, 0, 0);
+          }
+          if constexpr (st % 4 == 3) {
+            if (g == 0 && more && j < cvalid) {   // (as below)
+#pragma unroll
+              for (int rb = 0; rb < 2; ++rb) {
+                int64_t row = r0 + (t + kMWaves) * kMTileRows + 32 * rb + ml;
+                row = row < N ? row : N - 1;
+                ixc[rb][j] = *reinterpret_cast<const mu32x2*>(a.idx + row * C + 8 * h + 16 * j);
+              }
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }, std::make_integer_sequence<int, 4 * C16>{});
+        continue;
+      }
       // operands of product step s (codebooks 16 j + i and + 8: j = s / 8,
       // i = s % 8), read one step ahead of the products that use them
       auto load_ops = [&](auto sc, mi32x4 (&At)[WB], mi32x4 (&Bt)[2]) {
@@ -323,6 +424,59 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
       }, std::make_integer_sequence<int, 8 * C16>{});
     }
 
+    if constexpr (SP) {
+      // ---------------- epilogue of the sparse products: lane (ml, h)
+      // holds column ml of each 32 x 32 block, rows 8 q + 4 h .. + 3 in
+      // registers 4 q .. 4 q + 3
+      if (plain) {
+        // a dword transpose over each quad of lanes gives lane 4 a + u row
+        // 8 q + 4 h + u, columns 4 a .. 4 a + 3: a store instruction writes
+        // 8 whole 128-byte row segments, as streaming stores
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < WB; ++cb) {
+            const int lc = 32 * cb + 4 * (ml >> 2);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              mi32x4 x;
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                x[e] = __float_as_int(__builtin_fmaf((float)acc[rb][cb][4 * q + e], step, bias32));
+              mquad_transpose_dw(x, lane);
+              const int64_t row = r0 + t * kMTileRows + 32 * rb + 8 * q + 4 * h + (ml & 3);
+              if (row < r1)
+                __builtin_nontemporal_store(layer_out(__builtin_bit_cast(mf32x4, x), lc),
+                                            reinterpret_cast<mf32x4*>(a.y + row * M + col0 + lc));
+            }
+          }
+        continue;
+      }
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < WB; ++cb) {
+          const int lc = 32 * cb + ml;
+          if (col0 + lc >= M) continue;
+          const float bb = a.act != 0 && a.bias_lds ? s_bias[lc] : 0.0f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int64_t row = r0 + t * kMTileRows + 32 * rb + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (row >= r1) continue;
+            const int sv = acc[rb][cb][r];
+            if (a.y) {
+              float z = __builtin_fmaf((float)sv, step, bias32);
+              if (a.act != 0) {
+                z = z + bb;
+                if (a.act == 2) z = z > 0.0f ? z : 0.0f;
+              }
+              a.y[row * M + col0 + lc] = z;
+            }
+            if (a.acc) a.acc[row * M + col0 + lc] = sv;
+          }
+        }
+      continue;
+    }
     // ---------------- epilogue: lane (ml, h) holds row ml of each block and,
     // in registers 4 q .. 4 q + 3, columns 8 q + 4 h .. + 3 of each 32-column block
     if (plain && WB == 4) {
@@ -406,16 +560,20 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
 
 int macc_width(int C) { return C <= 64 ? 128 : 64; }
 
+constexpr bool kMSparse = true;   // the 2:4-sparse products (else the dense ones)
+
 hipError_t launch_macc(const MArgs& m, int blocks, hipStream_t stream) {
-  const void* fn = m.C <= 64 ? reinterpret_cast<const void*>(&macc_kernel<4, 4>)
-                             : reinterpret_cast<const void*>(&macc_kernel<8, 2>);
+  const void* fn = m.C <= 64 ? reinterpret_cast<const void*>(&macc_kernel<4, 4, kMSparse>)
+                             : reinterpret_cast<const void*>(&macc_kernel<8, 2, kMSparse>);
   hipError_t err = hipSuccess;
   launch_prepare(fn, kMWaves * 64, m.lds_total, &err);
   if (err != hipSuccess) return err;
   if (m.C <= 64)
-    hipLaunchKernelGGL((macc_kernel<4, 4>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total, stream, m);
+    hipLaunchKernelGGL((macc_kernel<4, 4, kMSparse>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total,
+                       stream, m);
   else
-    hipLaunchKernelGGL((macc_kernel<8, 2>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total, stream, m);
+    hipLaunchKernelGGL((macc_kernel<8, 2, kMSparse>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total,
+                       stream, m);
   return hipGetLastError();
 }
 
