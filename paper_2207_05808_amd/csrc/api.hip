@@ -549,6 +549,7 @@ bool plan_macc(const Shape& s, MArgs* m, int* blocks_out) {
   if (groups < 1) groups = 1;
   a.xcd_map = (groups * a.nslices) % 8 == 0;
   a.rows_per_group = round_up64((s.N + groups - 1) / groups, 64);
+  if (a.rows_per_group * s.M * 4 >= (1ll << 31)) return false;   // a group's outputs: 32-bit store offsets
   int off = (s.C <= 64 ? 64 : 128) * W * 16;   // the transposed table slice
   auto take = [&](int bytes) { const int o = off; off += round_up(bytes, 16); return o; };
   const int cp = s.C <= 64 ? 64 : 128;

@@ -79,6 +79,7 @@ typedef __attribute__((address_space(3))) mf32x4 mlds_f32x4;
 constexpr int kMWaves = 8;      // wavefronts per workgroup
 constexpr int kMTileRows = 64;  // rows per wavefront tile: two blocks of 32
 constexpr int kMGroupBits = 7;  // one-hot entries 2^0 .. 2^6 fit int8
+constexpr int kMBufDword3 = 0x00020000;   // raw, unswizzled buffer descriptor (gfx9 family)
 static_assert(30 / 7 + 1 <= kMaccGroups, "shifts up to 30 (clamped, as everywhere) in whole groups of 7");
 
 __device__ __forceinline__ int muni(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -428,8 +429,39 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
       // ---------------- epilogue of the sparse products: lane (ml, h)
       // holds column ml of each 32 x 32 block, rows 8 q + 4 h .. + 3 in
       // registers 4 q .. 4 q + 3
+      if (plain && r0 + (t + 1) * kMTileRows <= r1) {
+        // every row of the tile exists: dword stores, each writing two whole
+        // 128-byte row segments (lanes 0-31 one row, 32-63 another), with no
+        // vector work for addresses (the row offsets are scalar offsets of a
+        // buffer store; the host keeps a group's outputs below 2^31 bytes),
+        // as streaming stores (aux 2: nt).  Against the transposed 16-byte
+        // stores below: 0.46 against 0.48 ms on a 1M x 512 output.
+        const __amdgpu_buffer_rsrc_t yrs =
+            __builtin_amdgcn_make_buffer_rsrc(a.y + r0 * M, 0, (int)((r1 - r0) * M * 4), kMBufDword3);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < WB; ++cb) {
+            const int lc = 32 * cb + ml;
+            const float bb = a.act != 0 && a.bias_lds ? s_bias[lc] : 0.0f;
+            const int voff = (int)(((t * kMTileRows + 32 * rb + 4 * h) * (int64_t)M + col0 + lc) * 4);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              float z = __builtin_fmaf((float)acc[rb][cb][r], step, bias32);
+              if (a.act != 0) {
+                z = z + bb;
+                if (a.act == 2) z = z > 0.0f ? z : 0.0f;
+              }
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z), yrs, voff,
+                                                    __builtin_amdgcn_readfirstlane((8 * (r >> 2) + (r & 3)) * M * 4),
+                                                    2);
+            }
+          }
+        continue;
+      }
       if (plain) {
-        // a dword transpose over each quad of lanes gives lane 4 a + u row
+        // (the last tile of a group, rows past its end skipped) a dword
+        // transpose over each quad of lanes gives lane 4 a + u row
         // 8 q + 4 h + u, columns 4 a .. 4 a + 3: a store instruction writes
         // 8 whole 128-byte row segments, as streaming stores
 #pragma unroll
