@@ -557,7 +557,6 @@ bool plan_macc(const Shape& s, MArgs* m, int* blocks_out) {
   a.off_sh = take(4 * cp);
   a.off_misc = take(16);
   a.off_bias = take(4 * W);
-  a.off_oh = take(8 * 16 * 16);   // one-hot operands: 8 rows of 16 entries
   a.lds_total = off;
   if (off > kLdsBytes) return false;
   *m = a;

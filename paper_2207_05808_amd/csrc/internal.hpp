@@ -190,7 +190,7 @@ struct MArgs {
   int C, M, act;          // act: 0 none, 1 bias, 2 bias + ReLU (a softmax runs as a second pass)
   int bias_lds;           // column biases staged in LDS (act != 0 and col_bias given)
   int nslices, xcd_map;
-  int off_val, off_sh, off_misc, off_bias, off_oh, lds_total;   // LDS byte offsets (the table slice at 0)
+  int off_val, off_sh, off_misc, off_bias, lds_total;   // LDS byte offsets (the table slice at 0)
 };
 constexpr int kMaccGroups = 5;   // one-hot shift groups of 7 for shifts up to 30
 int macc_width(int C);

@@ -6,49 +6,40 @@
 // of the selected table rows).  For int8 tables in block floating point the
 // exact integer sum is acc = sum_c 2^sh_c q_c[idx_c] with sh_c = e_c - e_min;
 // with the one-hot entry of codebook c set to 2^sh_c instead of 1, acc is one
-// int8 x int8 -> int32 product over K = 16 C, which v_mfma_i32_32x32x32_i8
-// computes exactly (int32 wraps only past the documented bound, and every
-// partial sum obeys the same bound).  One-hot entries must fit int8, so the
-// codebooks are taken in shift groups of width 7 (2^0 .. 2^6), the highest
-// group first, with the sums shifted left by 7 between groups: a table whose
-// shifts are all below 7 (the common case) takes one pass.
+// int8 x int8 -> int32 product over K = 16 C, which the matrix cores compute
+// exactly (int32 wraps only past the documented bound, and every partial sum
+// obeys the same bound).  One-hot entries must fit int8, so the codebooks
+// are taken in shift groups of width 7 (2^0 .. 2^6), the highest group
+// first, with the sums shifted left by 7 between groups: a table whose shifts
+// are all below 7 (the common case) takes one pass.
 //
 // Sparse products.  A one-hot operand has at most one nonzero in every group
 // of 4 consecutive K values, so it is 2:4 sparse, and the sparse product
 // v_smfmac_i32_32x32x64_i8 covers 64 K values (4 codebooks) in about the time
 // of one 32-value dense product: the one-hot operand goes as the compressed
 // sparse operand (two stored values and their 2-bit positions per group,
-// built in registers from the index bytes), the table as the dense one.  The
-// dense form (one-hot entries read from a small LDS table) stays as the
-// instantiation with SP = false.
+// built in registers from the index bytes), the table as the dense one.
 //
 // Why the matrix cores: summed by gathers, each lookup reads 2 bytes of LDS
 // (a 16-bit field per column), and on layers with hundreds of output columns
-// the LDS, not HBM, sets the time.  The product does 16 times the arithmetic
-// of the gathers but on units that are otherwise idle, and reads the table
-// from LDS once per 64 rows: the kernel is left bound by its output stores.
+// the LDS, not HBM, sets the time.  The products do 8 times the arithmetic of
+// the gathers but on units that are otherwise idle, and read the table from
+// LDS once per 64 rows.
 //
 // Layout.  A workgroup (8 wavefronts) owns one column slice of W = 32 WB
 // columns for its lifetime, staged once into LDS transposed, as [codebook]
-// [column][16 prototypes] bytes: the 16 bytes a lane passes as the table
-// operand of one product (32 columns x 32 K values: two codebooks, one per
-// half-wavefront) are one 16-byte read.  Each wavefront then takes tiles of
-// 64 rows (two 32-row blocks) of the workgroup's row range independently (no
-// barrier after the prologue): per pair of codebooks it reads the one-hot
-// operands of its two row blocks from a 2 KB LDS table of the 8 possible
-// one-hot rows (entries 2^0 .. 2^6, and zero), at the entry of each row's
-// index byte, reads WB table operands, all one step ahead, and issues 2 WB
-// products.  Index rows come in 8-byte chunks, each reloaded with the next
-// tile's as soon as its last product step has been issued.  The product's K
-// order inside an operand is the hardware's, but the same for both operands,
-// so the byte a lane places at a position of the table operand and the byte
-// it places at that position of the one-hot operand always belong to the same
-// (codebook, prototype).  Results come out with the rows across the lanes and
-// 4 consecutive columns per group of 4 registers; y = fmaf(float(acc),
-// 2^e_min, bias32) (the offsets' double sum, codebooks ascending, rounded
-// once), then the layer output's bias and ReLU, and 16-byte stores (for
-// 128-column slices after a quad transpose, so that each store instruction
-// writes whole 128-byte row segments).
+// [column][16 prototypes] bytes, so the table operand of a product (32
+// columns x 64 K values) is two 16-byte reads per lane.  Each wavefront takes
+// tiles of 64 rows (two 32-row blocks) of the workgroup's row range
+// independently (no barrier after the prologue): per 4 codebooks it reads WB
+// table operands one step ahead, builds the compressed one-hot operands of
+// its two row blocks, and issues 2 WB products.  Index rows come in 8-byte
+// chunks, each reloaded with the next tile's as soon as its last product step
+// has been issued.  Results come out with the columns across the lanes and
+// the rows in registers; y = fmaf(float(acc), 2^e_min, bias32) (the offsets'
+// double sum, codebooks ascending, rounded once), then the layer output's
+// bias and ReLU, and dword streaming stores, each writing two whole 128-byte
+// row segments.
 //
 // Workgroups are numbered so that the slices of one row group run on one XCD,
 // or on as few as the group's slices fill (block b runs on XCD b % 8): the
@@ -90,29 +81,6 @@ __device__ __forceinline__ void mfor(F&& f, std::integer_sequence<int, I...>) {
   (f(std::integral_constant<int, I>{}), ...);
 }
 
-// 4 x 4 transpose of 16-byte elements over the four lanes of every quad:
-// element k of lane u (its position in the quad) on entry is element u of
-// lane k on return (two exchange stages: partner u ^ 1, then u ^ 2; a DPP
-// move and a select each)
-__device__ __forceinline__ void mquad_transpose(mi32x4 (&x)[4], int lane) {
-  const int b0 = lane & 1, b1 = (lane >> 1) & 1;
-  mi32x4 z[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int v = __builtin_amdgcn_mov_dpp(x[k ^ 1][e], 0xB1, 0xf, 0xf, false);   // quad_perm [1, 0, 3, 2]
-      z[k][e] = b0 == (k & 1) ? x[k][e] : v;
-    }
-#pragma unroll
-  for (int k = 0; k < 4; ++k)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int v = __builtin_amdgcn_mov_dpp(z[k ^ 2][e], 0x4E, 0xf, 0xf, false);   // quad_perm [2, 3, 0, 1]
-      x[k][e] = b1 == ((k >> 1) & 1) ? z[k][e] : v;
-    }
-}
-
 // 4 x 4 transpose of dwords over the four lanes of every quad: dword e of
 // lane u on entry is dword u of lane e on return (the same two stages)
 __device__ __forceinline__ void mquad_transpose_dw(mi32x4& x, int lane) {
@@ -150,7 +118,7 @@ __device__ __forceinline__ void msparse_half(uint32_t x, uint32_t v, int k, int&
 
 // C16: codebooks in units of 16 (padded codebooks have one-hot entries 0);
 // WB: 32-column blocks per wavefront (W = 32 WB columns per slice)
-template <int C16, int WB, bool SP>
+template <int C16, int WB>
 __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   constexpr int W = 32 * WB;
   constexpr int CP = 16 * C16;                 // staged codebooks
@@ -160,7 +128,6 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   mlds_i32* s_sh = reinterpret_cast<mlds_i32*>(s_tab + a.off_sh);      // [CP] shifts (-1: padding)
   mlds_i32* s_misc = reinterpret_cast<mlds_i32*>(s_tab + a.off_misc);  // bias32 bits, e_min, max shift
   mlds_f32* s_bias = reinterpret_cast<mlds_f32*>(s_tab + a.off_bias);  // [W] column biases of the slice
-  mlds_u32* s_oh = reinterpret_cast<mlds_u32*>(s_tab + a.off_oh);      // [8][16][16 bytes] one-hot operands
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -240,21 +207,12 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   __syncthreads();
   const int maxsh = muni(s_misc[2]);
   const int ngroups = maxsh / kMGroupBits + 1;
-  // the one-hot operands: row r < 7, entry x has byte x = 2^r (the others
-  // 0); row 7 is all zero.  Per shift group g, codebook c takes row sh_c - 7 g
-  // when its shift is in the group, else row 7.
-  for (int u = tid; u < 8 * 16 * 4; u += kMWaves * 64) {
-    const int r = u >> 6, x = (u >> 2) & 15, dw = u & 3;
-    s_oh[u] = (r < kMGroupBits && (x >> 2) == dw) ? (1u << r) << (8 * (x & 3)) : 0u;
-  }
   for (int u = tid; u < ngroups * CP; u += kMWaves * 64) {
     const int g = u / CP, c = u % CP;
     const int sh = s_sh[c];
-    const bool in = sh >= 0 && sh / kMGroupBits == g;
-    if (SP)   // the one-hot entry itself
-      s_val[u] = in ? (uint8_t)(1u << (sh - kMGroupBits * g)) : (uint8_t)0;
-    else      // the row of the one-hot table
-      s_val[u] = in ? (uint8_t)(sh - kMGroupBits * g) : (uint8_t)kMGroupBits;
+    // the one-hot entry of codebook c in shift group g: 2^(sh_c - 7 g) when
+    // its shift is in the group, else 0
+    s_val[u] = (sh >= 0 && sh / kMGroupBits == g) ? (uint8_t)(1u << (sh - kMGroupBits * g)) : (uint8_t)0;
   }
   __syncthreads();
   const float step = __builtin_ldexpf(1.0f, emin);
@@ -263,7 +221,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   // ---------------- row tiles
   const int h = lane >> 5;    // half-wavefront: codebook 16 j + 8 h + i of the pair
   const int ml = lane & 31;   // table operand: column; one-hot operand and results: row
-  const uint32_t lane_tab = (uint32_t)(uintptr_t)(s_tab + ((SP ? h : 8 * h) * W + ml) * 16);
+  const uint32_t lane_tab = (uint32_t)(uintptr_t)(s_tab + (h * W + ml) * 16);
   const int cvalid = (C + 15) >> 4;   // index chunks of 16 codebooks that exist
   const int64_t ntiles = (r1 - r0 + kMTileRows - 1) / kMTileRows;
 
@@ -283,7 +241,6 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   // index chunks of the current tile; chunk j is reloaded with the next
   // tile's as soon as the last product step that reads it has been issued
   mu32x2 ixc[2][C16];
-  const uint32_t oh_base = (uint32_t)(uintptr_t)s_oh;
   const bool plain = a.y && !a.acc && col0 + W <= M;   // uniform
   // the layer output of 4 consecutive columns from slice column lc: bias,
   // then ReLU (act 2)
@@ -324,7 +281,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int j = 0; j < C16; ++j) asm volatile("" : "+v"(ixc[rb][j]));
-      if constexpr (SP) {
+      {
         // sparse product step s (j = s / 4, i = s % 4) covers codebooks
         // 16 j + 2 i + {0, 1, 8, 9}: the lane's one-hot operand (row ml)
         // holds 16 j + 8 h + 2 i + k in groups 4 k .. 4 k + 3 (k = 0, 1);
@@ -376,56 +333,10 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
           }
           __builtin_amdgcn_sched_barrier(0);
         }, std::make_integer_sequence<int, 4 * C16>{});
-        continue;
       }
-      // operands of product step s (codebooks 16 j + i and + 8: j = s / 8,
-      // i = s % 8), read one step ahead of the products that use them
-      auto load_ops = [&](auto sc, mi32x4 (&At)[WB], mi32x4 (&Bt)[2]) {
-        constexpr int st = decltype(sc)::value;
-        constexpr int j = st / 8, i = st % 8;
-#pragma unroll
-        for (int cb = 0; cb < WB; ++cb)
-          At[cb] = *reinterpret_cast<const mlds_i32x4*>((const mlds_t*)(uintptr_t)lane_tab +
-                                                        ((16 * j + i) * W + 32 * cb) * 16);
-        const uint32_t vb = oh_base + (((vv[j][i >> 2] >> (8 * (i & 3))) & 0xffu) << 8);
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-          const uint32_t x = (ixc[rb][j][i >> 2] >> (8 * (i & 3))) & 15u;
-          Bt[rb] = *reinterpret_cast<const mlds_i32x4*>((const mlds_t*)(uintptr_t)(vb + (x << 4)));
-        }
-      };
-      mi32x4 Ta[WB], Tb[WB], Ba[2], Bb[2];
-      load_ops(std::integral_constant<int, 0>{}, Ta, Ba);
-      mfor([&](auto sc) {
-        constexpr int st = decltype(sc)::value;
-        mi32x4(&cur)[WB] = (st & 1) ? Tb : Ta;
-        mi32x4(&nxt)[WB] = (st & 1) ? Ta : Tb;
-        mi32x4(&bcur)[2] = (st & 1) ? Bb : Ba;
-        mi32x4(&bnxt)[2] = (st & 1) ? Ba : Bb;
-        if constexpr (st + 1 < 8 * C16) load_ops(std::integral_constant<int, st + 1>{}, nxt, bnxt);
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-          for (int cb = 0; cb < WB; ++cb)
-            acc[rb][cb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(cur[cb], bcur[rb], acc[rb][cb], 0, 0, 0);
-        if constexpr (st % 8 == 7) {
-          // chunk st / 8 has been read for the last time in this pass: in
-          // the last pass, start loading the next tile's
-          constexpr int j = st / 8;
-          if (g == 0 && more && j < cvalid) {
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-              int64_t row = r0 + (t + kMWaves) * kMTileRows + 32 * rb + ml;
-              row = row < N ? row : N - 1;
-              ixc[rb][j] = *reinterpret_cast<const mu32x2*>(a.idx + row * C + 8 * h + 16 * j);
-            }
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }, std::make_integer_sequence<int, 8 * C16>{});
     }
 
-    if constexpr (SP) {
+    {
       // ---------------- epilogue of the sparse products: lane (ml, h)
       // holds column ml of each 32 x 32 block, rows 8 q + 4 h .. + 3 in
       // registers 4 q .. 4 q + 3
@@ -507,104 +418,23 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
             if (a.acc) a.acc[row * M + col0 + lc] = sv;
           }
         }
-      continue;
-    }
-    // ---------------- epilogue: lane (ml, h) holds row ml of each block and,
-    // in registers 4 q .. 4 q + 3, columns 8 q + 4 h .. + 3 of each 32-column block
-    if (plain && WB == 4) {
-      // y only (any layer output), every column of the slice exists, and 128
-      // columns: a quad transpose first gives lane 4 a + u of the quad the
-      // 16 bytes at columns 8 u + 4 h of rows 4 a .. 4 a + 3, so a store
-      // instruction writes 8 whole 128-byte row segments (16 bytes per lane),
-      // as streaming stores (whole lines: nothing is read back).  Against
-      // 32-byte pieces of 32 rows per instruction: 0.50 against 0.58 ms on a
-      // 1M x 512 output.
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        const int64_t rowq = r0 + t * kMTileRows + 32 * rb + (ml & ~3);   // first row of the lane's quad
-#pragma unroll
-        for (int cb = 0; cb < WB; ++cb) {
-          mi32x4 x[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              x[q][e] = __float_as_int(__builtin_fmaf((float)acc[rb][cb][4 * q + e], step, bias32));
-          mquad_transpose(x, lane);   // x[k]: columns 8 (ml % 4) + 4 h .. + 3 of row rowq + k
-          const int lc = 32 * cb + 8 * (ml & 3) + 4 * h;
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            if (rowq + k < r1)
-              __builtin_nontemporal_store(layer_out(__builtin_bit_cast(mf32x4, x[k]), lc),
-                                          reinterpret_cast<mf32x4*>(a.y + (rowq + k) * M + col0 + lc));
-        }
-      }
-      continue;
-    }
-    if (plain) {   // y only (any layer output), every column of the slice exists
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        const int64_t row = r0 + t * kMTileRows + 32 * rb + ml;
-        if (row >= r1) continue;
-        mf32x4* yr = reinterpret_cast<mf32x4*>(a.y + row * M + col0 + 4 * h);
-#pragma unroll
-        for (int cb = 0; cb < WB; ++cb)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            mf32x4 z;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) z[e] = __builtin_fmaf((float)acc[rb][cb][4 * q + e], step, bias32);
-            yr[(32 * cb + 8 * q) / 4] = layer_out(z, 32 * cb + 8 * q + 4 * h);
-          }
-      }
-      continue;
-    }
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      const int64_t row = r0 + t * kMTileRows + 32 * rb + ml;
-      if (row >= r1) continue;
-#pragma unroll
-      for (int cb = 0; cb < WB; ++cb)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int lc = 32 * cb + 8 * q + 4 * h;   // column within the slice
-          if (col0 + lc >= M) continue;             // (M % 4 == 0: groups of 4 are whole)
-          const int s0 = acc[rb][cb][4 * q], s1 = acc[rb][cb][4 * q + 1];
-          const int s2 = acc[rb][cb][4 * q + 2], s3 = acc[rb][cb][4 * q + 3];
-          if (a.y) {
-            mf32x4 z = {__builtin_fmaf((float)s0, step, bias32), __builtin_fmaf((float)s1, step, bias32),
-                        __builtin_fmaf((float)s2, step, bias32), __builtin_fmaf((float)s3, step, bias32)};
-            if (a.act != 0) {
-              const mf32x4 bb = a.bias_lds ? *reinterpret_cast<const mlds_f32x4*>(s_bias + lc)
-                                           : (mf32x4){0.0f, 0.0f, 0.0f, 0.0f};
-              z = z + bb;
-              if (a.act == 2)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) z[e] = z[e] > 0.0f ? z[e] : 0.0f;
-            }
-            *reinterpret_cast<mf32x4*>(a.y + row * M + col0 + lc) = z;
-          }
-          if (a.acc) *reinterpret_cast<mi32x4*>(a.acc + row * M + col0 + lc) = (mi32x4){s0, s1, s2, s3};
-        }
     }
   }
 }
 
 int macc_width(int C) { return C <= 64 ? 128 : 64; }
 
-constexpr bool kMSparse = true;   // the 2:4-sparse products (else the dense ones)
-
 hipError_t launch_macc(const MArgs& m, int blocks, hipStream_t stream) {
-  const void* fn = m.C <= 64 ? reinterpret_cast<const void*>(&macc_kernel<4, 4, kMSparse>)
-                             : reinterpret_cast<const void*>(&macc_kernel<8, 2, kMSparse>);
+  const void* fn = m.C <= 64 ? reinterpret_cast<const void*>(&macc_kernel<4, 4>)
+                             : reinterpret_cast<const void*>(&macc_kernel<8, 2>);
   hipError_t err = hipSuccess;
   launch_prepare(fn, kMWaves * 64, m.lds_total, &err);
   if (err != hipSuccess) return err;
   if (m.C <= 64)
-    hipLaunchKernelGGL((macc_kernel<4, 4, kMSparse>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total,
+    hipLaunchKernelGGL((macc_kernel<4, 4>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total,
                        stream, m);
   else
-    hipLaunchKernelGGL((macc_kernel<8, 2, kMSparse>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total,
+    hipLaunchKernelGGL((macc_kernel<8, 2>), dim3((unsigned)blocks), dim3(kMWaves * 64), m.lds_total,
                        stream, m);
   return hipGetLastError();
 }
