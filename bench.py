@@ -335,8 +335,9 @@ def workload_block(name, steps, warmup, sample_n=2048):
                     "encode_hbm_frac": round((4 * spec.D + spec.C) * N / (enc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
         if onehot_product_route(spec, N):
             # the one-hot int8 product on the matrix cores: N x 16 C x M
-            # multiply-adds against the dense int8 peak, and the output
-            # stores against the HBM peak
+            # multiply-adds (dense-equivalent: the kernel issues them as 2:4
+            # sparse products) against the dense int8 peak, never the sparse
+            # one, and the output stores against the HBM peak
             macs = N * 16 * spec.C * spec.M
             out.update({"accumulate_route": "one-hot int8 product (matrix cores)",
                         "accumulate_mfma_frac": round(2 * macs / (acc_us * 1e-6) / 1e12 / I8_MFMA_PEAK_TOPS, 4),
@@ -510,7 +511,8 @@ def main():
         result["context"] = {"encode_only_us": round(enc_us, 2), "accumulate_only_us": round(acc_us, 2)}
         if not headline and onehot_product_route(spec, N):
             # the one-hot int8 product on the matrix cores: N x 16 C x M
-            # multiply-adds against the dense int8 peak
+            # multiply-adds (dense-equivalent, issued as 2:4 sparse products)
+            # against the dense int8 peak
             macs = N * 16 * spec.C * spec.M
             tops = 2 * macs / (acc_us * 1e-6) / 1e12
             result["context"]["accumulate_mfma_roofline"] = {
