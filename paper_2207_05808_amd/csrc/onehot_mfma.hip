@@ -98,20 +98,25 @@ __device__ __forceinline__ void mquad_transpose_dw(mi32x4& x, int lane) {
   }
 }
 
-// One codebook's half of a 2:4-compressed one-hot operand: 16 prototypes in
+// The 2:4-compressed one-hot operand of a codebook: its 16 prototypes in
 // groups of 4, two stored values per group, each with a 2-bit position.  The
 // group x / 4 holding prototype x stores (v, 0) at positions (x % 4, x % 4 +
-// 1 mod 4); the other groups store (0, 0) at positions (0, 1).  Writes the
-// codebook's two dwords of compressed values and xors its 16 position bits
-// (starting from 0x4 per group) into ix, at bit 16 k.
-__device__ __forceinline__ void msparse_half(uint32_t x, uint32_t v, int k, int& lo, int& hi, int& ix) {
-  x &= 15u;
-  const uint32_t b = x >> 2;
-  const uint64_t p = (uint64_t)v << (16 * b);
-  lo = (int)(uint32_t)p;
-  hi = (int)(uint32_t)(p >> 32);
-  const uint32_t d = (0x070A0D00u >> (8 * (x & 3u))) & 0xffu;   // position bits ^ 0x4 for x % 4 = 0..3
-  ix ^= (int)(d << (16 * k + 4 * b));
+// 1 mod 4), the other groups (0, 0) at positions (0, 1).  So the stored
+// values are v at byte 2 (x / 4) of the codebook's 8 bytes, and the position
+// bits 0x4444 ^ (d(x % 4) << 4 (x / 4)), d = 0, 13, 10, 7 (the xor of 0x4
+// with the group's two positions).  For the 4 index bytes of w at once:
+// lo, hi = the low and high bytes of those 16 position bits (per byte of w),
+// sh16 = 16 (x / 4) per byte (the shift of v within the 8 bytes).  A byte
+// table of 0x44 ^ (d(x % 4) << 4 (x / 4 % 2)) for x % 8, looked up with
+// v_perm, gives the varying byte; the other byte is 0x44.
+__device__ __forceinline__ void msparse_fields(uint32_t w, uint32_t& lo, uint32_t& hi, uint32_t& sh16) {
+  constexpr uint32_t kT8lo = 0x434E4944u;   // x % 8 = 0..3: 0x44, 0x49, 0x4E, 0x43
+  constexpr uint32_t kT8hi = 0x34E49444u;   // x % 8 = 4..7: 0x44, 0x94, 0xE4, 0x34
+  const uint32_t t = __builtin_amdgcn_perm(kT8hi, kT8lo, w & 0x07070707u);
+  const uint32_t big = ((w >> 3) & 0x01010101u) * 0xffu;   // 0xff in the bytes with x >= 8
+  lo = (big & 0x44444444u) | (~big & t);
+  hi = (big & t) | (~big & 0x44444444u);
+  sh16 = (w << 2) & 0x30303030u;                          // 16 (x / 4) per byte
 }
 
 }  // namespace
@@ -308,15 +313,21 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
           mi32x8(&cur)[WB] = (st & 1) ? Tb : Ta;
           mi32x8(&nxt)[WB] = (st & 1) ? Ta : Tb;
           if constexpr (st + 1 < 4 * C16) load_tab(std::integral_constant<int, st + 1>{}, nxt);
-          // bytes 2 i, 2 i + 1 of the chunk: dword i / 2, bits 16 (i % 2) ..
+          // bytes 2 i, 2 i + 1 of the chunk: dword i / 2, bytes 2 (i % 2) and
+          // 2 (i % 2) + 1; the work on a whole dword (4 codebooks, two steps)
+          // is shared by its two steps
           const uint32_t vw = vv[j][i >> 1] >> (16 * (i & 1));
 #pragma unroll
           for (int rb = 0; rb < 2; ++rb) {
-            const uint32_t xw = ixc[rb][j][i >> 1] >> (16 * (i & 1));
-            int a0, a1, a2, a3, ix = 0x44444444;
-            msparse_half(xw, vw & 0xffu, 0, a0, a1, ix);
-            msparse_half(xw >> 8, (vw >> 8) & 0xffu, 1, a2, a3, ix);
-            const mi32x4 A = {a0, a1, a2, a3};
+            const uint32_t w = ixc[rb][j][i >> 1];
+            uint32_t lo, hi, sh16;
+            msparse_fields(w, lo, hi, sh16);
+            const int ix = (int)__builtin_amdgcn_perm(hi, lo, (i & 1) ? 0x07030602u : 0x05010400u);
+            const int p0 = 16 * (i & 1);   // bit offset of the step's first byte
+            const uint64_t q0 = (uint64_t)(vw & 0xffu) << ((sh16 >> p0) & 0xffu);
+            const uint64_t q1 = (uint64_t)((vw >> 8) & 0xffu) << ((sh16 >> (p0 + 8)) & 0xffu);
+            const mi32x4 A = {(int)(uint32_t)q0, (int)(uint32_t)(q0 >> 32), (int)(uint32_t)q1,
+                              (int)(uint32_t)(q1 >> 32)};
 #pragma unroll
             for (int cb = 0; cb < WB; ++cb)
               acc[rb][cb] = __builtin_amdgcn_smfmac_i32_32x32x64_i8(A, cur[cb], acc[rb][cb], ix, 0, 0);
