@@ -277,7 +277,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
           for (int cb = 0; cb < WB; ++cb) acc[rb][cb] <<= kMGroupBits;
       }
       const mlds_t* vrow = reinterpret_cast<const mlds_t*>(s_val) + g * CP + 8 * h;
-      mu32x2 vv[C16];   // one-hot rows of the lane's codebooks in this group
+      mu32x2 vv[C16];   // one-hot entries of the lane's codebooks in this group
 #pragma unroll
       for (int j = 0; j < C16; ++j) vv[j] = *reinterpret_cast<const mlds_u32x2*>(vrow + 16 * j);
       // (the index bytes opaque here: their extraction stays inside the group
@@ -333,7 +333,9 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
               acc[rb][cb] = __builtin_amdgcn_smfmac_i32_32x32x64_i8(A, cur[cb], acc[rb][cb], ix, 0, 0);
           }
           if constexpr (st % 4 == 3) {
-            if (g == 0 && more && j < cvalid) {   // (as below)
+            // chunk j has been read for the last time in this pass: in the
+            // last pass, start loading the next tile's
+            if (g == 0 && more && j < cvalid) {
 #pragma unroll
               for (int rb = 0; rb < 2; ++rb) {
                 int64_t row = r0 + (t + kMWaves) * kMTileRows + 32 * rb + ml;
