@@ -296,9 +296,10 @@ def _idx_out(idx_out, N, C):
 
 
 def matmul_index_bytes(A, C, M, f32=False, act=0) -> int:
-    """Device bytes the fused entry points need in idx_out for this A and
+    """Device bytes of idx_out the fused entry points use for this A and
     shape (maddness_matmul_index_bytes): 0 when the call runs as one launch,
-    else N * C."""
+    else N * C (the two-phase path; for the shapes that also have a slower
+    one-launch route, the faster one through the index array)."""
     N, D, lda = _rows(A)
     n = int(_lib.lib().maddness_matmul_index_bytes(_ptr(A), N, D, lda, C, M, 1 if f32 else 0, _act(act)))
     if n < 0:
@@ -307,10 +308,10 @@ def matmul_index_bytes(A, C, M, f32=False, act=0) -> int:
 
 
 def _index_array(idx_out, A, N, D, lda, C, M, f32, act, stream):
-    """idx_out when the caller gave one; else, when the call needs an index
-    array (the table does not fit the single-launch kernels), a new one from
-    torch's allocator, kept alive for `stream`; else None.  The library
-    itself never allocates."""
+    """idx_out when the caller gave one; else, when the call uses an index
+    array (the table does not fit the single-launch kernels, or two phases
+    through it are faster), a new one from torch's allocator, kept alive for
+    `stream`; else None.  The library itself never allocates."""
     if idx_out is not None:
         return idx_out
     n = int(_lib.lib().maddness_matmul_index_bytes(_ptr(A), N, D, lda, C, M, 1 if f32 else 0, int(act)))
