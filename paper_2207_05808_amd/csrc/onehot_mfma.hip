@@ -247,6 +247,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
   // tile's as soon as the last product step that reads it has been issued
   mu32x2 ixc[2][C16];
   const bool plain = a.y && !a.acc && col0 + W <= M;   // uniform
+  const bool whole = a.y && col0 + W <= M;               // (the int32 sums too, whole tiles only)
   // the layer output of 4 consecutive columns from slice column lc: bias,
   // then ReLU (act 2)
   auto layer_out = [&](mf32x4 z, int lc) -> mf32x4 {
@@ -353,7 +354,7 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
       // ---------------- epilogue of the sparse products: lane (ml, h)
       // holds column ml of each 32 x 32 block, rows 8 q + 4 h .. + 3 in
       // registers 4 q .. 4 q + 3
-      if (plain && r0 + (t + 1) * kMTileRows <= r1) {
+      if (whole && r0 + (t + 1) * kMTileRows <= r1) {
         // every row of the tile exists: dword stores, each writing two whole
         // 128-byte row segments (lanes 0-31 one row, 32-63 another), with no
         // vector work for addresses (the row offsets are scalar offsets of a
@@ -362,6 +363,8 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
         // stores below: 0.46 against 0.48 ms on a 1M x 512 output.
         const __amdgpu_buffer_rsrc_t yrs =
             __builtin_amdgcn_make_buffer_rsrc(a.y + r0 * M, 0, (int)((r1 - r0) * M * 4), kMBufDword3);
+        const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+            a.acc ? a.acc + r0 * M : nullptr, 0, a.acc ? (int)((r1 - r0) * M * 4) : 0, kMBufDword3);
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
@@ -376,9 +379,9 @@ __global__ void __launch_bounds__(kMWaves * 64) macc_kernel(const MArgs a) {
                 z = z + bb;
                 if (a.act == 2) z = z > 0.0f ? z : 0.0f;
               }
-              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z), yrs, voff,
-                                                    __builtin_amdgcn_readfirstlane((8 * (r >> 2) + (r & 3)) * M * 4),
-                                                    2);
+              const int soff = __builtin_amdgcn_readfirstlane((8 * (r >> 2) + (r & 3)) * M * 4);
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z), yrs, voff, soff, 2);
+              if (a.acc) __builtin_amdgcn_raw_buffer_store_b32((uint32_t)acc[rb][cb][r], ars, voff, soff, 2);
             }
           }
         continue;
